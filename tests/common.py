@@ -1,0 +1,78 @@
+"""Test helpers: oracle-side shard slicing and the parity tolerance.
+
+The oracle side slices the canonical tensors with the oracle's own
+apportionment; the HIP side (in ``gpu_common``) slices with the ranges the
+C library reports. Both draw from the same seeded generator.
+"""
+import numpy as np
+
+import oracle
+from synth import LayerDims, Workload
+from synth.gen import LayerInputs
+
+# Parity bar on fp16 outputs: max relative error 2e-2, element-wise, with the
+# denominator floored at 1% of the vector's largest magnitude so that entries
+# that are near zero by cancellation do not dominate.
+REL_TOL = 2e-2
+REL_FLOOR = 1e-2
+
+
+def max_rel_err(got, ref, floor=REL_FLOOR):
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    assert got.shape == ref.shape, (got.shape, ref.shape)
+    if got.size == 0:
+        return 0.0
+    if not np.all(np.isfinite(got)):
+        return float("inf")
+    scale = np.max(np.abs(ref), axis=-1, keepdims=True)
+    if np.any(scale == 0):
+        # an all-zero reference vector must be reproduced exactly
+        zero_rows = (scale == 0)[..., 0]
+        if np.any(got[zero_rows] != 0):
+            return float("inf")
+        scale = np.where(scale == 0, 1.0, scale)
+    denom = np.maximum(np.abs(ref), floor * scale)
+    return float(np.max(np.abs(got - ref) / denom))
+
+
+def oracle_ranges(wl: Workload, device=None):
+    d = wl.dims
+    return oracle.shard_ranges(d.n_heads, d.n_kv_heads, d.ffn, wl.fracs, wl.fracs,
+                               wl.device if device is None else device)
+
+
+def oracle_shard_weights(li: LayerInputs, r) -> oracle.ShardWeights:
+    d = li.wl.dims.head_dim
+    q0, q1 = r.q_head_begin * d, (r.q_head_begin + r.n_q_heads) * d
+    k0, k1 = r.kv_head_begin * d, (r.kv_head_begin + r.n_kv_heads) * d
+    c0, c1 = r.col_begin, r.col_begin + r.n_cols
+    return oracle.ShardWeights(
+        g_attn=li.g_attn(), wq=li.rows("wq", q0, q1), wk=li.rows("wk", k0, k1),
+        wv=li.rows("wv", k0, k1), wo=li.cols("wo", q0, q1), g_ffn=li.g_ffn(),
+        wg=li.rows("wg", c0, c1), wu=li.rows("wu", c0, c1), wd=li.cols("wd", c0, c1))
+
+
+def full_weights(li: LayerInputs) -> oracle.ShardWeights:
+    """The unsharded layer as a single shard."""
+    return oracle.ShardWeights(
+        g_attn=li.g_attn(), wq=li.full("wq"), wk=li.full("wk"), wv=li.full("wv"),
+        wo=li.full("wo"), g_ffn=li.g_ffn(), wg=li.full("wg"), wu=li.full("wu"),
+        wd=li.full("wd"))
+
+
+def oracle_decode(wl: Workload, li: LayerInputs, r, x, kc, vc, pos, peer_attn=None,
+                  peer_ffn=None, w=None):
+    d = wl.dims
+    w = w if w is not None else oracle_shard_weights(li, r)
+    return oracle.decode(w, r.n_q_heads, r.n_kv_heads, d.head_dim, d.rms_eps, d.rope_base,
+                         x, kc, vc, pos, peer_attn, peer_ffn)
+
+
+def tiny_workload(seed_id, hidden, n_heads, n_kv, head_dim, ffn, fracs, device, ctx,
+                  sigma=0.25, chunk=0):
+    return Workload(key=f"tiny{seed_id}", seed_id=seed_id, title="tiny test layer",
+                    dims=LayerDims(hidden=hidden, n_heads=n_heads, n_kv_heads=n_kv,
+                                   head_dim=head_dim, ffn=ffn),
+                    fracs=tuple(fracs), device=device, weight_sigma=sigma, ctx=ctx,
+                    chunk=chunk)
