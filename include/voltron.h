@@ -1,0 +1,221 @@
+/*
+ * voltron.h - C ABI of one device's share of an unevenly tensor-parallel
+ * decoder layer (Voltron, arXiv 2607.07046), on one AMD Instinct MI355X.
+ *
+ * What a shard is (paper Sec. 3.2.1, Fig. Motivation1(b)): under tensor
+ * parallelism the main device broadcasts a layer's input activation, every
+ * device computes its shard of the layer, and the results are aggregated on
+ * the main device, once per layer. Sec. 4.2.1 assigns shards to devices
+ * greedily by their performance, so shards are uneven. Here a shard is a
+ * contiguous range of KV groups (a KV head plus the query heads sharing it,
+ * Sec. 2.1 GQA) and a contiguous range of FFN columns. Its outputs are the
+ * two partial sums (after the output linear O and after the FFN down
+ * projection) that the aggregation would add up; the cross-device
+ * reduction itself is not part of this library.
+ *
+ * Layer (Sec. 2.1, Fig. Background1(a)) with the readings the paper leaves
+ * open: pre-norm RMSNorm; Q/K/V projections; rotary position embedding on
+ * adjacent pairs (2i, 2i+1) by angle pos * rope_base^(-2i/head_dim); the new
+ * token's K and V appended to the KV cache (Sec. 2.1, LLM Inference);
+ * scaled dot-product attention with scale 1/sqrt(head_dim) over positions
+ * 0..pos, query head j using KV head j / (n_heads / n_kv_heads); output
+ * linear O; residual; RMSNorm; SwiGLU FFN down(silu(gate) * up); residual.
+ * No biases.
+ *
+ * Conventions for every entry point:
+ *  - Numbers are fp16 (IEEE binary16) in device memory unless stated;
+ *    arithmetic accumulates in fp32.
+ *  - Matrices are row-major, canonical out x in; "ld" is the row stride in
+ *    elements. Every device pointer must be 16-byte aligned and every ld a
+ *    multiple of 8, else VT_ERR_ALIGN.
+ *  - The library never allocates device memory and never synchronises. All
+ *    buffers are owned by the caller. Work is enqueued on ``stream`` (a
+ *    hipStream_t; NULL is the default stream).
+ *  - Arguments are validated before anything is enqueued; on error nothing
+ *    is enqueued, no output and no ``kv->len`` changes, and
+ *    vt_last_error() (thread-local) describes the problem. Faults inside a
+ *    kernel surface at the caller's next synchronisation.
+ */
+#ifndef VOLTRON_H
+#define VOLTRON_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum vt_status {
+  VT_OK = 0,
+  VT_ERR_ARG = -1,          /* null pointer, bad dimension, fraction or flag */
+  VT_ERR_ALIGN = -2,        /* pointer not 16-byte aligned, or ld not a multiple of 8 */
+  VT_ERR_KV_FULL = -3,      /* the append would pass the cache capacity */
+  VT_ERR_POS = -4,          /* pos differs from kv->len */
+  VT_ERR_HIP = -5,          /* a HIP runtime call failed */
+  VT_ERR_UNSUPPORTED = -6,  /* shape outside what the kernels handle */
+  VT_ERR_WORKSPACE = -7     /* workspace missing or smaller than vt_workspace_size */
+} vt_status;
+
+/* Shape of the whole (unsharded) layer. head_dim must be 64 or 128;
+ * hidden a multiple of 8; n_heads a multiple of n_kv_heads. */
+typedef struct vt_layer_dims {
+  int32_t hidden;
+  int32_t n_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t ffn;
+  float rms_eps;
+  float rope_base;
+} vt_layer_dims;
+
+/* One device's shard: query heads [q_head_begin, +n_q_heads), KV heads
+ * [kv_head_begin, +n_kv_heads) (n_q_heads = n_kv_heads * group) and FFN
+ * columns [col_begin, +n_cols) of the layer. */
+typedef struct vt_shard_info {
+  int32_t q_head_begin;
+  int32_t n_q_heads;
+  int32_t kv_head_begin;
+  int32_t n_kv_heads;
+  int32_t col_begin;
+  int32_t n_cols;
+} vt_shard_info;
+
+typedef struct vt_shard_spec vt_shard_spec; /* opaque, host-only, immutable */
+
+/* Partition a layer over ``n_devices`` devices and describe ``device``'s
+ * share (paper Sec. 4.2.1: greedy, performance-proportional shards).
+ * head_frac[i] / col_frac[i] are device i's fractions of the KV groups and
+ * of the FFN columns: finite, >= 0, each array summing to 1 within 1e-9.
+ * Rounding: largest remainder. Device i gets floor(frac[i] * units) units
+ * (product in IEEE double), then the units still unassigned go one each to
+ * the devices with the largest fractional parts, the lower index first on
+ * ties; devices take contiguous ranges in index order. A device may get no
+ * heads or no columns; its partial sums are then zero.
+ * On success *out receives a spec to free with vt_shard_spec_destroy. */
+vt_status vt_shard_spec_create(const vt_layer_dims* dims, int32_t n_devices,
+                               const double* head_frac, const double* col_frac,
+                               int32_t device, vt_shard_spec** out);
+
+/* Copy the spec's layer shape and shard ranges out (either may be NULL). */
+vt_status vt_shard_spec_query(const vt_shard_spec* spec, vt_layer_dims* dims_out,
+                              vt_shard_info* info_out);
+
+void vt_shard_spec_destroy(vt_shard_spec* spec);
+
+/* The shard's weights, caller-owned device fp16, rows as described (shard
+ * rows / shard columns of the canonical layer tensors; the columns of wo
+ * and wd are the shard's query-head features and FFN columns). Each ld is
+ * the row stride in elements (>= row length, multiple of 8).
+ *   g_attn [hidden]                 RMSNorm gain before attention
+ *   wq [n_q_heads*head_dim][hidden]  wk, wv [n_kv_heads*head_dim][hidden]
+ *   wo [hidden][n_q_heads*head_dim]
+ *   g_ffn [hidden]                  RMSNorm gain before the FFN
+ *   wg, wu [n_cols][hidden]         gate and up projections
+ *   wd [hidden][n_cols]             down projection
+ * Pointers of a part the shard does not have (no heads / no columns) may be
+ * NULL. */
+typedef struct vt_layer_weights {
+  const void* g_attn;
+  const void* wq; int64_t ld_q;
+  const void* wk; int64_t ld_k;
+  const void* wv; int64_t ld_v;
+  const void* wo; int64_t ld_o;
+  const void* g_ffn;
+  const void* wg; int64_t ld_g;
+  const void* wu; int64_t ld_u;
+  const void* wd; int64_t ld_d;
+} vt_layer_weights;
+
+/* KV cache of the shard's KV heads for one layer: k and v are
+ * [n_kv_heads][capacity][head_dim] fp16, caller-owned. ``len`` is the number
+ * of positions filled (0..len-1); successful appends advance it on the host
+ * when the work is enqueued. Keys are stored after rotation. */
+typedef struct vt_kv_view {
+  void* k;
+  void* v;
+  int32_t capacity;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t len;
+} vt_kv_view;
+
+/* Activations of T tokens (T = 1 for decode), each [T][hidden] fp16:
+ *   x            in   layer input (the broadcast activation)
+ *   peer_attn    in   nullable; sum of the other devices' attention partials
+ *   peer_ffn     in   nullable; sum of the other devices' FFN partials
+ *   attn_partial out  Wo[:, shard heads] * attention output   (VT_ATTN)
+ *   h            out  x + attn_partial + peer_attn            (VT_ATTN)
+ *                in   FFN input when VT_FFN runs without VT_ATTN
+ *   ffn_partial  out  Wd[:, shard columns] * silu(gate) * up  (VT_FFN)
+ *   y            out  nullable; h + ffn_partial + peer_ffn     (VT_FFN)
+ * NULL peers count as zero. When both phases run, the FFN reads h as
+ * written (rounded to fp16). */
+typedef struct vt_layer_io {
+  const void* x;
+  const void* peer_attn;
+  const void* peer_ffn;
+  void* attn_partial;
+  void* h;
+  void* ffn_partial;
+  void* y;
+} vt_layer_io;
+
+/* Phase mask bits for vt_layer_decode / vt_layer_prefill_chunk. */
+#define VT_ATTN 1u          /* RMSNorm, QKV, RoPE, KV append, attention, O, h */
+#define VT_FFN 2u           /* RMSNorm, gate/up, SiLU-gate, down, y */
+#define VT_STAGED 0x100u    /* decode only: one kernel launch per stage instead
+                               of the single persistent kernel (same results
+                               up to fp32 rounding order, which is fixed) */
+
+/* Append n_tok tokens' keys and values at positions pos..pos+n_tok-1 of
+ * every KV head (paper Sec. 2.1, LLM Inference: the K and V of new tokens
+ * are accumulated into the KV cache). k, v: [n_tok][n_kv_heads][head_dim]
+ * fp16 device. A pure copy: the stored bytes equal the input bytes and no
+ * other byte of the cache changes. Requires pos == kv->len (VT_ERR_POS) and
+ * pos + n_tok <= capacity (VT_ERR_KV_FULL); then kv->len = pos + n_tok. */
+vt_status vt_kv_append(vt_kv_view* kv, const void* k, const void* v, int32_t n_tok,
+                       int32_t pos, void* stream);
+
+/* Bytes of device workspace that vt_layer_decode / vt_layer_prefill_chunk
+ * need for this shard with up to ``max_tokens`` tokens per chunk (1 for
+ * decode only) and ``max_ctx`` cached-plus-new positions. The workspace must
+ * be zero-filled once before its first use; the library leaves its
+ * synchronisation words zero after every call. One workspace must not be
+ * used by two calls that may run at the same time. */
+vt_status vt_workspace_size(const vt_shard_spec* spec, int32_t max_tokens,
+                            int32_t max_ctx, size_t* bytes);
+
+/* Batch-1 decode of one token at position ``pos`` through the shard
+ * (paper Sec. 2.1 LLM Inference, Sec. 3.2.1 TP shard). ``phases`` is
+ * VT_ATTN, VT_FFN or both, optionally with VT_STAGED. With VT_ATTN the
+ * token's rotated key and its value are appended at slot ``pos`` of every
+ * shard KV head (pos must equal kv->len and be < capacity; kv->len becomes
+ * pos + 1) and attention covers positions 0..pos. ``kv`` and ``pos`` are
+ * ignored without VT_ATTN. Outputs per vt_layer_io. */
+vt_status vt_layer_decode(const vt_shard_spec* spec, const vt_layer_weights* w,
+                          vt_kv_view* kv, const vt_layer_io* io, int32_t pos,
+                          uint32_t phases, void* ws, size_t ws_bytes, void* stream);
+
+/* Prefill of a chunk of n_tok tokens at positions pos0..pos0+n_tok-1 (paper
+ * Sec. 2.1: prompt tokens are processed in parallel). All n_tok keys and
+ * values are appended (pos0 must equal kv->len); token t attends to
+ * positions 0..pos0+t. Activations in io are [n_tok][hidden]. The
+ * projections run as fp16 matrix-core (MFMA) GEMMs with fp32 accumulation;
+ * their activation operands are rounded to fp16 first. */
+vt_status vt_layer_prefill_chunk(const vt_shard_spec* spec, const vt_layer_weights* w,
+                                 vt_kv_view* kv, const vt_layer_io* io, int32_t n_tok,
+                                 int32_t pos0, uint32_t phases, void* ws, size_t ws_bytes,
+                                 void* stream);
+
+/* Static text of a status code. */
+const char* vt_status_string(vt_status s);
+
+/* Detail of the last error on the calling thread ("" if none). */
+const char* vt_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* VOLTRON_H */

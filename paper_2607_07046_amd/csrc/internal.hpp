@@ -1,0 +1,32 @@
+// Host-side internals shared by the library's translation units.
+#pragma once
+
+#include <cstdarg>
+#include <cstdint>
+
+#include "voltron.h"
+
+struct vt_shard_spec {
+  vt_layer_dims dims;
+  vt_shard_info info;
+};
+
+namespace vt {
+
+// Record a formatted detail for vt_last_error() and return ``s``.
+vt_status fail(vt_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+void clear_error();
+
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Checks shared by the decode and prefill entry points.
+vt_status check_layer_dims(const vt_layer_dims& d);
+vt_status check_weights(const vt_shard_spec& s, const vt_layer_weights* w, bool attn, bool ffn);
+vt_status check_kv(const vt_shard_spec& s, const vt_kv_view* kv, int32_t pos, int32_t n_tok);
+
+}  // namespace vt
+
+namespace vt {
+size_t decode_workspace_bytes(const vt_shard_spec& s, int32_t max_ctx);
+size_t prefill_workspace_bytes(const vt_shard_spec& s, int32_t max_tokens, int32_t max_ctx);
+}  // namespace vt

@@ -1,0 +1,185 @@
+"""ctypes binding of libvoltron.so (the C ABI declared in include/voltron.h).
+
+Argument marshalling only: every step of the decoder-layer shard runs in the
+library's HIP kernels. Functions keep the C names; a non-OK status raises
+``VoltronError`` carrying the status and ``vt_last_error()``. Device buffers
+are passed as integer addresses (e.g. ``tensor.data_ptr()``), streams as
+``hipStream_t`` handles (e.g. ``torch.cuda.current_stream().cuda_stream``).
+"""
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libvoltron.so")
+
+VT_OK = 0
+VT_ERR_ARG = -1
+VT_ERR_ALIGN = -2
+VT_ERR_KV_FULL = -3
+VT_ERR_POS = -4
+VT_ERR_HIP = -5
+VT_ERR_UNSUPPORTED = -6
+VT_ERR_WORKSPACE = -7
+
+VT_ATTN = 1
+VT_FFN = 2
+VT_STAGED = 0x100
+
+# every symbol include/voltron.h declares
+EXPORTS = ("vt_shard_spec_create", "vt_shard_spec_query", "vt_shard_spec_destroy",
+           "vt_kv_append", "vt_workspace_size", "vt_layer_decode", "vt_layer_prefill_chunk",
+           "vt_status_string", "vt_last_error")
+
+
+class VoltronError(RuntimeError):
+    def __init__(self, status, detail):
+        super().__init__(f"{status_string(status)} ({status}): {detail}")
+        self.status = status
+        self.detail = detail
+
+
+class vt_layer_dims(ctypes.Structure):
+    _fields_ = [("hidden", ctypes.c_int32), ("n_heads", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("ffn", ctypes.c_int32), ("rms_eps", ctypes.c_float),
+                ("rope_base", ctypes.c_float)]
+
+
+class vt_shard_info(ctypes.Structure):
+    _fields_ = [("q_head_begin", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
+                ("kv_head_begin", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("col_begin", ctypes.c_int32), ("n_cols", ctypes.c_int32)]
+
+
+class vt_layer_weights(ctypes.Structure):
+    _fields_ = [("g_attn", ctypes.c_void_p),
+                ("wq", ctypes.c_void_p), ("ld_q", ctypes.c_int64),
+                ("wk", ctypes.c_void_p), ("ld_k", ctypes.c_int64),
+                ("wv", ctypes.c_void_p), ("ld_v", ctypes.c_int64),
+                ("wo", ctypes.c_void_p), ("ld_o", ctypes.c_int64),
+                ("g_ffn", ctypes.c_void_p),
+                ("wg", ctypes.c_void_p), ("ld_g", ctypes.c_int64),
+                ("wu", ctypes.c_void_p), ("ld_u", ctypes.c_int64),
+                ("wd", ctypes.c_void_p), ("ld_d", ctypes.c_int64)]
+
+
+class vt_kv_view(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p),
+                ("capacity", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("len", ctypes.c_int32)]
+
+
+class vt_layer_io(ctypes.Structure):
+    _fields_ = [("x", ctypes.c_void_p), ("peer_attn", ctypes.c_void_p),
+                ("peer_ffn", ctypes.c_void_p), ("attn_partial", ctypes.c_void_p),
+                ("h", ctypes.c_void_p), ("ffn_partial", ctypes.c_void_p),
+                ("y", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def load_library(path=None):
+    """Load the HIP library; raises if it has not been built."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise RuntimeError(f"{p} is missing: build it with paper_2607_07046_amd.build.build()")
+    lib = ctypes.CDLL(p)
+    P, I32, U32, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint32, ctypes.c_size_t
+    lib.vt_shard_spec_create.argtypes = [ctypes.POINTER(vt_layer_dims), I32,
+                                         ctypes.POINTER(ctypes.c_double),
+                                         ctypes.POINTER(ctypes.c_double), I32,
+                                         ctypes.POINTER(P)]
+    lib.vt_shard_spec_query.argtypes = [P, ctypes.POINTER(vt_layer_dims),
+                                        ctypes.POINTER(vt_shard_info)]
+    lib.vt_shard_spec_destroy.argtypes = [P]
+    lib.vt_shard_spec_destroy.restype = None
+    lib.vt_kv_append.argtypes = [ctypes.POINTER(vt_kv_view), P, P, I32, I32, P]
+    lib.vt_workspace_size.argtypes = [P, I32, I32, ctypes.POINTER(SZ)]
+    lib.vt_layer_decode.argtypes = [P, ctypes.POINTER(vt_layer_weights),
+                                    ctypes.POINTER(vt_kv_view), ctypes.POINTER(vt_layer_io),
+                                    I32, U32, P, SZ, P]
+    lib.vt_layer_prefill_chunk.argtypes = [P, ctypes.POINTER(vt_layer_weights),
+                                           ctypes.POINTER(vt_kv_view),
+                                           ctypes.POINTER(vt_layer_io), I32, I32, U32, P, SZ, P]
+    for name in ("vt_shard_spec_create", "vt_shard_spec_query", "vt_kv_append",
+                 "vt_workspace_size", "vt_layer_decode", "vt_layer_prefill_chunk"):
+        getattr(lib, name).restype = ctypes.c_int
+    lib.vt_status_string.argtypes = [ctypes.c_int]
+    lib.vt_status_string.restype = ctypes.c_char_p
+    lib.vt_last_error.argtypes = []
+    lib.vt_last_error.restype = ctypes.c_char_p
+    if path is None:
+        _lib = lib
+    return lib
+
+
+def status_string(status):
+    return load_library().vt_status_string(status).decode()
+
+
+def vt_last_error():
+    return load_library().vt_last_error().decode()
+
+
+def _check(status):
+    if status != VT_OK:
+        raise VoltronError(status, vt_last_error())
+
+
+class ShardSpec:
+    """Owns a vt_shard_spec handle."""
+
+    def __init__(self, handle):
+        self.handle = handle
+
+    def __del__(self):
+        if getattr(self, "handle", None) and _lib is not None:
+            _lib.vt_shard_spec_destroy(self.handle)
+            self.handle = None
+
+
+def vt_shard_spec_create(dims: vt_layer_dims, head_frac, col_frac, device) -> ShardSpec:
+    n = len(head_frac)
+    if len(col_frac) != n:
+        raise ValueError("head and column fractions must have the same length")
+    hf = (ctypes.c_double * max(n, 1))(*head_frac)
+    cf = (ctypes.c_double * max(n, 1))(*col_frac)
+    out = ctypes.c_void_p()
+    _check(load_library().vt_shard_spec_create(ctypes.byref(dims), n, hf, cf, device,
+                                               ctypes.byref(out)))
+    return ShardSpec(out.value)
+
+
+def vt_shard_spec_query(spec: ShardSpec):
+    d, i = vt_layer_dims(), vt_shard_info()
+    _check(load_library().vt_shard_spec_query(spec.handle, ctypes.byref(d), ctypes.byref(i)))
+    return d, i
+
+
+def vt_workspace_size(spec: ShardSpec, max_tokens: int, max_ctx: int) -> int:
+    n = ctypes.c_size_t()
+    _check(load_library().vt_workspace_size(spec.handle, max_tokens, max_ctx, ctypes.byref(n)))
+    return n.value
+
+
+def vt_kv_append(kv: vt_kv_view, k, v, n_tok, pos, stream=None):
+    _check(load_library().vt_kv_append(ctypes.byref(kv), k, v, n_tok, pos, stream))
+
+
+def vt_layer_decode(spec: ShardSpec, w: vt_layer_weights, kv, io: vt_layer_io, pos, phases,
+                    ws, ws_bytes, stream=None):
+    _check(load_library().vt_layer_decode(spec.handle, ctypes.byref(w),
+                                          ctypes.byref(kv) if kv is not None else None,
+                                          ctypes.byref(io), pos, phases, ws, ws_bytes, stream))
+
+
+def vt_layer_prefill_chunk(spec: ShardSpec, w: vt_layer_weights, kv, io: vt_layer_io, n_tok,
+                           pos0, phases, ws, ws_bytes, stream=None):
+    _check(load_library().vt_layer_prefill_chunk(spec.handle, ctypes.byref(w),
+                                                 ctypes.byref(kv) if kv is not None else None,
+                                                 ctypes.byref(io), n_tok, pos0, phases, ws,
+                                                 ws_bytes, stream))

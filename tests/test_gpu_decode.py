@@ -1,0 +1,222 @@
+"""GPU parity of batch-1 decode (vt_layer_decode, vt_kv_append) against the
+fp64 oracle, through the C ABI.
+
+Bar: every fp16 output vector within max relative error 2e-2 (element-wise,
+denominator floored at 1% of the vector's largest magnitude); KV indexing
+bit-exact (the appended slot holds the new key/value, every other cache
+byte keeps its sentinel or context value, ``len`` advances by one).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_07046_amd import voltron as vt
+from synth import get
+from synth.gen import LayerInputs
+from tests.common import (REL_TOL, full_weights, max_rel_err, oracle_ranges,
+                          oracle_shard_weights, tiny_workload)
+from tests.gpu_common import SENTINEL, GpuShard
+
+pytestmark = pytest.mark.gpu
+
+BOTH = vt.VT_ATTN | vt.VT_FFN
+MODES = {"fused": 0, "staged": vt.VT_STAGED}
+
+_cache = {}
+
+
+def oracle_case(wl, device=None, li=None):
+    """Oracle inputs/outputs of the workload's shard at its decode position."""
+    key = (wl.key, wl.seed_id, device)
+    if key not in _cache:
+        li = li or LayerInputs(wl)
+        r = oracle_ranges(wl, device)
+        w = oracle_shard_weights(li, r)
+        kc, vc = li.kv_context_heads(r.kv_head_begin, r.kv_head_begin + r.n_kv_heads)
+        d = wl.dims
+        x = li.x(0)
+        ref = oracle.decode(w, r.n_q_heads, r.n_kv_heads, d.head_dim, d.rms_eps, d.rope_base,
+                            x, kc, vc, wl.ctx)
+        _cache[key] = (li, r, x, ref)
+    return _cache[key]
+
+
+def check_outputs(got, ref, keys=("p_attn", "h", "p_ffn", "y")):
+    errs = {k: max_rel_err(got[k], ref[k]) for k in keys}
+    bad = {k: e for k, e in errs.items() if not e <= REL_TOL}
+    assert not bad, f"relative errors {errs}"
+    return errs
+
+
+def check_kv(gs, ref, pos, k_before, v_before):
+    kc, vc = gs.cache()
+    assert gs.kv.len == pos + 1
+    # every slot except pos is byte-identical to before
+    mask = np.ones(kc.shape[1], bool)
+    mask[pos] = False
+    assert np.array_equal(kc[:, mask], k_before[:, mask])
+    assert np.array_equal(vc[:, mask], v_before[:, mask])
+    k_new = kc[:, pos].view(np.float16).astype(np.float64)
+    v_new = vc[:, pos].view(np.float16).astype(np.float64)
+    for g in range(k_new.shape[0]):
+        assert max_rel_err(k_new[g], ref["k_new"][g]) <= REL_TOL
+        assert max_rel_err(v_new[g], ref["v_new"][g]) <= REL_TOL
+
+
+@pytest.mark.parametrize("mode", MODES)
+@pytest.mark.parametrize("key", ["tiny", "7b", "70b_gqa"])
+def test_decode_matches_oracle(key, mode):
+    wl = get(key)
+    li, r, x, ref = oracle_case(wl)
+    gs = GpuShard(wl, li=li)
+    assert (gs.info.n_q_heads, gs.info.n_kv_heads, gs.info.n_cols) == \
+           (r.n_q_heads, r.n_kv_heads, r.n_cols)
+    k0, v0 = gs.cache()
+    got = gs.decode(x, wl.ctx, BOTH | MODES[mode])
+    errs = check_outputs(got, ref)
+    print(key, mode, errs)
+    check_kv(gs, ref, wl.ctx, k0, v0)
+    assert not np.any(gs.sync_words()), "synchronisation words not cleared"
+
+
+def test_fused_staged_and_repeat_are_bitwise_equal():
+    wl = get("7b")
+    li, r, x, ref = oracle_case(wl)
+    outs = []
+    for flags in (0, vt.VT_STAGED, 0):
+        gs = GpuShard(wl, li=li)
+        outs.append((gs.decode(x, wl.ctx, BOTH | flags), gs.cache()))
+    for o, c in outs[1:]:
+        for k in ("p_attn", "h", "p_ffn", "y"):
+            assert np.array_equal(o[k], outs[0][0][k]), k
+        assert np.array_equal(c[0], outs[0][1][0]) and np.array_equal(c[1], outs[0][1][1])
+
+
+@pytest.mark.parametrize("key", ["tiny", "7b"])
+def test_all_shards_sum_to_unsharded_layer(key):
+    """Sec. 3.2.1: the aggregated partials of every shard are the layer."""
+    wl = get(key)
+    d = wl.dims
+    li = LayerInputs(wl)
+    x = li.x(0)
+    kc, vc = li.kv_context_heads(0, d.n_kv_heads)
+    full = oracle.decode(full_weights(li), d.n_heads, d.n_kv_heads, d.head_dim, d.rms_eps,
+                         d.rope_base, x, kc, vc, wl.ctx)
+    shards = [GpuShard(wl, device=s, li=li) for s in range(len(wl.fracs))]
+    parts = [gs.decode(x, wl.ctx, vt.VT_ATTN) for gs in shards]
+    sum_attn = np.sum([p["p_attn"] for p in parts], axis=0)
+    assert max_rel_err(sum_attn, full["p_attn"]) <= REL_TOL
+    # aggregation on the main device (host stand-in), then the FFN shards
+    h = (x.astype(np.float64) + sum_attn).astype(np.float16)
+    ffn = [gs.decode(None, phases=vt.VT_FFN, h_in=h) for gs in shards]
+    sum_ffn = np.sum([f["p_ffn"] for f in ffn], axis=0)
+    assert max_rel_err(sum_ffn, full["p_ffn"]) <= REL_TOL
+    # peer semantics: shard 0 given the others' partials produces the full h and y
+    peer_a = np.sum([p["p_attn"] for p in parts[1:]], axis=0).astype(np.float16)
+    peer_f = np.sum([f["p_ffn"] for f in ffn[1:]], axis=0).astype(np.float16)
+    gs0 = GpuShard(wl, device=0, li=li)
+    got = gs0.decode(x, wl.ctx, BOTH, peer_attn=peer_a, peer_ffn=peer_f)
+    assert max_rel_err(got["h"], full["h"]) <= REL_TOL
+    assert max_rel_err(got["y"], full["y"]) <= REL_TOL
+
+
+def test_consecutive_tokens_match_oracle_chain():
+    wl = get("tiny")
+    d = wl.dims
+    li = LayerInputs(wl)
+    r = oracle_ranges(wl)
+    w = oracle_shard_weights(li, r)
+    kc, vc = li.kv_context_heads(r.kv_head_begin, r.kv_head_begin + r.n_kv_heads)
+    kc, vc = kc.astype(np.float64), vc.astype(np.float64)
+    gs = GpuShard(wl, li=li, capacity=wl.ctx + 16)
+    for t in range(12):
+        pos = wl.ctx + t
+        x = li.x(t)
+        ref = oracle.decode(w, r.n_q_heads, r.n_kv_heads, d.head_dim, d.rms_eps, d.rope_base,
+                            x, kc, vc, pos)
+        got = gs.decode(x, pos, BOTH | (vt.VT_STAGED if t % 2 else 0))
+        check_outputs(got, ref)
+        kc = np.concatenate([kc, ref["k_new"][:, None]], axis=1)
+        vc = np.concatenate([vc, ref["v_new"][:, None]], axis=1)
+    assert gs.kv.len == wl.ctx + 12
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_empty_cache_and_last_slot(mode):
+    """pos = 0 (nothing cached) and an append into the last free slot."""
+    wl = tiny_workload(201, 256, 4, 2, 64, 300, (0.5, 0.5), 1, 0, sigma=0.05)
+    li, r, x, ref = oracle_case(wl)
+    gs = GpuShard(wl, li=li, capacity=1)
+    k0, v0 = gs.cache()
+    got = gs.decode(x, 0, BOTH | MODES[mode])
+    check_outputs(got, ref)
+    check_kv(gs, ref, 0, k0, v0)
+    with pytest.raises(vt.VoltronError) as e:
+        gs.decode(x, 1, BOTH)
+    assert e.value.status == vt.VT_ERR_KV_FULL
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_ragged_shapes_and_gqa_groups(mode):
+    """Odd column counts (ragged last piece), head_dim 64 with GQA group 4,
+    several attention chunks with a ragged last chunk."""
+    wl = tiny_workload(202, 1024, 16, 4, 64, 3000, (0.37, 0.33, 0.30), 2, 150, sigma=0.03)
+    li, r, x, ref = oracle_case(wl)
+    gs = GpuShard(wl, li=li)
+    assert gs.info.n_cols % 8 != 0
+    k0, v0 = gs.cache()
+    got = gs.decode(x, wl.ctx, BOTH | MODES[mode])
+    check_outputs(got, ref)
+    check_kv(gs, ref, wl.ctx, k0, v0)
+
+
+def test_empty_shard_outputs_zero_partials():
+    """A device that gets no heads and no columns (e.g. one whose share was
+    pruned away) contributes zero partials; h and y pass x and peers through."""
+    wl = tiny_workload(203, 512, 8, 8, 64, 1376, (1.0, 0.0), 1, 16, sigma=0.02)
+    li = LayerInputs(wl)
+    gs = GpuShard(wl, li=li)
+    assert gs.info.n_q_heads == 0 and gs.info.n_cols == 0
+    x = li.x(0)
+    pa, pf = li.peer("attn"), li.peer("ffn")
+    got = gs.decode(x, wl.ctx, BOTH, peer_attn=pa, peer_ffn=pf)
+    assert np.all(got["p_attn"] == 0) and np.all(got["p_ffn"] == 0)
+    h = (x.astype(np.float64) + pa.astype(np.float64)).astype(np.float16).astype(np.float64)
+    assert max_rel_err(got["h"], h) <= 1e-3
+    assert max_rel_err(got["y"], h + pf.astype(np.float64)) <= 1e-2
+
+
+def test_attn_only_then_ffn_only_equals_both():
+    wl = get("tiny")
+    li, r, x, ref = oracle_case(wl)
+    a = GpuShard(wl, li=li)
+    ga = a.decode(x, wl.ctx, vt.VT_ATTN)
+    gf = a.decode(None, phases=vt.VT_FFN, h_in=ga["h"].astype(np.float16))
+    b = GpuShard(wl, li=li)
+    gb = b.decode(x, wl.ctx, BOTH)
+    for k in ("p_attn", "h"):
+        assert np.array_equal(ga[k], gb[k]), k
+    for k in ("p_ffn", "y"):
+        assert np.array_equal(gf[k], gb[k]), k
+
+
+def test_kv_append_is_a_bit_exact_copy():
+    wl = tiny_workload(204, 512, 8, 4, 128, 64, (0.5, 0.5), 0, 0)
+    gs = GpuShard(wl, capacity=40, fill_ctx=False)
+    rng = np.random.default_rng(5)
+    nkv, d = gs.info.n_kv_heads, gs.dims.head_dim
+    written = np.full((nkv, 40, d), SENTINEL, np.int16), np.full((nkv, 40, d), SENTINEL, np.int16)
+    pos = 0
+    for n in (7, 1, 0, 13, 19):
+        bits_k = rng.integers(-2 ** 15, 2 ** 15, size=(n, nkv, d), dtype=np.int16)
+        bits_v = rng.integers(-2 ** 15, 2 ** 15, size=(n, nkv, d), dtype=np.int16)
+        gs.append(bits_k.view(np.float16), bits_v.view(np.float16))
+        written[0][:, pos:pos + n] = np.transpose(bits_k, (1, 0, 2))
+        written[1][:, pos:pos + n] = np.transpose(bits_v, (1, 0, 2))
+        pos += n
+        assert gs.kv.len == pos
+        kc, vc = gs.cache()
+        assert np.array_equal(kc, written[0]) and np.array_equal(vc, written[1])
+    with pytest.raises(vt.VoltronError):
+        gs.append(np.zeros((1, nkv, d), np.float16), np.zeros((1, nkv, d), np.float16))

@@ -1,0 +1,187 @@
+"""Host-side checks of libvoltron.so that need no GPU.
+
+* the library loads and exports every symbol include/voltron.h declares;
+* vt_shard_spec_create reproduces the oracle's apportionment bit-exactly
+  (workload partitions and random fractions);
+* argument validation rejects bad input before anything is enqueued.
+"""
+import ctypes
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2607_07046_amd import voltron as vt
+from synth import WORKLOADS
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return vt.load_library()
+
+
+def test_exports_every_declared_symbol(lib):
+    with open(os.path.join(ROOT, "include", "voltron.h")) as f:
+        hdr = f.read()
+    declared = set(re.findall(r"^\s*(?:vt_status|void|const char\*)\s+(vt_\w+)\s*\(", hdr, re.M))
+    assert declared == set(vt.EXPORTS)
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+def _dims(wd):
+    return vt.vt_layer_dims(hidden=wd.hidden, n_heads=wd.n_heads, n_kv_heads=wd.n_kv_heads,
+                            head_dim=wd.head_dim, ffn=wd.ffn, rms_eps=wd.rms_eps,
+                            rope_base=wd.rope_base)
+
+
+@pytest.mark.parametrize("key", sorted(WORKLOADS))
+def test_spec_matches_oracle_on_workloads(lib, key):
+    wl = WORKLOADS[key]
+    for dev in range(len(wl.fracs)):
+        spec = vt.vt_shard_spec_create(_dims(wl.dims), wl.fracs, wl.fracs, dev)
+        _, info = vt.vt_shard_spec_query(spec)
+        r = oracle.shard_ranges(wl.dims.n_heads, wl.dims.n_kv_heads, wl.dims.ffn, wl.fracs,
+                                wl.fracs, dev)
+        got = (info.q_head_begin, info.n_q_heads, info.kv_head_begin, info.n_kv_heads,
+               info.col_begin, info.n_cols)
+        want = (r.q_head_begin, r.n_q_heads, r.kv_head_begin, r.n_kv_heads, r.col_begin,
+                r.n_cols)
+        assert got == want, (key, dev)
+
+
+def test_spec_matches_oracle_random_fractions(lib):
+    rng = np.random.default_rng(11)
+    for _ in range(400):
+        n = int(rng.integers(1, 9))
+        kv = int(rng.integers(1, 65))
+        group = int(rng.choice([1, 2, 4, 8]))
+        ffn = int(rng.integers(0, 60000))
+        hf = rng.random(n) * (rng.random(n) > 0.15)
+        cf = rng.random(n) * (rng.random(n) > 0.15)
+        if hf.sum() == 0 or cf.sum() == 0:
+            continue
+        hf, cf = list(hf / hf.sum()), list(cf / cf.sum())
+        if abs(math.fsum(hf) - 1) > 1e-9 or abs(math.fsum(cf) - 1) > 1e-9:
+            continue
+        dims = vt.vt_layer_dims(hidden=512, n_heads=kv * group, n_kv_heads=kv, head_dim=64,
+                                ffn=ffn, rms_eps=1e-5, rope_base=1e4)
+        for dev in range(n):
+            _, info = vt.vt_shard_spec_query(vt.vt_shard_spec_create(dims, hf, cf, dev))
+            r = oracle.shard_ranges(kv * group, kv, ffn, hf, cf, dev)
+            assert (info.kv_head_begin, info.n_kv_heads, info.col_begin, info.n_cols,
+                    info.q_head_begin, info.n_q_heads) == \
+                   (r.kv_head_begin, r.n_kv_heads, r.col_begin, r.n_cols, r.q_head_begin,
+                    r.n_q_heads)
+
+
+BAD_SPECS = [
+    (dict(), (0.5, 0.4), 0, vt.VT_ERR_ARG),                       # fractions sum 0.9
+    (dict(), (1.5, -0.5), 0, vt.VT_ERR_ARG),                      # negative fraction
+    (dict(), (float("nan"), 1.0), 0, vt.VT_ERR_ARG),
+    (dict(), (0.5, 0.5), 2, vt.VT_ERR_ARG),                       # device out of range
+    (dict(head_dim=96), (1.0,), 0, vt.VT_ERR_UNSUPPORTED),
+    (dict(n_heads=12, n_kv_heads=8), (1.0,), 0, vt.VT_ERR_ARG),   # heads not multiple of kv
+    (dict(hidden=500), (1.0,), 0, vt.VT_ERR_UNSUPPORTED),
+    (dict(hidden=0), (1.0,), 0, vt.VT_ERR_ARG),
+]
+
+
+@pytest.mark.parametrize("over,fr,dev,status", BAD_SPECS)
+def test_spec_rejects_bad_input(lib, over, fr, dev, status):
+    base = dict(hidden=512, n_heads=8, n_kv_heads=8, head_dim=64, ffn=1376, rms_eps=1e-5,
+                rope_base=1e4)
+    base.update(over)
+    with pytest.raises(vt.VoltronError) as e:
+        vt.vt_shard_spec_create(vt.vt_layer_dims(**base), fr, fr, dev)
+    assert e.value.status == status
+    assert vt.vt_last_error() != ""
+
+
+def _tiny_spec():
+    dims = vt.vt_layer_dims(hidden=512, n_heads=8, n_kv_heads=8, head_dim=64, ffn=1376,
+                            rms_eps=1e-5, rope_base=1e4)
+    return vt.vt_shard_spec_create(dims, (0.5, 0.5), (0.5, 0.5), 0)
+
+
+def _fake_weights(addr=1 << 20):
+    # addresses are never dereferenced: every case fails validation first
+    return vt.vt_layer_weights(g_attn=addr, wq=addr, ld_q=512, wk=addr, ld_k=512, wv=addr,
+                               ld_v=512, wo=addr, ld_o=256, g_ffn=addr, wg=addr, ld_g=512,
+                               wu=addr, ld_u=512, wd=addr, ld_d=688)
+
+
+def _fake_io(addr=1 << 20):
+    return vt.vt_layer_io(x=addr, peer_attn=None, peer_ffn=None, attn_partial=addr, h=addr,
+                          ffn_partial=addr, y=None)
+
+
+def test_decode_validation_errors(lib):
+    spec = _tiny_spec()
+    ws_need = vt.vt_workspace_size(spec, 1, 129)
+    assert ws_need > 0
+    A = 1 << 20
+    kv = vt.vt_kv_view(k=A, v=A, capacity=200, n_kv_heads=4, head_dim=64, len=128)
+
+    def call(w=None, kv_=kv, io=None, pos=128, phases=vt.VT_ATTN | vt.VT_FFN, ws=A,
+             wsb=ws_need):
+        with pytest.raises(vt.VoltronError) as e:
+            vt.vt_layer_decode(spec, w or _fake_weights(), kv_, io or _fake_io(), pos, phases,
+                               ws, wsb)
+        return e.value.status
+
+    assert call(pos=127) == vt.VT_ERR_POS
+    full = vt.vt_kv_view(k=A, v=A, capacity=128, n_kv_heads=4, head_dim=64, len=128)
+    assert call(kv_=full) == vt.VT_ERR_KV_FULL
+    assert call(wsb=ws_need - 1) == vt.VT_ERR_WORKSPACE
+    assert call(ws=None) == vt.VT_ERR_WORKSPACE
+    assert call(phases=0) == vt.VT_ERR_ARG
+    assert call(phases=4) == vt.VT_ERR_ARG
+    w = _fake_weights()
+    w.wq = A + 8
+    assert call(w=w) == vt.VT_ERR_ALIGN
+    w = _fake_weights()
+    w.ld_d = 690
+    assert call(w=w) == vt.VT_ERR_ALIGN
+    w = _fake_weights()
+    w.ld_o = 128
+    assert call(w=w) == vt.VT_ERR_ARG
+    w = _fake_weights()
+    w.wd = None
+    assert call(w=w) == vt.VT_ERR_ARG
+    io = _fake_io()
+    io.x = None
+    assert call(io=io) == vt.VT_ERR_ARG
+    io = _fake_io()
+    io.peer_attn = A + 2
+    assert call(io=io) == vt.VT_ERR_ALIGN
+    bad_kv = vt.vt_kv_view(k=A, v=A, capacity=200, n_kv_heads=3, head_dim=64, len=128)
+    assert call(kv_=bad_kv) == vt.VT_ERR_ARG
+    # KV length is untouched by failed calls
+    assert kv.len == 128
+
+
+def test_kv_append_validation_errors(lib):
+    A = 1 << 20
+    kv = vt.vt_kv_view(k=A, v=A, capacity=10, n_kv_heads=2, head_dim=128, len=4)
+    for (n, pos, status) in ((1, 3, vt.VT_ERR_POS), (7, 4, vt.VT_ERR_KV_FULL),
+                             (-1, 4, vt.VT_ERR_ARG)):
+        with pytest.raises(vt.VoltronError) as e:
+            vt.vt_kv_append(kv, A, A, n, pos)
+        assert e.value.status == status
+    with pytest.raises(vt.VoltronError) as e:
+        vt.vt_kv_append(kv, A + 4, A, 1, 4)
+    assert e.value.status == vt.VT_ERR_ALIGN
+    assert kv.len == 4
+    vt.vt_kv_append(kv, A, A, 0, 4)       # empty append: nothing enqueued
+    assert kv.len == 4
+
+
+def test_status_strings(lib):
+    for s in range(-7, 1):
+        assert vt.status_string(s) not in ("", "unknown status")
