@@ -10,14 +10,20 @@ import oracle
 from synth import LayerDims, Workload
 from synth.gen import LayerInputs
 
-# Parity bar on fp16 outputs: max relative error 2e-2, element-wise, with the
-# denominator floored at 1% of the vector's largest magnitude so that entries
-# that are near zero by cancellation do not dominate.
+# Parity bar on fp16 outputs (max relative error 2e-2). Element-wise relative
+# error, with each denominator floored at the root-mean-square of the
+# reference vector: |got_i - ref_i| / max(|ref_i|, rms(ref)). The floor is
+# needed because the error that fp16 activations at the sub-layer boundaries
+# (x, h, the partial sums) carry into a projection scales with the vector's
+# norm, not with each element, so elements near zero by cancellation would
+# otherwise dominate. A normwise bound ||got - ref|| / ||ref|| <= NORM_TOL
+# (an order of magnitude above fp16 rounding noise) also catches small
+# systematic slips such as one wrong column of a wide projection.
 REL_TOL = 2e-2
-REL_FLOOR = 1e-2
+NORM_TOL = 4e-3
 
 
-def max_rel_err(got, ref, floor=REL_FLOOR):
+def max_rel_err(got, ref):
     got = np.asarray(got, np.float64)
     ref = np.asarray(ref, np.float64)
     assert got.shape == ref.shape, (got.shape, ref.shape)
@@ -25,15 +31,31 @@ def max_rel_err(got, ref, floor=REL_FLOOR):
         return 0.0
     if not np.all(np.isfinite(got)):
         return float("inf")
-    scale = np.max(np.abs(ref), axis=-1, keepdims=True)
-    if np.any(scale == 0):
+    rms = np.sqrt(np.mean(ref * ref, axis=-1, keepdims=True))
+    if np.any(rms == 0):
         # an all-zero reference vector must be reproduced exactly
-        zero_rows = (scale == 0)[..., 0]
+        zero_rows = (rms == 0)[..., 0]
         if np.any(got[zero_rows] != 0):
             return float("inf")
-        scale = np.where(scale == 0, 1.0, scale)
-    denom = np.maximum(np.abs(ref), floor * scale)
+        rms = np.where(rms == 0, 1.0, rms)
+    denom = np.maximum(np.abs(ref), rms)
     return float(np.max(np.abs(got - ref) / denom))
+
+
+def norm_rel_err(got, ref):
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    if not np.all(np.isfinite(got)):
+        return float("inf")
+    n = np.linalg.norm(ref)
+    e = np.linalg.norm(got - ref)
+    return float(e / n) if n > 0 else (0.0 if e == 0 else float("inf"))
+
+
+def assert_close(got, ref, what=""):
+    e, n = max_rel_err(got, ref), norm_rel_err(got, ref)
+    assert e <= REL_TOL and n <= NORM_TOL, f"{what}: element-wise {e:.3g}, normwise {n:.3g}"
+    return e, n
 
 
 def oracle_ranges(wl: Workload, device=None):

@@ -2,7 +2,8 @@
 fp64 oracle, through the C ABI.
 
 Bar: every fp16 output vector within max relative error 2e-2 (element-wise,
-denominator floored at 1% of the vector's largest magnitude); KV indexing
+denominator floored at the reference vector's RMS) and normwise relative
+error 4e-3 (see tests/common.py); KV indexing
 bit-exact (the appended slot holds the new key/value, every other cache
 byte keeps its sentinel or context value, ``len`` advances by one).
 """
@@ -14,8 +15,8 @@ import oracle
 from paper_2607_07046_amd import voltron as vt
 from synth import get
 from synth.gen import LayerInputs
-from tests.common import (REL_TOL, full_weights, max_rel_err, oracle_ranges,
-                          oracle_shard_weights, tiny_workload)
+from tests.common import (NORM_TOL, REL_TOL, assert_close, full_weights, max_rel_err,
+                          norm_rel_err, oracle_ranges, oracle_shard_weights, tiny_workload)
 from tests.gpu_common import SENTINEL, GpuShard
 
 pytestmark = pytest.mark.gpu
@@ -43,9 +44,9 @@ def oracle_case(wl, device=None, li=None):
 
 
 def check_outputs(got, ref, keys=("p_attn", "h", "p_ffn", "y")):
-    errs = {k: max_rel_err(got[k], ref[k]) for k in keys}
-    bad = {k: e for k, e in errs.items() if not e <= REL_TOL}
-    assert not bad, f"relative errors {errs}"
+    errs = {k: (max_rel_err(got[k], ref[k]), norm_rel_err(got[k], ref[k])) for k in keys}
+    bad = {k: e for k, e in errs.items() if not (e[0] <= REL_TOL and e[1] <= NORM_TOL)}
+    assert not bad, f"(element-wise, normwise) relative errors {errs}"
     return errs
 
 
@@ -60,8 +61,8 @@ def check_kv(gs, ref, pos, k_before, v_before):
     k_new = kc[:, pos].view(np.float16).astype(np.float64)
     v_new = vc[:, pos].view(np.float16).astype(np.float64)
     for g in range(k_new.shape[0]):
-        assert max_rel_err(k_new[g], ref["k_new"][g]) <= REL_TOL
-        assert max_rel_err(v_new[g], ref["v_new"][g]) <= REL_TOL
+        assert_close(k_new[g], ref["k_new"][g], f"appended key of KV head {g}")
+        assert_close(v_new[g], ref["v_new"][g], f"appended value of KV head {g}")
 
 
 @pytest.mark.parametrize("mode", MODES)
@@ -106,19 +107,19 @@ def test_all_shards_sum_to_unsharded_layer(key):
     shards = [GpuShard(wl, device=s, li=li) for s in range(len(wl.fracs))]
     parts = [gs.decode(x, wl.ctx, vt.VT_ATTN) for gs in shards]
     sum_attn = np.sum([p["p_attn"] for p in parts], axis=0)
-    assert max_rel_err(sum_attn, full["p_attn"]) <= REL_TOL
+    assert_close(sum_attn, full["p_attn"], "sum of attention partials")
     # aggregation on the main device (host stand-in), then the FFN shards
     h = (x.astype(np.float64) + sum_attn).astype(np.float16)
     ffn = [gs.decode(None, phases=vt.VT_FFN, h_in=h) for gs in shards]
     sum_ffn = np.sum([f["p_ffn"] for f in ffn], axis=0)
-    assert max_rel_err(sum_ffn, full["p_ffn"]) <= REL_TOL
+    assert_close(sum_ffn, full["p_ffn"], "sum of FFN partials")
     # peer semantics: shard 0 given the others' partials produces the full h and y
     peer_a = np.sum([p["p_attn"] for p in parts[1:]], axis=0).astype(np.float16)
     peer_f = np.sum([f["p_ffn"] for f in ffn[1:]], axis=0).astype(np.float16)
     gs0 = GpuShard(wl, device=0, li=li)
     got = gs0.decode(x, wl.ctx, BOTH, peer_attn=peer_a, peer_ffn=peer_f)
-    assert max_rel_err(got["h"], full["h"]) <= REL_TOL
-    assert max_rel_err(got["y"], full["y"]) <= REL_TOL
+    assert_close(got["h"], full["h"], "h with peer partials")
+    assert_close(got["y"], full["y"], "y with peer partials")
 
 
 def test_consecutive_tokens_match_oracle_chain():
