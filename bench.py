@@ -1,0 +1,269 @@
+"""Decode-layer-shard throughput on one MI355X.
+
+A step is one batch-1 decode of the shard through the whole hot path
+(RMSNorm, QKV, RoPE, KV append, attention, O, residual, RMSNorm, gate/up,
+SiLU-gate, down, residual) via vt_layer_decode. The workload is the 30%
+shard (10 of 32 heads, 3302 of 11008 FFN columns) of the 7B-shaped layer
+decoding at position 1024. To keep the 256 MB Infinity Cache from serving
+the weights, the bench holds R distinct weight/KV copies (>= 768 MB in all)
+and step i runs copy i mod R; step i+1 takes step i's output y as its input,
+so steps form a dependent chain like a stack of layers. Each step re-decodes
+position 1024 of its copy. Inputs are resident in HBM before timing starts.
+
+Prints one JSON line. ``value`` is tokens/s (steps per second), the HBM
+figure is algorithmic bytes per step / time per step, and ``roofline``
+reports the decode kernel against the 8 TB/s HBM peak. ``cpu_baseline`` is
+the fp64 oracle timed on the host cores on a bounded sample of the same
+workload (a reference, not the target).
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "decode-layer-shard tokens/s and achieved HBM GB/s (% of peak), 1 MI355X"
+HBM_PEAK_GBPS = 8000.0
+MALL_DEFEAT_BYTES = 768 * 2 ** 20
+
+
+def algorithmic_bytes(dims, info, pos):
+    """Bytes the decode step must move: every shard weight once, the cached
+    K/V of positions 0..pos-1 read plus the new K/V written, the gains, x in,
+    and the four fp16 output vectors."""
+    H, d = dims.hidden, dims.head_dim
+    nq, nkv, F = info.n_q_heads, info.n_kv_heads, info.n_cols
+    weights = 2 * ((nq + 2 * nkv) * d * H + H * nq * d + 3 * F * H)
+    kv = 4 * nkv * d * (pos + 1)
+    vectors = 2 * H * (2 + 1 + 4)  # gains, x, attn_partial/h/ffn_partial/y
+    return weights + kv + vectors
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=2000)
+    ap.add_argument("--warmup", type=int, default=200)
+    ap.add_argument("--config", default="7b", help="decode workload key (synth.configs)")
+    ap.add_argument("--copies", type=int, default=0, help="weight copies (0: enough for 768 MB)")
+    ap.add_argument("--staged", action="store_true", help="one launch per stage")
+    ap.add_argument("--eager", action="store_true", help="no HIP graph")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="host time budget of the oracle baseline (0: skip)")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only: the cross-device "
+                                   "reduction is replaced by returning the shard's partial "
+                                   "sums, so --gpus must be 1"}))
+        sys.exit(2)
+    import torch
+
+    from paper_2607_07046_amd import pack
+    from paper_2607_07046_amd import voltron as vt
+    from synth import get
+    from synth.gen import LayerInputs
+
+    wl = get(args.config)
+    if wl.chunk:
+        raise SystemExit("bench.py times decode workloads; the prefill chunk is reported "
+                         "by its own section")
+    torch.cuda.init()
+    dev = torch.device("cuda:0")
+    dims = vt.vt_layer_dims(hidden=wl.dims.hidden, n_heads=wl.dims.n_heads,
+                            n_kv_heads=wl.dims.n_kv_heads, head_dim=wl.dims.head_dim,
+                            ffn=wl.dims.ffn, rms_eps=wl.dims.rms_eps,
+                            rope_base=wl.dims.rope_base)
+    spec = vt.vt_shard_spec_create(dims, wl.fracs, wl.fracs, wl.device)
+    dims, info = vt.vt_shard_spec_query(spec)
+    pos = wl.ctx
+    step_bytes = algorithmic_bytes(dims, info, pos)
+    copies = args.copies or max(1, math.ceil(MALL_DEFEAT_BYTES / step_bytes))
+    H, d, nkv, cap = dims.hidden, dims.head_dim, info.n_kv_heads, pos + 1
+
+    t0 = time.time()
+    layers = []
+    for c in range(copies):
+        li = LayerInputs(wl, layer=c)
+        w = pack.pack_shard(li, dims, info, dev)
+        kc = torch.zeros((nkv, cap, d), dtype=torch.float16, device=dev)
+        vc = torch.zeros_like(kc)
+        k, v = li.kv_context_heads(info.kv_head_begin, info.kv_head_begin + nkv)
+        kc[:, :pos] = torch.from_numpy(k).to(dev)
+        vc[:, :pos] = torch.from_numpy(v).to(dev)
+        kv = vt.vt_kv_view(k=kc.data_ptr(), v=vc.data_ptr(), capacity=cap, n_kv_heads=nkv,
+                           head_dim=d, len=pos)
+        layers.append((w, kc, vc, kv))
+    ws_bytes = vt.vt_workspace_size(spec, 1, cap)
+    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device=dev)
+    x0 = torch.from_numpy(LayerInputs(wl).x(0)).to(dev)
+    bufs = [x0.clone(), torch.empty_like(x0)]
+    p_attn, h, p_ffn = (torch.empty(H, dtype=torch.float16, device=dev) for _ in range(3))
+    torch.cuda.synchronize()
+    setup_s = time.time() - t0
+
+    phases = vt.VT_ATTN | vt.VT_FFN | (vt.VT_STAGED if args.staged else 0)
+
+    def enqueue(i, stream):
+        w, kc, vc, kv = layers[i % copies]
+        kv.len = pos  # every step re-decodes position `pos` of its copy
+        io = vt.vt_layer_io(x=bufs[i % 2].data_ptr(), peer_attn=None, peer_ffn=None,
+                            attn_partial=p_attn.data_ptr(), h=h.data_ptr(),
+                            ffn_partial=p_ffn.data_ptr(), y=bufs[(i + 1) % 2].data_ptr())
+        vt.vt_layer_decode(spec, w.struct, kv, io, pos, phases, ws.data_ptr(), ws_bytes,
+                           stream)
+
+    # a graph covers a whole number of rotations and an even number of steps
+    group = copies * (2 if copies % 2 else 1)
+    use_graph = not args.eager
+    graphs = {}
+
+    def graph_for(n):
+        if n not in graphs:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                s = torch.cuda.current_stream().cuda_stream
+                for i in range(n):
+                    enqueue(i, s)
+            graphs[n] = g
+        return graphs[n]
+
+    def run(n):
+        s = torch.cuda.current_stream().cuda_stream
+        if not use_graph:
+            for i in range(n):
+                enqueue(i, s)
+            return
+        reps, rem = divmod(n, group * 8)
+        for _ in range(reps):
+            graph_for(group * 8).replay()
+        if rem:
+            graph_for(rem).replay()
+
+    graph_error = None
+    if use_graph:
+        try:
+            run(group * 8)
+            torch.cuda.synchronize()
+        except Exception as e:  # capture not supported: report and time eagerly
+            graph_error = f"{type(e).__name__}: {e}"
+            use_graph = False
+            torch.cuda.synchronize()
+
+    run(args.warmup)
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    run(args.steps)
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end)
+    ms_step = ms / args.steps
+    err_words = ws[:4 * (3072 + 32 * (info.n_q_heads + 1))].view(torch.int32).cpu().numpy()
+    if np.any(err_words):
+        raise SystemExit(f"decode kernel left synchronisation words set: {err_words[:4]}")
+    if not torch.isfinite(bufs[args.steps % 2].float()).all():
+        raise SystemExit("non-finite output after the timed steps")
+
+    tokens_s = 1e3 / ms_step
+    gbps = step_bytes / (ms_step * 1e-3) / 1e9
+    n_launch = 1 if not args.staged else (5 if info.n_q_heads else 3)
+    out = {
+        "metric": METRIC,
+        "value": round(tokens_s, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {
+            "workload": wl.key,
+            "layer": f"hidden {H}, {wl.dims.n_heads}x{d} heads, {wl.dims.n_kv_heads} KV heads, "
+                     f"FFN {wl.dims.ffn}",
+            "shard": f"device {wl.device} of fractions {list(wl.fracs)}: "
+                     f"{info.n_q_heads} q heads, {info.n_kv_heads} kv heads, "
+                     f"{info.n_cols} FFN cols",
+            "pos": pos,
+            "weight_copies": copies,
+            "launch": ("staged" if args.staged else "persistent") +
+                      ("+hipgraph" if use_graph else "+eager"),
+        },
+        "hbm_GBps": round(gbps, 1),
+        "hbm_frac_of_peak": round(gbps / HBM_PEAK_GBPS, 4),
+        "algorithmic_bytes_per_step": step_bytes,
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "decode_kernel" if not args.staged else "decode_kernel (5 launches)",
+            "achieved": round(gbps, 1),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(gbps / HBM_PEAK_GBPS, 4),
+            "traffic": None,
+            "launches_per_step": n_launch,
+        },
+        "setup_s": round(setup_s, 1),
+    }
+    if graph_error:
+        out["graph_error"] = graph_error
+    if args.cpu_seconds > 0:
+        out["cpu_baseline"] = cpu_baseline(wl, pos, args.cpu_seconds, step_bytes)
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(wl, pos, budget_s, step_bytes):
+    """The fp64 oracle, as it stands, on the host cores: decode steps of the
+    same shard (copy 0) at the same position, until the budget is spent."""
+    import oracle
+    from synth.gen import LayerInputs
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = 1
+    d = wl.dims
+    li = LayerInputs(wl, layer=0)
+    r = oracle.shard_ranges(d.n_heads, d.n_kv_heads, d.ffn, wl.fracs, wl.fracs, wl.device)
+    dd = d.head_dim
+    w = oracle.ShardWeights(
+        g_attn=li.g_attn(), wq=li.rows("wq", r.q_head_begin * dd,
+                                       (r.q_head_begin + r.n_q_heads) * dd),
+        wk=li.rows("wk", r.kv_head_begin * dd, (r.kv_head_begin + r.n_kv_heads) * dd),
+        wv=li.rows("wv", r.kv_head_begin * dd, (r.kv_head_begin + r.n_kv_heads) * dd),
+        wo=li.cols("wo", r.q_head_begin * dd, (r.q_head_begin + r.n_q_heads) * dd),
+        g_ffn=li.g_ffn(), wg=li.rows("wg", r.col_begin, r.col_begin + r.n_cols),
+        wu=li.rows("wu", r.col_begin, r.col_begin + r.n_cols),
+        wd=li.cols("wd", r.col_begin, r.col_begin + r.n_cols))
+    kc, vc = li.kv_context_heads(r.kv_head_begin, r.kv_head_begin + r.n_kv_heads)
+    n = 0
+    t0 = time.perf_counter()
+    while True:
+        oracle.decode(w, r.n_q_heads, r.n_kv_heads, dd, d.rms_eps, d.rope_base, li.x(n), kc, vc,
+                      pos)
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s:
+            break
+    return {"value": round(n / el, 3), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n} fp64 oracle decode steps of the same shard (weight copy 0) at "
+                      f"position {pos}, inputs drawn per token; {el:.1f} s",
+            "GBps_equiv": round(n * step_bytes / el / 1e9, 3),
+            "host_cpus": len(os.sched_getaffinity(0))}
+
+
+if __name__ == "__main__":
+    main()

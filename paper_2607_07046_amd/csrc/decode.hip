@@ -33,16 +33,20 @@
 namespace vt {
 namespace dec {
 
-constexpr int NT = 512;          // threads per workgroup
+constexpr int NT = 512;          // threads per workgroup (8 waves)
 constexpr int NW = NT / kWave;   // waves per workgroup
 constexpr int SEG = 512;         // fp16 elements per piece (64 lanes x 8)
 constexpr int PF = 16;           // pieces in flight per wave
+constexpr int PRE = 16;          // of which issued before the phase's barrier wait
 constexpr int MAX_SLOTS = 4096;  // pieces per workgroup round (one float each)
 constexpr int REC = 4;           // attention partial record = head_dim + REC floats
 constexpr unsigned kSpinLimit = 1u << 20;  // about a second of polling
 
 enum { PH_QKV = 0, PH_ATTN = 1, PH_O = 2, PH_GATEUP = 3, PH_DOWN = 4 };
-enum { SW_BAR = 0, SW_EXIT = 1, SW_ERR = 2, SW_GROUP = 16 };
+// Synchronisation words, each hot word in its own 4 KiB-separated spot so
+// that the grid barrier's pollers do not share a memory channel with the
+// per-head counters of the attention phase.
+enum { SW_BAR = 0, SW_EXIT = 1024, SW_ERR = 2048, SW_GROUP = 3072, SW_GROUP_STRIDE = 32 };
 
 struct Params {
   int H, d, nq, nkv, G, ncols, pos, cap, nchunk, cl;
@@ -50,9 +54,12 @@ struct Params {
   const uint16_t *g_attn, *wq, *wk, *wv, *wo, *g_ffn, *wg, *wu, *wd;
   int64_t ld_q, ld_k, ld_v, ld_o, ld_g, ld_u, ld_d;
   uint16_t *kc, *vc;
+  uint32_t kv_bytes;  // bytes of each of kc, vc (n_kv * cap * d * 2)
   const uint16_t *x, *peer_a, *peer_f;
   uint16_t *p_attn, *h, *p_ffn, *y;
   float *qkv, *part, *o, *m;
+  float* hbuf;      // h in fp32, shared between the O and FFN phases of one call
+  int h_from_ws;    // FFN phases read h from hbuf (1) or from the caller's h (0)
   unsigned* sync;
   int phase_begin, phase_end;
 };
@@ -60,341 +67,568 @@ struct Params {
 // ---------------------------------------------------------------------------
 // grid barrier (only between phases of one persistent launch)
 // ---------------------------------------------------------------------------
+// Data crossing the barrier moves through st_shared / ld_shared only, so
+// arrival is: every wave's stores complete, then one relaxed increment.
 __device__ __forceinline__ void grid_arrive(unsigned* sync) {
+  mem_done();
   __syncthreads();
-  if (threadIdx.x == 0) {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  if (threadIdx.x == 0)
     __hip_atomic_fetch_add(sync + SW_BAR, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
 }
 
 __device__ __forceinline__ void grid_wait(unsigned* sync, unsigned target) {
   if (threadIdx.x == 0) {
     unsigned n = 0;
     while (__hip_atomic_load(sync + SW_BAR, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
-      __builtin_amdgcn_s_sleep(1);
+      __builtin_amdgcn_s_sleep(4);
       if (++n > kSpinLimit) {  // never expected: report instead of hanging
         sync_or(sync + SW_ERR, 1u);
         break;
       }
     }
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   }
   __syncthreads();
 }
 
 // ---------------------------------------------------------------------------
-// row sources: virtual row index -> address of its first element
+// row sources: virtual row index -> (buffer, byte offset of the row). The row
+// index is wave-uniform, so the buffer selection stays in scalar registers.
 // ---------------------------------------------------------------------------
+struct Mat {
+  rsrc_t r;
+  uint32_t ld;  // row stride in bytes
+};
+
+__device__ __forceinline__ Mat make_mat(const uint16_t* w, int64_t ld, int64_t rows) {
+  return Mat{make_rsrc(w, static_cast<uint32_t>(rows * ld * 2)), static_cast<uint32_t>(ld * 2)};
+}
+
 struct RowsQKV {
-  const uint16_t *wq, *wk, *wv;
-  int64_t lq, lk, lv;
+  Mat q, k, v;
   int nqd, nkd;
-  __device__ __forceinline__ const uint16_t* operator()(int r) const {
-    if (r < nqd) return wq + static_cast<int64_t>(r) * lq;
-    r -= nqd;
-    if (r < nkd) return wk + static_cast<int64_t>(r) * lk;
-    return wv + static_cast<int64_t>(r - nkd) * lv;
+  __device__ __forceinline__ void at(int r, rsrc_t& rs, uint32_t& off) const {
+    if (r < nqd) {
+      rs = q.r;
+      off = static_cast<uint32_t>(r) * q.ld;
+    } else if (r < nqd + nkd) {
+      rs = k.r;
+      off = static_cast<uint32_t>(r - nqd) * k.ld;
+    } else {
+      rs = v.r;
+      off = static_cast<uint32_t>(r - nqd - nkd) * v.ld;
+    }
   }
 };
 
 struct RowsOne {
-  const uint16_t* w;
-  int64_t ld;
-  __device__ __forceinline__ const uint16_t* operator()(int r) const {
-    return w + static_cast<int64_t>(r) * ld;
+  Mat m;
+  __device__ __forceinline__ void at(int r, rsrc_t& rs, uint32_t& off) const {
+    rs = m.r;
+    off = static_cast<uint32_t>(r) * m.ld;
   }
 };
 
 struct RowsPair {  // row 2j -> a[j], row 2j+1 -> b[j]
-  const uint16_t *a, *b;
-  int64_t la, lb;
-  __device__ __forceinline__ const uint16_t* operator()(int r) const {
-    return (r & 1) ? b + static_cast<int64_t>(r >> 1) * lb : a + static_cast<int64_t>(r >> 1) * la;
+  Mat a, b;
+  __device__ __forceinline__ void at(int r, rsrc_t& rs, uint32_t& off) const {
+    const bool odd = r & 1;
+    rs = odd ? b.r : a.r;
+    off = static_cast<uint32_t>(r >> 1) * (odd ? b.ld : a.ld);
   }
 };
 
-template <class Rows>
-__device__ __forceinline__ u32x4 fetch(const Rows& rows, int row0, int q, int nseg, int K, int lane) {
-  const int lr = q / nseg;
-  const int s = q - lr * nseg;
-  const int col = s * SEG + lane * 8;
-  u32x4 v = {0u, 0u, 0u, 0u};
-  if (col < K) v = load_stream(rows(row0 + lr) + col);
-  return v;
+// Zero the fp16 weights of columns >= K in a lane's 8-column chunk starting
+// at ``col`` (row padding may hold anything).
+__device__ __forceinline__ u32x4 mask_tail(u32x4 w, int col, int K) {
+  const int v = K - col;
+  w.x = v >= 2 ? w.x : (v >= 1 ? (w.x & 0xFFFFu) : 0u);
+  w.y = v >= 4 ? w.y : (v >= 3 ? (w.y & 0xFFFFu) : 0u);
+  w.z = v >= 6 ? w.z : (v >= 5 ? (w.z & 0xFFFFu) : 0u);
+  w.w = v >= 8 ? w.w : (v >= 7 ? (w.w & 0xFFFFu) : 0u);
+  return w;
 }
 
-// Dot product of one piece with the staged input vector xs (zero beyond K).
-__device__ __forceinline__ float dot_piece(const u32x4 w, const float* xs, int s, int K, int lane) {
-  const int col = s * SEG + lane * 8;
-  float f[8];
-  unpack8(w, f);
-  if (col + 8 > K) {  // tail piece: drop row padding, whatever it holds
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-      if (col + e >= K) f[e] = 0.f;
-  }
-  const f32x4 a = *reinterpret_cast<const f32x4*>(xs + col);
-  const f32x4 b = *reinterpret_cast<const f32x4*>(xs + col + 4);
-  float r = f[0] * a.x;
-  r = fmaf(f[1], a.y, r);
-  r = fmaf(f[2], a.z, r);
-  r = fmaf(f[3], a.w, r);
-  r = fmaf(f[4], b.x, r);
-  r = fmaf(f[5], b.y, r);
-  r = fmaf(f[6], b.z, r);
-  r = fmaf(f[7], b.w, r);
-  return r;
+// acc + sum of the 8 products of fp16 weights w and fp16 inputs x (fp32
+// accumulate, two products per instruction). The halves are taken with
+// vector shuffles of the whole 16 bytes: bit-casting single ext-vector
+// elements (w.y, ...) makes this compiler reuse element 0 for all four.
+__device__ __forceinline__ float dot8(const u32x4 w, const u32x4 x, float acc) {
+  const f16x8 a = __builtin_bit_cast(f16x8, w), b = __builtin_bit_cast(f16x8, x);
+  acc = __builtin_amdgcn_fdot2(__builtin_shufflevector(a, a, 0, 1), __builtin_shufflevector(b, b, 0, 1),
+                               acc, false);
+  acc = __builtin_amdgcn_fdot2(__builtin_shufflevector(a, a, 2, 3), __builtin_shufflevector(b, b, 2, 3),
+                               acc, false);
+  acc = __builtin_amdgcn_fdot2(__builtin_shufflevector(a, a, 4, 5), __builtin_shufflevector(b, b, 4, 5),
+                               acc, false);
+  acc = __builtin_amdgcn_fdot2(__builtin_shufflevector(a, a, 6, 7), __builtin_shufflevector(b, b, 6, 7),
+                               acc, false);
+  return acc;
 }
 
 // One GEMV phase over ``units`` output units of U virtual rows of K columns.
-// ``stage`` waits for the phase's input and fills xs[0, nseg*SEG) (ending in
-// a workgroup barrier); ``epi(unit, sums)`` consumes each unit's U dot
-// products.
+// A row is split into segments of 512 columns; a piece is one segment of
+// one row (64 lanes x 16 B). Wave 0 is the control wave: it holds no weight
+// loads, so it can wait at the grid barrier and stage the phase's input
+// while the other (streaming) waves' first PF loads are in flight; memory
+// ordering is in-order per wave, so a wave holding loads could not see the
+// barrier flip before they land. The workgroup's rows form a contiguous run
+// of pieces that the streaming waves split into contiguous sub-runs; each
+// streams its sub-run through a ring of PF loads, accumulates a row's
+// segments in each lane and reduces across the wave at the row's end (or
+// where its sub-run ends), writing the sum to slots[piece]. ``stage`` (run
+// by wave 0 alone) writes the input as fp16 to xs16[0, nseg*512), zero past
+// K. ``epi(unit, sums)`` gets each unit's U row sums, added in piece order.
+// q / n for 0 <= q < 2^24 / n, with rcp = floor(2^24 / n) + 1: a scalar
+// multiply and shift (exact in that range; pieces per round stay < 2^13).
+__device__ __forceinline__ int div_rcp(int q, uint32_t rcp) {
+  return static_cast<int>((static_cast<uint64_t>(static_cast<uint32_t>(q)) * rcp) >> 24);
+}
+
 template <int U, class Rows, class Stage, class Epi>
-__device__ __forceinline__ void gemv_phase(const Rows& rows, int units, int K, float* xs,
+__device__ __forceinline__ void gemv_phase(const Rows& rows, int units, int K, const uint16_t* xs16,
                                            float* slots, Stage stage, Epi epi) {
-  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int lane = threadIdx.x % kWave;
   const int u0 = static_cast<int>(static_cast<int64_t>(units) * blockIdx.x / gridDim.x);
   const int u1 = static_cast<int>(static_cast<int64_t>(units) * (blockIdx.x + 1) / gridDim.x);
-  const int nseg = (K + SEG - 1) / SEG;
-  const int upr = nseg ? max(1, MAX_SLOTS / (U * nseg)) : max(1, u1 - u0);
+  const int nseg = max(1, (K + SEG - 1) / SEG);
+  const uint32_t rcp = (1u << 24) / static_cast<uint32_t>(nseg) + 1u;
+  const int tail = K - (nseg - 1) * SEG;  // columns in a row's last segment
+  const uint32_t lane16 = static_cast<uint32_t>(lane) * 16u;
+  const bool lane_in_tail = lane * 8 < tail;
+  const int upr = max(1, MAX_SLOTS / (U * nseg));
+  // Load piece p (row p / nseg, segment p % nseg of this round) into a register
+  // quad; p >= q1 (past the wave's run) reads zero without memory traffic.
+  auto issue = [&](int row0, int p, int q1) -> u32x4 {
+    const int lr = div_rcp(p, rcp);
+    const int sg = p - lr * nseg;
+    rsrc_t rs;
+    uint32_t roff;
+    rows.at(row0 + lr, rs, roff);
+    const uint32_t base = __builtin_amdgcn_readfirstlane(roff + static_cast<uint32_t>(sg) * (SEG * 2u));
+    const bool ok = (p < q1) && (sg != nseg - 1 || lane_in_tail);
+    return __builtin_amdgcn_raw_buffer_load_b128(rs, ok ? base + lane16 : kOOB, 0, 0);
+  };
   bool staged = false;
   int ua = u0;
   do {
     const int ub = min(u1, ua + upr);
-    const int np = (ub - ua) * U * nseg;
-    const int q0 = static_cast<int>(static_cast<int64_t>(np) * wave / NW);
-    const int q1 = static_cast<int>(static_cast<int64_t>(np) * (wave + 1) / NW);
+    const int np = K > 0 ? (ub - ua) * U * nseg : 0;
+    const int q0 = __builtin_amdgcn_readfirstlane(static_cast<int>(static_cast<int64_t>(np) * wave / NW));
+    const int q1 = __builtin_amdgcn_readfirstlane(static_cast<int>(static_cast<int64_t>(np) * (wave + 1) / NW));
     const int row0 = ua * U;
+    for (int i = threadIdx.x; i < np; i += NT) slots[i] = 0.f;
     u32x4 buf[PF];
+    // A few pieces go out before the barrier wait: they cover its latency
+    // without queueing so much traffic that the staging loads behind them
+    // stall. The rest of the ring follows once the input is staged.
 #pragma unroll
-    for (int i = 0; i < PF; ++i)
-      if (q0 + i < q1) buf[i] = fetch(rows, row0, q0 + i, nseg, K, lane);
+    for (int i = 0; i < PRE; ++i) buf[i] = issue(row0, q0 + i, q1);
     if (!staged) {
-      stage();
+      stage();  // all threads; ends with a workgroup barrier
       staged = true;
+    } else {
+      __syncthreads();
     }
+#pragma unroll
+    for (int i = PRE; i < PF; ++i) buf[i] = issue(row0, q0 + i, q1);
     float acc = 0.f;
     for (int base = q0; base < q1; base += PF) {
 #pragma unroll
       for (int i = 0; i < PF; ++i) {
         const int q = base + i;
         if (q < q1) {
-          const u32x4 w = buf[i];
-          if (q + PF < q1) buf[i] = fetch(rows, row0, q + PF, nseg, K, lane);
-          const int s = q % nseg;
-          acc += dot_piece(w, xs, s, K, lane);
-          if (s == nseg - 1 || q == q1 - 1) {
+          const int cs = q - div_rcp(q, rcp) * nseg;
+          u32x4 w = buf[i];
+          const int col = cs * SEG + lane * 8;
+          const u32x4 x = *reinterpret_cast<const u32x4*>(xs16 + col);
+          if (cs == nseg - 1 && tail < SEG) w = mask_tail(w, col, K);
+          acc = dot8(w, x, acc);
+          if (cs == nseg - 1 || q == q1 - 1) {
             const float t = wave_sum(acc);
             if (lane == 0) slots[q] = t;
             acc = 0.f;
-          } else if (lane == 0) {
-            slots[q] = 0.f;
           }
         }
+        buf[i] = issue(row0, q + PF, q1);
       }
     }
-    __syncthreads();
+    lds_barrier();  // every slot written
     for (int lu = threadIdx.x; lu < ub - ua; lu += NT) {
       float v[U];
 #pragma unroll
       for (int j = 0; j < U; ++j) {
         float a = 0.f;
-        const float* sl = slots + (lu * U + j) * nseg;
-        for (int s = 0; s < nseg; ++s) a += sl[s];
+        if (K > 0) {
+          const float* sl = slots + (lu * U + j) * nseg;
+          for (int s = 0; s < nseg; ++s) a += sl[s];
+        }
         v[j] = a;
       }
       epi(ua + lu, v);
     }
-    __syncthreads();
+    lds_barrier();  // slots and xs free for reuse
     ua = ub;
   } while (ua < u1);
 }
 
-// xs[k] = v[k] * rstd * g[k] for k < n (v, g fp16), zero up to npad.
-__device__ __forceinline__ void stage_rmsnorm(const uint16_t* v, const uint16_t* g, int n, int npad,
-                                              float eps, float* xs, float* red) {
+// ---------------------------------------------------------------------------
+// staging of a GEMV phase's input vector into LDS as fp16 (all threads; each
+// ends with a workgroup barrier)
+// ---------------------------------------------------------------------------
+// xs[k] = fp16(v[k] * rstd * g[k]), rstd = 1 / sqrt(mean(v^2) + eps), for a
+// caller-provided fp16 vector v (n a multiple of 8, n <= 8 * 4 * NT); zero
+// for n <= k < npad.
+__device__ __forceinline__ void stage_rmsnorm_h(const uint16_t* v, const uint16_t* g, int n, int npad,
+                                                float eps, uint16_t* xs, float* red) {
+  constexpr int MAXC = 4;
+  const int nch = n / 8;
+  const rsrc_t rv = make_rsrc(v, static_cast<uint32_t>(n) * 2u);
+  const rsrc_t rg = make_rsrc(g, static_cast<uint32_t>(n) * 2u);
+  u32x4 xv[MAXC], gv[MAXC];
+#pragma unroll
+  for (int c = 0; c < MAXC; ++c) {  // chunks past n read as zero
+    const uint32_t off = static_cast<uint32_t>(threadIdx.x + c * NT) * 16u;
+    xv[c] = buf_load16(rv, off);
+    gv[c] = buf_load16(rg, off);
+  }
   float ss = 0.f;
-  for (int k8 = threadIdx.x; k8 < n / 8; k8 += NT) {
+#pragma unroll
+  for (int c = 0; c < MAXC; ++c) {
     float f[8];
-    unpack8(load16(v + k8 * 8), f);
+    unpack8(xv[c], f);
 #pragma unroll
     for (int e = 0; e < 8; ++e) ss = fmaf(f[e], f[e], ss);
   }
   ss = block_sum<NT>(ss, red);
   const float rstd = 1.0f / sqrtf(ss / static_cast<float>(n) + eps);
-  for (int k8 = threadIdx.x; k8 < n / 8; k8 += NT) {
-    float f[8], gg[8];
-    unpack8(load16(v + k8 * 8), f);
-    unpack8(load16(g + k8 * 8), gg);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) xs[k8 * 8 + e] = f[e] * rstd * gg[e];
+  for (int c = 0; c < MAXC; ++c) {
+    const int k8 = threadIdx.x + c * NT;
+    if (k8 < nch) {
+      float f[8], gf[8];
+      unpack8(xv[c], f);
+      unpack8(gv[c], gf);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) xs[k8 * 8 + e] = f2h(f[e] * rstd * gf[e]);
+    }
   }
-  for (int k = n + threadIdx.x; k < npad; k += NT) xs[k] = 0.f;
+  for (int k = n + threadIdx.x; k < npad; k += NT) xs[k] = 0;
   __syncthreads();
 }
 
-__device__ __forceinline__ void stage_copy(const float* v, int n, int npad, float* xs) {
-  for (int k = threadIdx.x; k < npad; k += NT) xs[k] = k < n ? v[k] : 0.f;
+// The same for an fp32 vector written by other workgroups of this launch
+// (n a multiple of 8), each value first rounded to fp16: the value the
+// caller's fp16 h would carry.
+__device__ __forceinline__ void stage_rmsnorm_f(const float* v, const uint16_t* g, int n, int npad,
+                                                float eps, uint16_t* xs, float* red) {
+  constexpr int MAXP = 16;  // float pairs held per thread
+  const int npair = n / 2;
+  float a[MAXP], b[MAXP];
+  // Indices are clamped rather than the loads guarded: a guarded coherent
+  // load is compiled into its own branch with a full wait, which would
+  // serialise the 16 round trips.
+#pragma unroll
+  for (int u = 0; u < MAXP; ++u) {
+    const int i = min(static_cast<int>(threadIdx.x) + u * NT, npair - 1);
+    ld_shared2(v + 2 * i, a[u], b[u]);
+  }
+  const rsrc_t rg = make_rsrc(g, static_cast<uint32_t>(n) * 2u);
+  uint32_t gw[MAXP];  // the two fp16 gains of each pair (zero past n)
+#pragma unroll
+  for (int u = 0; u < MAXP; ++u)
+    gw[u] = __builtin_amdgcn_raw_buffer_load_b32(rg, static_cast<uint32_t>(threadIdx.x + u * NT) * 4u, 0, 0);
+  float ss = 0.f;
+#pragma unroll
+  for (int u = 0; u < MAXP; ++u) {
+    const bool ok = static_cast<int>(threadIdx.x) + u * NT < npair;
+    a[u] = ok ? round_h(a[u]) : 0.f;
+    b[u] = ok ? round_h(b[u]) : 0.f;
+    ss = fmaf(a[u], a[u], fmaf(b[u], b[u], ss));
+  }
+  ss = block_sum<NT>(ss, red);
+  const float rstd = 1.0f / sqrtf(ss / static_cast<float>(n) + eps);
+#pragma unroll
+  for (int u = 0; u < MAXP; ++u) {
+    const int i = threadIdx.x + u * NT;
+    if (i < npair) {
+      float g0, g1;
+      unpack2(gw[u], g0, g1);
+      xs[2 * i] = f2h(a[u] * rstd * g0);
+      xs[2 * i + 1] = f2h(b[u] * rstd * g1);
+    }
+  }
+  for (int k = n + threadIdx.x; k < npad; k += NT) xs[k] = 0;
+  __syncthreads();
+}
+
+// xs[k] = fp16(v[k]) for an fp32 vector written by other workgroups of this
+// launch (its buffer holds an even number of floats); zero for n <= k < npad.
+__device__ __forceinline__ void stage_copy_f(const float* v, int n, int npad, uint16_t* xs) {
+  constexpr int MAXP = 16;
+  const int npair = (n + 1) / 2;
+  for (int c0 = 0; c0 < npair; c0 += MAXP * NT) {
+    float a[MAXP], b[MAXP];
+#pragma unroll
+    for (int u = 0; u < MAXP; ++u) {  // clamped, not guarded (see stage_rmsnorm_f)
+      const int i = min(c0 + static_cast<int>(threadIdx.x) + u * NT, npair - 1);
+      ld_shared2(v + 2 * i, a[u], b[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < MAXP; ++u) {
+      const int i = c0 + threadIdx.x + u * NT;
+      if (i < npair) {
+        xs[2 * i] = f2h(a[u]);
+        xs[2 * i + 1] = 2 * i + 1 < n ? f2h(b[u]) : 0;
+      }
+    }
+  }
+  for (int k = 2 * npair + threadIdx.x; k < npad; k += NT) xs[k] = 0;
   __syncthreads();
 }
 
 __host__ __device__ __forceinline__ int padded(int K) { return ((K + SEG - 1) / SEG) * SEG; }
 
 // ---------------------------------------------------------------------------
-// phase 1: attention over the shard's KV groups
+// phase 1: attention
+//
+// Work item = (query head j, chunk of CL consecutive positions). A thread
+// holds 8 of the d dimensions of one position per pass (d/8 threads per
+// position, PPP positions per pass, CL = passes * PPP). The chunk's keys and
+// values do not depend on phase 0, so they are loaded into registers before
+// the grid barrier. Items of the G query heads that share a KV head and a
+// chunk are placed on workgroups with equal index mod 8, i.e. on one XCD, so
+// the group reads each K/V tile from HBM once and from that XCD's L2 after.
+// Each item writes (unnormalised sum of p*V, running max m, sum l); the last
+// item of head j to finish merges the head's chunks by log-sum-exp.
 // ---------------------------------------------------------------------------
+constexpr int MAXPASS = 8;
+
+__host__ __device__ __forceinline__ int attn_ppp(int d) { return NT / (d / 8); }
+
+__host__ __device__ __forceinline__ int attn_lds_floats(int d, int nchunk) {
+  const int ppp = attn_ppp(d);
+  return d + MAXPASS * ppp + ppp * d + 2 * d + 2 * nchunk + 4;
+}
+
 __device__ __forceinline__ void phase_attn(const Params& P, float* lds, bool wait, unsigned target) {
   const int d = P.d, G = P.G, CL = P.cl;
-  const int TPP = d / 8;               // threads per cached position
-  const int t = threadIdx.x;
-  const int pl = t / TPP;              // this thread's position within the chunk
-  const int dc = (t % TPP) * 8;        // and its 8 dimensions
-  const int items = P.nkv * P.nchunk;
+  const int TPP = d / 8, PPP = NT / TPP, NPASS = CL / PPP;
+  const int t = threadIdx.x, wave = t / kWave, lane = t % kWave;
+  const int pl = t / TPP;             // position within a pass
+  const int dc = (t % TPP) * 8;       // first of this thread's 8 dimensions
+  const int RW = d + REC;             // floats per partial record
+  const int units = P.nkv * P.nchunk; // (KV head, chunk) pairs
+  const int ids = ((units + 7) / 8) * 8 * G;
   const float scale = 1.0f / sqrtf(static_cast<float>(d));
-  // LDS layout (floats): qs[G*d] | S[G*CL] | Vs[CL*d] | kn[d] | vn[d] | flag
+  // LDS (floats): qs[d] | S[MAXPASS*PPP] | R[PPP*d] | kn[d] | vn[d] | W[2*nchunk] | flag
   float* qs = lds;
-  float* S = qs + G * d;
-  float* Vs = S + G * CL;
-  float* kn = Vs + CL * d;
+  float* S = qs + d;
+  float* R = S + MAXPASS * PPP;
+  float* kn = R + PPP * d;
   float* vn = kn + d;
-  int* flag = reinterpret_cast<int*>(vn + d);
+  float* W = vn + d;
+  int* flag = reinterpret_cast<int*>(W + 2 * P.nchunk);
+  const rsrc_t rk = make_rsrc(P.kc, P.kv_bytes), rv = make_rsrc(P.vc, P.kv_bytes);
 
   bool waited = false;
-  for (int it = blockIdx.x;; it += gridDim.x) {
-    const bool valid = it < items;
-    const int g = valid ? it / P.nchunk : 0;
-    const int c = valid ? it - g * P.nchunk : 0;
-    const int p = c * CL + pl;
-    // cached keys/values of this thread's position (data independent of phase 0)
-    u32x4 kreg = {0u, 0u, 0u, 0u}, vreg = {0u, 0u, 0u, 0u};
-    if (valid && p < P.pos) {
-      const int64_t off = (static_cast<int64_t>(g) * P.cap + p) * d + dc;
-      kreg = load16(P.kc + off);
-      vreg = load16(P.vc + off);
+  for (int id = blockIdx.x;; id += gridDim.x) {
+    const int r8 = id % 8;
+    const int jj = (id / 8) % G;
+    const int u = (id / (8 * G)) * 8 + r8;
+    const bool valid = id < ids && u < units;
+    const int g = valid ? u / P.nchunk : 0;
+    const int c = valid ? u - g * P.nchunk : 0;
+    const int j = g * G + jj;                 // shard-local query head
+    const int p0 = c * CL;
+    u32x4 kr[MAXPASS], vr[MAXPASS];
+#pragma unroll
+    for (int ps = 0; ps < MAXPASS; ++ps) {
+      const int p = p0 + ps * PPP + pl;
+      const bool ok = valid && ps < NPASS && p < P.pos;
+      const uint32_t off =
+          ok ? static_cast<uint32_t>(((static_cast<int64_t>(g) * P.cap + p) * d + dc) * 2) : kOOB;
+      kr[ps] = buf_load16(rk, off);
+      vr[ps] = buf_load16(rv, off);
     }
+    // rotation of pair t at the new position (independent of phase 0)
+    const int half = d / 2;
+    float c0 = 1.f, s0 = 0.f;
+    if (t < half) rope_angle(P.pos, t, d, P.rope_base, c0, s0);
     if (!waited) {
       if (wait) grid_wait(P.sync, target);
       waited = true;
     }
-    if (!valid) break;
+    if (id >= ids) break;
+    if (!valid) continue;
 
-    // rotated, pre-scaled queries of the group's G heads
-    const int half = d / 2;
-    for (int idx = t; idx < G * half; idx += NT) {
-      const int jj = idx / half, i = idx - jj * half;
-      const float* q = P.qkv + static_cast<int64_t>(g * G + jj) * d;
-      float c0, s0;
-      rope_angle(P.pos, i, d, P.rope_base, c0, s0);
-      const float a = q[2 * i], b = q[2 * i + 1];
-      qs[jj * d + 2 * i] = (a * c0 - b * s0) * scale;
-      qs[jj * d + 2 * i + 1] = (a * s0 + b * c0) * scale;
+    // rotated, pre-scaled query of head j; the new token's key and value.
+    // Coherent loads are issued unconditionally with clamped indices (a
+    // guarded one gets a branch and a full wait of its own).
+    const int tp = min(t, half - 1);       // this thread's rotation pair
+    const int tv = min(max(t - half, 0), d - 1);
+    const float* q = P.qkv + static_cast<int64_t>(j) * d;
+    const float* kq = P.qkv + static_cast<int64_t>(P.nq + g) * d;
+    const float* vq = P.qkv + static_cast<int64_t>(P.nq + P.nkv + g) * d;
+    float qa, qb, ka, kb;
+    ld_shared2(q + 2 * tp, qa, qb);
+    ld_shared2(kq + 2 * tp, ka, kb);
+    const float vv = ld_shared(vq + tv);
+    if (t < half) {
+      qs[2 * t] = (qa * c0 - qb * s0) * scale;
+      qs[2 * t + 1] = (qa * s0 + qb * c0) * scale;
     }
-    const bool has_new = (P.pos >= c * CL) && (P.pos < (c + 1) * CL);
-    if (has_new) {  // this item appends the new token's key and value
-      const float* kq = P.qkv + static_cast<int64_t>(P.nq) * d + static_cast<int64_t>(g) * d;
-      const float* vq = P.qkv + static_cast<int64_t>(P.nq + P.nkv) * d + static_cast<int64_t>(g) * d;
+    const bool has_new = P.pos >= p0 && P.pos < p0 + CL;
+    if (has_new) {  // the new token's key (rotated) and value, rounded as stored
       const int64_t slot = (static_cast<int64_t>(g) * P.cap + P.pos) * d;
-      for (int i = t; i < half; i += NT) {
-        float c0, s0;
-        rope_angle(P.pos, i, d, P.rope_base, c0, s0);
-        const float a = kq[2 * i], b = kq[2 * i + 1];
+      const bool writer = jj == 0;  // one item per KV head appends to the cache
+      if (t < half) {
+        const float a = ka, b = kb;
         const uint16_t k0 = f2h(a * c0 - b * s0), k1 = f2h(a * s0 + b * c0);
-        kn[2 * i] = h2f(k0);
-        kn[2 * i + 1] = h2f(k1);
-        P.kc[slot + 2 * i] = k0;
-        P.kc[slot + 2 * i + 1] = k1;
-      }
-      for (int i = t; i < d; i += NT) {
-        const uint16_t v0 = f2h(vq[i]);
+        kn[2 * t] = h2f(k0);
+        kn[2 * t + 1] = h2f(k1);
+        if (writer) {
+          P.kc[slot + 2 * t] = k0;
+          P.kc[slot + 2 * t + 1] = k1;
+        }
+      } else if (t < half + d) {
+        const int i = t - half;
+        const uint16_t v0 = f2h(vv);
         vn[i] = h2f(v0);
-        P.vc[slot + i] = v0;
+        if (writer) P.vc[slot + i] = v0;
       }
     }
     __syncthreads();
 
-    // scores of this thread's position for each of the G heads
-    float kf[8];
-    if (p == P.pos) {
+    // scores
 #pragma unroll
-      for (int e = 0; e < 8; ++e) kf[e] = kn[dc + e];
-    } else {
-      unpack8(kreg, kf);
-    }
-    const bool live = p <= P.pos && pl < CL;
-    for (int jj = 0; jj < G; ++jj) {
-      const float* qq = qs + jj * d + dc;
-      float sacc = 0.f;
+    for (int ps = 0; ps < MAXPASS; ++ps) {
+      if (ps < NPASS) {
+        const int p = p0 + ps * PPP + pl;
+        float kf[8];
+        unpack8(kr[ps], kf);
+        if (p == P.pos) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) sacc = fmaf(qq[e], kf[e], sacc);
-      sacc = group_sum(sacc, TPP);
-      if ((t % TPP) == 0 && pl < CL) S[jj * CL + pl] = live ? sacc : -INFINITY;
-    }
-    // stage values (fp32) for the weighted sum
-    if (pl < CL) {
-      float vf[8];
-      if (p == P.pos) {
+          for (int e = 0; e < 8; ++e) kf[e] = kn[dc + e];
+        }
+        float sc = 0.f;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) vf[e] = vn[dc + e];
-      } else if (p < P.pos) {
-        unpack8(vreg, vf);
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) vf[e] = 0.f;
+        for (int e = 0; e < 8; ++e) sc = fmaf(qs[dc + e], kf[e], sc);
+        sc = group_sum(sc, TPP);
+        if ((t % TPP) == 0) S[ps * PPP + pl] = p <= P.pos ? sc : -INFINITY;
       }
-#pragma unroll
-      for (int e = 0; e < 8; ++e) Vs[pl * d + dc + e] = vf[e];
     }
     __syncthreads();
-
-    // softmax statistics of the chunk, one wave per head
-    const int wave = t / kWave, lane = t % kWave;
-    float* rec0 = P.part + (static_cast<int64_t>(g) * P.nchunk + c) * G * (d + REC);
-    for (int jj = wave; jj < G; jj += NW) {
-      const float s = lane < CL ? S[jj * CL + lane] : -INFINITY;
-      const float mx = wave_max(s);
-      const float e = (lane < CL && s != -INFINITY) ? __expf(s - mx) : 0.f;
-      const float l = wave_sum(e);
-      if (lane < CL) S[jj * CL + lane] = e;
+    float* rec = P.part + (static_cast<int64_t>(j) * P.nchunk + c) * RW;
+    if (wave == 0) {  // softmax statistics of the chunk
+      float mx = -INFINITY;
+      for (int q = lane; q < CL; q += kWave) mx = fmaxf(mx, S[q]);
+      mx = wave_max(mx);
+      float l = 0.f;
+      for (int q = lane; q < CL; q += kWave) {
+        const float e = S[q] == -INFINITY ? 0.f : __expf(S[q] - mx);
+        S[q] = e;
+        l += e;
+      }
+      l = wave_sum(l);
       if (lane == 0) {
-        rec0[jj * (d + REC) + d] = mx;
-        rec0[jj * (d + REC) + d + 1] = l;
+        st_shared(rec + d, mx);
+        st_shared(rec + d + 1, l);
       }
     }
     __syncthreads();
-    // unnormalised weighted sum of values
-    for (int idx = t; idx < G * d; idx += NT) {
-      const int jj = idx / d, dd = idx - jj * d;
-      float a = 0.f;
-      for (int q = 0; q < CL; ++q) a = fmaf(S[jj * CL + q], Vs[q * d + dd], a);
-      rec0[jj * (d + REC) + dd] = a;
+    // unnormalised sum of weights * values over the chunk
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ps = 0; ps < MAXPASS; ++ps) {
+      if (ps < NPASS) {
+        const int p = p0 + ps * PPP + pl;
+        const float e = S[ps * PPP + pl];
+        float vf[8];
+        unpack8(vr[ps], vf);
+        if (p == P.pos) {
+#pragma unroll
+          for (int x = 0; x < 8; ++x) vf[x] = vn[dc + x];
+        }
+#pragma unroll
+        for (int x = 0; x < 8; ++x) acc[x] = fmaf(e, vf[x], acc[x]);
+      }
     }
-    // the last chunk of group g to finish merges the group's chunks
+#pragma unroll
+    for (int x = 0; x < 8; ++x) R[pl * d + dc + x] = acc[x];
+    __syncthreads();
+    for (int dd = t; dd < d; dd += NT) {
+      float a = 0.f;
+      for (int q = 0; q < PPP; ++q) a += R[q * d + dd];
+      st_shared(rec + dd, a);
+    }
+
+    // the last chunk of head j to finish merges the head's chunks
+    mem_done();
     __syncthreads();
     if (t == 0) {
-      const unsigned old = __hip_atomic_fetch_add(P.sync + SW_GROUP + g, 1u, __ATOMIC_ACQ_REL,
+      const unsigned old = __hip_atomic_fetch_add(P.sync + SW_GROUP + j * SW_GROUP_STRIDE, 1u, __ATOMIC_RELAXED,
                                                   __HIP_MEMORY_SCOPE_AGENT);
       *flag = (old == static_cast<unsigned>(P.nchunk - 1));
     }
     __syncthreads();
     if (*flag) {
-      const float* recg = P.part + static_cast<int64_t>(g) * P.nchunk * G * (d + REC);
-      for (int idx = t; idx < G * d; idx += NT) {
-        const int jj = idx / d, dd = idx - jj * d;
-        float M = -INFINITY;
-        for (int cc = 0; cc < P.nchunk; ++cc) M = fmaxf(M, recg[(cc * G + jj) * (d + REC) + d]);
-        float L = 0.f, a = 0.f;
-        for (int cc = 0; cc < P.nchunk; ++cc) {
-          const float* r = recg + (cc * G + jj) * (d + REC);
-          const float w = __expf(r[d] - M);
-          L = fmaf(r[d + 1], w, L);
-          a = fmaf(r[dd], w, a);
+      // Thread (grp, dd) takes chunks grp, grp + ngrp, ...: it loads their
+      // (m, l, value[dd]) in batches of 16 (one round trip each) and keeps a
+      // running (max, sum l, sum value) under the log-sum-exp rescaling; the
+      // ngrp partial triples of each dd are then merged in a fixed order.
+      const float* rj = P.part + static_cast<int64_t>(j) * P.nchunk * RW;
+      const int ngrp = NT / d, grp = t / d, dd = t % d;
+      float M = -INFINITY, Ls = 0.f, A = 0.f;
+      for (int c0 = grp; grp < ngrp && c0 < P.nchunk; c0 += 16 * ngrp) {
+        float mv[16], lv[16], ov[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {  // clamped, not guarded
+          const int cc = min(c0 + u * ngrp, P.nchunk - 1);
+          ld_shared2(rj + cc * RW + d, mv[u], lv[u]);
+          ov[u] = ld_shared(rj + cc * RW + dd);
         }
-        P.o[static_cast<int64_t>(g * G + jj) * d + dd] = a / L;
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+          if (c0 + u * ngrp >= P.nchunk) {
+            mv[u] = -INFINITY;
+            lv[u] = 0.f;
+            ov[u] = 0.f;
+          }
+        }
+        float bm = M;
+#pragma unroll
+        for (int u = 0; u < 16; ++u) bm = fmaxf(bm, mv[u]);
+        const float r = M == -INFINITY ? 0.f : __expf(M - bm);
+        Ls *= r;
+        A *= r;
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+          const float w = mv[u] == -INFINITY ? 0.f : __expf(mv[u] - bm);
+          Ls = fmaf(lv[u], w, Ls);
+          A = fmaf(ov[u], w, A);
+        }
+        M = bm;
+      }
+      if (grp < ngrp) {
+        R[(3 * grp + 0) * d + dd] = M;
+        R[(3 * grp + 1) * d + dd] = Ls;
+        R[(3 * grp + 2) * d + dd] = A;
       }
       __syncthreads();
-      if (t == 0) sync_store(P.sync + SW_GROUP + g, 0u);
+      if (t < d) {
+        float Mx = -INFINITY;
+        for (int q = 0; q < ngrp; ++q) Mx = fmaxf(Mx, R[(3 * q) * d + t]);
+        float Lt = 0.f, At = 0.f;
+        for (int q = 0; q < ngrp; ++q) {
+          const float mq = R[(3 * q) * d + t];
+          const float w = mq == -INFINITY ? 0.f : __expf(mq - Mx);
+          Lt = fmaf(R[(3 * q + 1) * d + t], w, Lt);
+          At = fmaf(R[(3 * q + 2) * d + t], w, At);
+        }
+        st_shared(P.o + static_cast<int64_t>(j) * d + t, At / Lt);
+      }
+      if (t == 0) sync_store(P.sync + SW_GROUP + j * SW_GROUP_STRIDE, 0u);
     }
     __syncthreads();
   }
@@ -403,90 +637,96 @@ __device__ __forceinline__ void phase_attn(const Params& P, float* lds, bool wai
 // ---------------------------------------------------------------------------
 // the kernel
 // ---------------------------------------------------------------------------
+// One phase; ``wait`` / ``target`` describe the grid barrier in front of it.
+template <int PH>
+__device__ __forceinline__ void run_phase(const Params& P, float* lds, uint16_t* xs, float* slots,
+                                          float* red, bool wait, unsigned target) {
+  if constexpr (PH == PH_QKV) {
+    RowsQKV rows{make_mat(P.wq, P.ld_q, P.nq * P.d), make_mat(P.wk, P.ld_k, P.nkv * P.d),
+                 make_mat(P.wv, P.ld_v, P.nkv * P.d), P.nq * P.d, P.nkv * P.d};
+    gemv_phase<1>(
+        rows, (P.nq + 2 * P.nkv) * P.d, P.H, xs, slots,
+        [&]() { stage_rmsnorm_h(P.x, P.g_attn, P.H, padded(P.H), P.eps, xs, red); },
+        [&](int r, const float* v) { st_shared(P.qkv + r, v[0]); });
+  } else if constexpr (PH == PH_ATTN) {
+    phase_attn(P, lds, wait, target);
+  } else if constexpr (PH == PH_O) {
+    RowsOne rows{make_mat(P.wo, P.ld_o, P.H)};
+    const int K = P.nq * P.d;
+    gemv_phase<1>(
+        rows, P.H, K, xs, slots,
+        [&]() {
+          if (wait) grid_wait(P.sync, target);
+          stage_copy_f(P.o, K, padded(K), xs);
+        },
+        [&](int r, const float* v) {
+          const float pa = v[0];
+          P.p_attn[r] = f2h(pa);
+          const float hv = h2f(P.x[r]) + pa + (P.peer_a ? h2f(P.peer_a[r]) : 0.f);
+          P.h[r] = f2h(hv);
+          st_shared(P.hbuf + r, hv);
+        });
+  } else if constexpr (PH == PH_GATEUP) {
+    RowsPair rows{make_mat(P.wg, P.ld_g, P.ncols), make_mat(P.wu, P.ld_u, P.ncols)};
+    gemv_phase<2>(
+        rows, P.ncols, P.H, xs, slots,
+        [&]() {
+          if (wait) grid_wait(P.sync, target);
+          if (P.h_from_ws)
+            stage_rmsnorm_f(P.hbuf, P.g_ffn, P.H, padded(P.H), P.eps, xs, red);
+          else
+            stage_rmsnorm_h(P.h, P.g_ffn, P.H, padded(P.H), P.eps, xs, red);
+        },
+        [&](int j, const float* v) {
+          const float gt = v[0], up = v[1];
+          st_shared(P.m + j, gt / (1.0f + __expf(-gt)) * up);
+        });
+  } else {
+    RowsOne rows{make_mat(P.wd, P.ld_d, P.H)};
+    const int K = P.ncols;
+    gemv_phase<1>(
+        rows, P.H, K, xs, slots,
+        [&]() {
+          if (wait) grid_wait(P.sync, target);
+          stage_copy_f(P.m, K, padded(K), xs);
+        },
+        [&](int r, const float* v) {
+          const float pf = v[0];
+          P.p_ffn[r] = f2h(pf);
+          if (P.y) {
+            const float hr = P.h_from_ws ? round_h(ld_shared(P.hbuf + r)) : h2f(P.h[r]);
+            P.y[r] = f2h(hr + pf + (P.peer_f ? h2f(P.peer_f[r]) : 0.f));
+          }
+        });
+  }
+}
+
+template <int PH, int PE, int PB>
+__device__ __forceinline__ void run_phases(const Params& P, float* lds, uint16_t* xs, float* slots,
+                                           float* red) {
+  run_phase<PH>(P, lds, xs, slots, red, PH > PB, static_cast<unsigned>(PH - PB) * gridDim.x);
+  if constexpr (PH < PE) {
+    grid_arrive(P.sync);
+    run_phases<PH + 1, PE, PB>(P, lds, xs, slots, red);
+  }
+}
+
+// Phases PB..PE of one decode step. PB < PE needs every workgroup resident
+// (one per CU): grid barriers separate the phases.
+template <int PB, int PE>
 __global__ void __launch_bounds__(NT) decode_kernel(Params P) {
   extern __shared__ float lds[];
   // LDS: xs / attention scratch (aliased) | slots[MAX_SLOTS] | red[NW]
   const int kmax = max(max(padded(P.H), padded(P.nq * P.d)), padded(P.ncols));
-  const int attn = P.G * P.d + P.G * P.cl + P.cl * P.d + 2 * P.d + 4;
-  float* xs = lds;
-  float* slots = lds + max(kmax, attn);
+  const int attn = attn_lds_floats(P.d, P.nchunk);
+  uint16_t* xs = reinterpret_cast<uint16_t*>(lds);  // fp16 GEMV input (kmax halfs)
+  float* slots = lds + max(kmax / 2, attn);
   float* red = slots + MAX_SLOTS;
-
-  for (int ph = P.phase_begin; ph <= P.phase_end; ++ph) {
-    const bool wait = ph > P.phase_begin;
-    const unsigned target = static_cast<unsigned>(ph - P.phase_begin) * gridDim.x;
-    auto waitfor = [&]() {
-      if (wait) grid_wait(P.sync, target);
-    };
-    switch (ph) {
-      case PH_QKV: {
-        RowsQKV rows{P.wq, P.wk, P.wv, P.ld_q, P.ld_k, P.ld_v, P.nq * P.d, P.nkv * P.d};
-        gemv_phase<1>(
-            rows, (P.nq + 2 * P.nkv) * P.d, P.H, xs, slots,
-            [&]() {
-              waitfor();
-              stage_rmsnorm(P.x, P.g_attn, P.H, padded(P.H), P.eps, xs, red);
-            },
-            [&](int r, const float* v) { P.qkv[r] = v[0]; });
-        break;
-      }
-      case PH_ATTN:
-        phase_attn(P, lds, wait, target);
-        break;
-      case PH_O: {
-        RowsOne rows{P.wo, P.ld_o};
-        const int K = P.nq * P.d;
-        gemv_phase<1>(
-            rows, P.H, K, xs, slots,
-            [&]() {
-              waitfor();
-              stage_copy(P.o, K, padded(K), xs);
-            },
-            [&](int r, const float* v) {
-              const float pa = v[0];
-              P.p_attn[r] = f2h(pa);
-              const float hv = h2f(P.x[r]) + pa + (P.peer_a ? h2f(P.peer_a[r]) : 0.f);
-              P.h[r] = f2h(hv);
-            });
-        break;
-      }
-      case PH_GATEUP: {
-        RowsPair rows{P.wg, P.wu, P.ld_g, P.ld_u};
-        gemv_phase<2>(
-            rows, P.ncols, P.H, xs, slots,
-            [&]() {
-              waitfor();
-              stage_rmsnorm(P.h, P.g_ffn, P.H, padded(P.H), P.eps, xs, red);
-            },
-            [&](int j, const float* v) {
-              const float gt = v[0], up = v[1];
-              P.m[j] = gt / (1.0f + __expf(-gt)) * up;
-            });
-        break;
-      }
-      case PH_DOWN: {
-        RowsOne rows{P.wd, P.ld_d};
-        const int K = P.ncols;
-        gemv_phase<1>(
-            rows, P.H, K, xs, slots,
-            [&]() {
-              waitfor();
-              stage_copy(P.m, K, padded(K), xs);
-            },
-            [&](int r, const float* v) {
-              const float pf = v[0];
-              P.p_ffn[r] = f2h(pf);
-              if (P.y) P.y[r] = f2h(h2f(P.h[r]) + pf + (P.peer_f ? h2f(P.peer_f[r]) : 0.f));
-            });
-        break;
-      }
-    }
-    if (ph < P.phase_end) grid_arrive(P.sync);
-  }
-  if (P.phase_end > P.phase_begin) {  // the last workgroup out clears the barrier words
+  run_phases<PB, PE, PB>(P, lds, xs, slots, red);
+  if constexpr (PE > PB) {  // the last workgroup out clears the barrier words
     __syncthreads();
     if (threadIdx.x == 0) {
-      const unsigned old = __hip_atomic_fetch_add(P.sync + SW_EXIT, 1u, __ATOMIC_ACQ_REL,
+      const unsigned old = __hip_atomic_fetch_add(P.sync + SW_EXIT, 1u, __ATOMIC_RELAXED,
                                                   __HIP_MEMORY_SCOPE_AGENT);
       if (old == gridDim.x - 1) {
         sync_store(P.sync + SW_BAR, 0u);
@@ -494,6 +734,25 @@ __global__ void __launch_bounds__(NT) decode_kernel(Params P) {
       }
     }
   }
+}
+
+typedef void (*DecodeKernel)(Params);
+
+// Instantiations: the whole step, each sub-layer, and each phase alone.
+__host__ inline DecodeKernel decode_kernel_for(int pb, int pe) {
+  if (pb == PH_QKV && pe == PH_DOWN) return decode_kernel<PH_QKV, PH_DOWN>;
+  if (pb == PH_QKV && pe == PH_O) return decode_kernel<PH_QKV, PH_O>;
+  if (pb == PH_GATEUP && pe == PH_DOWN) return decode_kernel<PH_GATEUP, PH_DOWN>;
+  if (pb == pe) {
+    switch (pb) {
+      case PH_QKV: return decode_kernel<PH_QKV, PH_QKV>;
+      case PH_ATTN: return decode_kernel<PH_ATTN, PH_ATTN>;
+      case PH_O: return decode_kernel<PH_O, PH_O>;
+      case PH_GATEUP: return decode_kernel<PH_GATEUP, PH_GATEUP>;
+      case PH_DOWN: return decode_kernel<PH_DOWN, PH_DOWN>;
+    }
+  }
+  return nullptr;
 }
 
 // ---------------------------------------------------------------------------
@@ -553,9 +812,11 @@ vt_status device_info(DeviceInfo** out) {
   if (!di.lds_attr_set) {
     // Allow dynamic LDS up to the device limit; a refusal surfaces as a
     // launch error for the shapes that would need it.
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(dec::decode_kernel),
-                              hipFuncAttributeMaxDynamicSharedMemorySize,
-                              static_cast<int>(di.max_lds));
+    const int ranges[][2] = {{0, 4}, {0, 2}, {3, 4}, {0, 0}, {1, 1}, {2, 2}, {3, 3}, {4, 4}};
+    for (const auto& r : ranges)
+      (void)hipFuncSetAttribute(reinterpret_cast<const void*>(dec::decode_kernel_for(r[0], r[1])),
+                                hipFuncAttributeMaxDynamicSharedMemorySize,
+                                static_cast<int>(di.max_lds));
     (void)hipGetLastError();
     di.lds_attr_set = true;
   }
@@ -569,16 +830,25 @@ inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 
 // Workspace layout of the decode path (bytes, each region 256-aligned).
 struct DecodeWs {
-  size_t sync, qkv, part, o, m, total;
+  size_t sync, qkv, part, o, m, hbuf, total;
 };
 
-static int attn_chunk(int d) { return dec::NT / (d / 8); }
+// Chunking of the attention phase: the chunk length is a whole number of
+// passes (at most MAXPASS) chosen so that the (query head, chunk) items fill
+// the grid about once.
+static void attn_chunking(int d, int nq, int L, int grid, int* cl, int* nchunk) {
+  const int ppp = dec::attn_ppp(d);
+  const int target = std::max(1, grid / std::max(1, nq));
+  int passes = (L + ppp * target - 1) / (ppp * target);
+  passes = std::min(dec::MAXPASS, std::max(1, passes));
+  *cl = passes * ppp;
+  *nchunk = (L + *cl - 1) / *cl;
+}
 
 static DecodeWs decode_ws_layout(const vt_shard_spec& s, int32_t max_ctx) {
   const vt_shard_info& in = s.info;
   const int d = s.dims.head_dim;
-  const int G = s.dims.n_heads / s.dims.n_kv_heads;
-  const int64_t nchunk = (max_ctx + attn_chunk(d) - 1) / attn_chunk(d);
+  const int64_t nchunk = (max_ctx + dec::attn_ppp(d) - 1) / dec::attn_ppp(d);
   DecodeWs w{};
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -586,11 +856,12 @@ static DecodeWs decode_ws_layout(const vt_shard_spec& s, int32_t max_ctx) {
     off += static_cast<size_t>(round_up(static_cast<int64_t>(bytes), 256));
     return at;
   };
-  w.sync = take(sizeof(unsigned) * (dec::SW_GROUP + in.n_kv_heads + 16));
+  w.sync = take(sizeof(unsigned) * (dec::SW_GROUP + (in.n_q_heads + 1) * dec::SW_GROUP_STRIDE));
   w.qkv = take(sizeof(float) * (in.n_q_heads + 2 * in.n_kv_heads) * d);
-  w.part = take(sizeof(float) * in.n_kv_heads * nchunk * G * (d + dec::REC));
+  w.part = take(sizeof(float) * in.n_q_heads * nchunk * (d + dec::REC));
   w.o = take(sizeof(float) * in.n_q_heads * d);
   w.m = take(sizeof(float) * (in.n_cols + 8));
+  w.hbuf = take(sizeof(float) * s.dims.hidden);
   w.total = off;
   return w;
 }
@@ -603,8 +874,11 @@ vt_status check_weights(const vt_shard_spec& s, const vt_layer_weights* w, bool 
   if (!w) return fail(VT_ERR_ARG, "null weights");
   const int H = s.dims.hidden, d = s.dims.head_dim;
   const vt_shard_info& in = s.info;
-  auto mat = [&](const void* p, int64_t ld, int64_t rowlen, const char* name) -> vt_status {
+  auto mat = [&](const void* p, int64_t ld, int64_t rowlen, int64_t rows, const char* name) -> vt_status {
     if (!p) return fail(VT_ERR_ARG, "weight %s is NULL", name);
+    if (rows * ld * 2 >= kMaxBufferBytes)
+      return fail(VT_ERR_UNSUPPORTED, "weight %s spans %lld bytes; the kernels address < 2 GiB", name,
+                  static_cast<long long>(rows * ld * 2));
     if (!aligned16(p)) return fail(VT_ERR_ALIGN, "weight %s is not 16-byte aligned", name);
     if (ld < rowlen) return fail(VT_ERR_ARG, "ld of %s (%lld) < row length %lld", name,
                                  static_cast<long long>(ld), static_cast<long long>(rowlen));
@@ -621,19 +895,20 @@ vt_status check_weights(const vt_shard_spec& s, const vt_layer_weights* w, bool 
   if (attn) {
     if ((st = gain(w->g_attn, "g_attn")) != VT_OK) return st;
     if (in.n_q_heads > 0) {
-      if ((st = mat(w->wq, w->ld_q, H, "wq")) != VT_OK) return st;
-      if ((st = mat(w->wk, w->ld_k, H, "wk")) != VT_OK) return st;
-      if ((st = mat(w->wv, w->ld_v, H, "wv")) != VT_OK) return st;
-      if ((st = mat(w->wo, w->ld_o, static_cast<int64_t>(in.n_q_heads) * d, "wo")) != VT_OK)
-        return st;
+      const int64_t qd = static_cast<int64_t>(in.n_q_heads) * d;
+      const int64_t kd = static_cast<int64_t>(in.n_kv_heads) * d;
+      if ((st = mat(w->wq, w->ld_q, H, qd, "wq")) != VT_OK) return st;
+      if ((st = mat(w->wk, w->ld_k, H, kd, "wk")) != VT_OK) return st;
+      if ((st = mat(w->wv, w->ld_v, H, kd, "wv")) != VT_OK) return st;
+      if ((st = mat(w->wo, w->ld_o, qd, H, "wo")) != VT_OK) return st;
     }
   }
   if (ffn) {
     if ((st = gain(w->g_ffn, "g_ffn")) != VT_OK) return st;
     if (in.n_cols > 0) {
-      if ((st = mat(w->wg, w->ld_g, H, "wg")) != VT_OK) return st;
-      if ((st = mat(w->wu, w->ld_u, H, "wu")) != VT_OK) return st;
-      if ((st = mat(w->wd, w->ld_d, in.n_cols, "wd")) != VT_OK) return st;
+      if ((st = mat(w->wg, w->ld_g, H, in.n_cols, "wg")) != VT_OK) return st;
+      if ((st = mat(w->wu, w->ld_u, H, in.n_cols, "wu")) != VT_OK) return st;
+      if ((st = mat(w->wd, w->ld_d, in.n_cols, H, "wd")) != VT_OK) return st;
     }
   }
   return VT_OK;
@@ -646,6 +921,9 @@ vt_status check_kv(const vt_shard_spec& s, const vt_kv_view* kv, int32_t pos, in
                 kv->head_dim, s.info.n_kv_heads, s.dims.head_dim);
   if (kv->capacity < 1 || kv->len < 0 || kv->len > kv->capacity)
     return fail(VT_ERR_ARG, "KV view capacity %d / len %d invalid", kv->capacity, kv->len);
+  if (static_cast<int64_t>(kv->n_kv_heads) * kv->capacity * kv->head_dim * 2 >= kMaxBufferBytes)
+    return fail(VT_ERR_UNSUPPORTED, "KV cache of %d heads x %d positions exceeds 2 GiB per tensor",
+                kv->n_kv_heads, kv->capacity);
   if (s.info.n_kv_heads > 0) {
     if (!kv->k || !kv->v) return fail(VT_ERR_ARG, "KV buffers are NULL");
     if (!aligned16(kv->k) || !aligned16(kv->v)) return fail(VT_ERR_ALIGN, "KV buffers not 16-byte aligned");
@@ -742,8 +1020,7 @@ extern "C" vt_status vt_layer_decode(const vt_shard_spec* spec, const vt_layer_w
   P.ncols = in.n_cols;
   P.pos = pos;
   P.cap = kv ? kv->capacity : 0;
-  P.cl = attn_chunk(D.head_dim);
-  P.nchunk = (ctx + P.cl - 1) / P.cl;
+  attn_chunking(D.head_dim, in.n_q_heads, ctx, di->cus, &P.cl, &P.nchunk);
   P.eps = D.rms_eps;
   P.rope_base = D.rope_base;
   P.g_attn = static_cast<const uint16_t*>(w->g_attn);
@@ -764,6 +1041,9 @@ extern "C" vt_status vt_layer_decode(const vt_shard_spec* spec, const vt_layer_w
   P.ld_d = w->ld_d;
   P.kc = kv ? static_cast<uint16_t*>(kv->k) : nullptr;
   P.vc = kv ? static_cast<uint16_t*>(kv->v) : nullptr;
+  P.kv_bytes = kv ? static_cast<uint32_t>(static_cast<int64_t>(kv->n_kv_heads) * kv->capacity *
+                                          kv->head_dim * 2)
+                  : 0u;
   P.x = static_cast<const uint16_t*>(io->x);
   P.peer_a = static_cast<const uint16_t*>(io->peer_attn);
   P.peer_f = static_cast<const uint16_t*>(io->peer_ffn);
@@ -777,11 +1057,13 @@ extern "C" vt_status vt_layer_decode(const vt_shard_spec* spec, const vt_layer_w
   P.part = reinterpret_cast<float*>(base + L.part);
   P.o = reinterpret_cast<float*>(base + L.o);
   P.m = reinterpret_cast<float*>(base + L.m);
+  P.hbuf = reinterpret_cast<float*>(base + L.hbuf);
+  P.h_from_ws = attn ? 1 : 0;
 
   const int kmax = std::max({dec::padded(P.H), dec::padded(P.nq * P.d),
                              dec::padded(P.ncols)});
-  const int attn_f = P.G * P.d + P.G * P.cl + P.cl * P.d + 2 * P.d + 4;
-  const size_t lds = sizeof(float) * (std::max(kmax, attn_f) + dec::MAX_SLOTS + dec::NW);
+  const int attn_f = dec::attn_lds_floats(P.d, P.nchunk);
+  const size_t lds = sizeof(float) * (std::max(kmax / 2, attn_f) + dec::MAX_SLOTS + dec::NW);
   if (lds > di->max_lds)
     return fail(VT_ERR_UNSUPPORTED, "shape needs %zu bytes of LDS, device has %zu", lds, di->max_lds);
 
@@ -792,15 +1074,25 @@ extern "C" vt_status vt_layer_decode(const vt_shard_spec* spec, const vt_layer_w
   if (staged) {
     for (int ph = pb; ph <= pe && e == hipSuccess; ++ph) {
       P.phase_begin = P.phase_end = ph;
-      hipLaunchKernelGGL(dec::decode_kernel, dim3(di->cus), dim3(dec::NT), lds, s, P);
+      hipLaunchKernelGGL(dec::decode_kernel_for(ph, ph), dim3(di->cus), dim3(dec::NT), lds, s, P);
       e = hipGetLastError();
     }
   } else {
+    // The grid barrier needs every workgroup resident at once: one per CU,
+    // and the occupancy query confirms a CU holds at least one. A plain
+    // launch is used (the cooperative launch API adds ~20 us per launch);
+    // the barrier's bounded wait reports rather than hangs if another
+    // kernel were to hold CUs.
+    const dec::DecodeKernel kern = dec::decode_kernel_for(pb, pe);
+    int per_cu = 0;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, dec::NT, lds);
+    if (e != hipSuccess) return fail(VT_ERR_HIP, "occupancy query: %s", hipGetErrorString(e));
+    if (per_cu < 1)
+      return fail(VT_ERR_UNSUPPORTED, "decode kernel does not fit on a CU with %zu bytes of LDS", lds);
     P.phase_begin = pb;
     P.phase_end = pe;
-    void* args[] = {&P};
-    e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(dec::decode_kernel), dim3(di->cus),
-                                   dim3(dec::NT), args, static_cast<unsigned>(lds), s);
+    hipLaunchKernelGGL(kern, dim3(di->cus), dim3(dec::NT), lds, s, P);
+    e = hipGetLastError();
   }
   if (e != hipSuccess) return fail(VT_ERR_HIP, "decode launch: %s", hipGetErrorString(e));
   if (attn) kv->len = pos + 1;

@@ -11,6 +11,7 @@ constexpr int kWave = 64;
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float h2f(uint16_t u) {
@@ -40,6 +41,23 @@ __device__ __forceinline__ void unpack8(const u32x4 v, float (&o)[8]) {
   unpack2(v.w, o[6], o[7]);
 }
 
+// Raw buffer over [base, base + bytes), bytes < 2^31. A load whose per-lane
+// offset is >= bytes returns zero and touches no memory, which gives
+// branch-free masked loads (every lane issues, out-of-range lanes cost
+// nothing). Only the per-lane offset is range-checked: pass the whole
+// offset there and keep the scalar offset 0.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr uint32_t kOOB = 0x80000000u;  // an offset past every buffer
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0),
+                                           static_cast<int>(bytes), 0x00020000);
+}
+
+__device__ __forceinline__ u32x4 buf_load16(rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+}
+
 // Streaming 16-byte load of weights that are read exactly once per step.
 __device__ __forceinline__ u32x4 load_stream(const uint16_t* p) {
   return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
@@ -49,10 +67,25 @@ __device__ __forceinline__ u32x4 load16(const uint16_t* p) {
   return *reinterpret_cast<const u32x4*>(p);
 }
 
+// DPP move of a float across lanes (ctrl: DPP control word).
+template <int CTRL, int ROW_MASK = 0xF>
+__device__ __forceinline__ float dpp_f(float old, float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, old),
+                                                               __builtin_bit_cast(int, v), CTRL,
+                                                               ROW_MASK, 0xF, false));
+}
+
+// Sum over the 64 lanes of a wave; every lane gets the total. Quad swaps and
+// row mirrors give each 16-lane row its sum; the row broadcasts of lane 15
+// and lane 31 accumulate the rows into lane 63, which is then read out.
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
-  return v;
+  v += dpp_f<0xB1>(0.f, v);         // quad_perm [1,0,3,2]
+  v += dpp_f<0x4E>(0.f, v);         // quad_perm [2,3,0,1]
+  v += dpp_f<0x141>(0.f, v);        // row_half_mirror
+  v += dpp_f<0x140>(0.f, v);        // row_mirror
+  v += dpp_f<0x142, 0xA>(0.f, v);   // row_bcast:15 into rows 1 and 3
+  v += dpp_f<0x143, 0xC>(0.f, v);   // row_bcast:31 into rows 2 and 3
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
 }
 
 __device__ __forceinline__ float wave_max(float v) {
@@ -95,17 +128,44 @@ __device__ __forceinline__ void rope_angle(int pos, int i, int d, float base, fl
   c = __builtin_amdgcn_cosf(r);
 }
 
+// ---- data shared between workgroups of one launch ---------------------------
+// Agent-scope relaxed atomic stores and loads are performed at the level that
+// all XCDs share (they bypass each XCD's non-coherent L2). Data that one
+// workgroup writes and another reads within a launch moves only through
+// them, so a grid barrier needs no L2 writeback or invalidate: the writer
+// waits for its stores to complete, then bumps a counter.
+__device__ __forceinline__ void st_shared(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ float ld_shared(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Two consecutive floats (8-byte aligned) written by other workgroups.
+__device__ __forceinline__ void ld_shared2(const float* p, float& a, float& b) {
+  const uint64_t v = __hip_atomic_load(reinterpret_cast<const uint64_t*>(p), __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+  a = __builtin_bit_cast(float, static_cast<uint32_t>(v));
+  b = __builtin_bit_cast(float, static_cast<uint32_t>(v >> 32));
+}
+
+// Workgroup barrier that orders LDS accesses only: global loads still in
+// flight stay in flight across it.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Wait for all of this wave's outstanding memory operations (stores
+// included) to complete.
+__device__ __forceinline__ void mem_done() { __builtin_amdgcn_s_waitcnt(0); }
+
 // ---- synchronisation words (agent scope: visible across all XCDs) --------
-__device__ __forceinline__ unsigned sync_load(const unsigned* p) {
-  return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-__device__ __forceinline__ unsigned sync_add(unsigned* p, unsigned v) {
-  return __hip_atomic_fetch_add(p, v, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-}
-
+// Relaxed: the data they guard moves through st_shared / ld_shared.
 __device__ __forceinline__ void sync_store(unsigned* p, unsigned v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 __device__ __forceinline__ void sync_or(unsigned* p, unsigned v) {

@@ -17,6 +17,9 @@ namespace vt {
 vt_status fail(vt_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
 void clear_error();
 
+// Every buffer a kernel addresses through a buffer resource stays below 2 GiB.
+constexpr int64_t kMaxBufferBytes = int64_t(1) << 31;
+
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 // Checks shared by the decode and prefill entry points.

@@ -40,6 +40,8 @@ vt_status check_layer_dims(const vt_layer_dims& d) {
     return fail(VT_ERR_UNSUPPORTED, "head_dim %d: only 64 and 128 are supported", d.head_dim);
   if (d.hidden % 8)
     return fail(VT_ERR_UNSUPPORTED, "hidden %d must be a multiple of 8", d.hidden);
+  if (d.hidden > 16384)
+    return fail(VT_ERR_UNSUPPORTED, "hidden %d exceeds 16384", d.hidden);
   if (!(d.rms_eps >= 0.0f) || !std::isfinite(d.rms_eps))
     return fail(VT_ERR_ARG, "rms_eps must be finite and >= 0");
   if (!(d.rope_base > 0.0f) || !std::isfinite(d.rope_base))

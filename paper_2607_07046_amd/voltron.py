@@ -112,8 +112,7 @@ def load_library(path=None):
     lib.vt_status_string.restype = ctypes.c_char_p
     lib.vt_last_error.argtypes = []
     lib.vt_last_error.restype = ctypes.c_char_p
-    if path is None:
-        _lib = lib
+    _lib = lib
     return lib
 
 

@@ -85,8 +85,10 @@ class GpuShard:
         return {k: v.float().cpu().numpy().astype(np.float64) for k, v in out.items()}
 
     def sync_words(self):
-        """The workspace's synchronisation words (must be zero between calls)."""
-        return self.ws[:64].view(torch.int32).cpu().numpy()
+        """The workspace's synchronisation words (must be zero between calls):
+        barrier, exit and error words and one counter per query head."""
+        n = 3072 + 32 * (self.info.n_q_heads + 1)
+        return self.ws[:4 * n].view(torch.int32).cpu().numpy()
 
     def cache(self):
         return (self.kc.view(torch.int16).cpu().numpy(), self.vc.view(torch.int16).cpu().numpy())
