@@ -45,6 +45,34 @@ def algorithmic_bytes(dims, info, pos):
     return weights + kv + vectors
 
 
+PROFILE = os.path.join(ROOT, "profiles", "decode_kernel_7b_shard30.md")
+
+
+def kernel_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("decode.hip", "device.hpp"):
+        with open(os.path.join(ROOT, "paper_2607_07046_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or
+    None if the kernel sources changed since the counters were taken."""
+    import re
+    try:
+        with open(PROFILE) as f:
+            txt = f.read()
+    except OSError:
+        return None
+    m_hash = re.search(r"first 16 hex\): `([0-9a-f]{16})`", txt)
+    m_traffic = re.search(r"\*\*([0-9,]+) B\*\*", txt)
+    if not m_hash or not m_traffic or m_hash.group(1) != kernel_source_hash():
+        return None
+    return int(m_traffic.group(1).replace(",", ""))
+
+
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -56,11 +84,29 @@ def parse():
     ap.add_argument("--eager", action="store_true", help="no HIP graph")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="host time budget of the oracle baseline (0: skip)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="instead of the bench: copy MIB MiB device-to-device 10 times "
+                         "(the known-size kernel that scales the HBM byte counters)")
     return ap.parse_args()
+
+
+def copy_calibration(mib):
+    import torch
+    n = mib * 2 ** 20 // 2
+    src = torch.ones(n, dtype=torch.float16, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(10):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_read_per_launch": n * 2,
+                      "bytes_written_per_launch": n * 2, "launches": 10}))
 
 
 def main():
     args = parse()
+    if args.copy_calibration:
+        return copy_calibration(args.copy_calibration)
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only: the cross-device "
                                    "reduction is replaced by returning the shard's partial "
@@ -213,7 +259,8 @@ def main():
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": round(gbps / HBM_PEAK_GBPS, 4),
-            "traffic": None,
+            "traffic": (measured_traffic() if (wl.key == "7b" and not args.staged) else None),
+            "traffic_unit": "B per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-scaled)",
             "launches_per_step": n_launch,
         },
         "setup_s": round(setup_s, 1),
