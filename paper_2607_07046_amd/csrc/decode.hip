@@ -870,6 +870,10 @@ size_t decode_workspace_bytes(const vt_shard_spec& s, int32_t max_ctx) {
   return decode_ws_layout(s, max_ctx).total;
 }
 
+// The synchronisation words sit at the start of the workspace; every other
+// entry point keeps its buffers past them.
+size_t workspace_sync_bytes(const vt_shard_spec& s) { return decode_ws_layout(s, 1).qkv; }
+
 vt_status check_weights(const vt_shard_spec& s, const vt_layer_weights* w, bool attn, bool ffn) {
   if (!w) return fail(VT_ERR_ARG, "null weights");
   const int H = s.dims.hidden, d = s.dims.head_dim;

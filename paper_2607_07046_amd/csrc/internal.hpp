@@ -32,4 +32,7 @@ vt_status check_kv(const vt_shard_spec& s, const vt_kv_view* kv, int32_t pos, in
 namespace vt {
 size_t decode_workspace_bytes(const vt_shard_spec& s, int32_t max_ctx);
 size_t prefill_workspace_bytes(const vt_shard_spec& s, int32_t max_tokens, int32_t max_ctx);
+// Leading workspace bytes that hold the decode kernel's synchronisation words
+// (zero between calls; no other entry point writes them).
+size_t workspace_sync_bytes(const vt_shard_spec& s);
 }  // namespace vt

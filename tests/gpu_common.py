@@ -84,6 +84,27 @@ class GpuShard:
         torch.cuda.synchronize()
         return {k: v.float().cpu().numpy().astype(np.float64) for k, v in out.items()}
 
+    def prefill(self, X, pos0=None, phases=vt.VT_ATTN | vt.VT_FFN, peer_attn=None,
+                peer_ffn=None, h_in=None):
+        """vt_layer_prefill_chunk of the [T][H] fp16 rows X at positions pos0.. ."""
+        H = self.dims.hidden
+        T = X.shape[0] if X is not None else h_in.shape[0]
+        pos0 = self.kv.len if pos0 is None else pos0
+        xt = h16(X) if X is not None else torch.zeros((T, H), dtype=torch.float16, device="cuda")
+        pa = h16(peer_attn) if peer_attn is not None else None
+        pf = h16(peer_ffn) if peer_ffn is not None else None
+        out = {k: torch.full((T, H), float("nan"), dtype=torch.float16, device="cuda")
+               for k in ("p_attn", "h", "p_ffn", "y")}
+        if h_in is not None:
+            out["h"] = h16(h_in)
+        io = vt.vt_layer_io(x=ptr(xt), peer_attn=ptr(pa), peer_ffn=ptr(pf),
+                            attn_partial=ptr(out["p_attn"]), h=ptr(out["h"]),
+                            ffn_partial=ptr(out["p_ffn"]), y=ptr(out["y"]))
+        vt.vt_layer_prefill_chunk(self.spec, self.w.struct, self.kv, io, T, pos0, phases,
+                                  ptr(self.ws), self.ws_bytes, None)
+        torch.cuda.synchronize()
+        return {k: v.float().cpu().numpy().astype(np.float64) for k, v in out.items()}
+
     def sync_words(self):
         """The workspace's synchronisation words (must be zero between calls):
         barrier, exit and error words and one counter per query head."""
