@@ -30,6 +30,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "decode-layer-shard tokens/s and achieved HBM GB/s (% of peak), 1 MI355X"
 HBM_PEAK_GBPS = 8000.0
+MFMA_F16_PEAK_TFLOPS = 2500.0  # dense fp16 matrix-core peak
 MALL_DEFEAT_BYTES = 768 * 2 ** 20
 
 
@@ -84,6 +85,8 @@ def parse():
     ap.add_argument("--eager", action="store_true", help="no HIP graph")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="host time budget of the oracle baseline (0: skip)")
+    ap.add_argument("--prefill-steps", type=int, default=200,
+                    help="timed prefill chunks of the prefill section (0: skip)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="instead of the bench: copy MIB MiB device-to-device 10 times "
                          "(the known-size kernel that scales the HBM byte counters)")
@@ -267,9 +270,135 @@ def main():
     }
     if graph_error:
         out["graph_error"] = graph_error
+    if args.prefill_steps > 0:
+        out["prefill"] = prefill_section(args.prefill_steps, max(1, args.prefill_steps // 10),
+                                         args.eager)
     if args.cpu_seconds > 0:
         out["cpu_baseline"] = cpu_baseline(wl, pos, args.cpu_seconds, step_bytes)
     print(json.dumps(out), flush=True)
+
+
+def prefill_flops(dims, info, T, pos0):
+    """Algorithmic flops of one prefill chunk: the five projection GEMMs and
+    causal attention (Q K^T and P V over keys 0..pos0+t for token t)."""
+    H, d = dims.hidden, dims.head_dim
+    nq, nkv, F = info.n_q_heads, info.n_kv_heads, info.n_cols
+    gemm = 2 * T * H * ((nq + 2 * nkv) * d + nq * d + 3 * F)
+    keys = T * pos0 + T * (T + 1) // 2
+    return gemm, 4 * d * nq * keys
+
+
+def prefill_bytes(dims, info, T, pos0):
+    """Bytes a prefill chunk must move: the shard weights once, the cached
+    K/V read and the chunk's K/V written, gains, X in and four [T][H]
+    outputs."""
+    H, d = dims.hidden, dims.head_dim
+    nq, nkv, F = info.n_q_heads, info.n_kv_heads, info.n_cols
+    weights = 2 * ((nq + 2 * nkv) * d * H + H * nq * d + 3 * F * H)
+    kv = 4 * nkv * d * (pos0 + T)
+    return weights + kv + 2 * H * 2 + 2 * T * H * 5
+
+
+def prefill_section(steps, warmup, eager=False):
+    """Prefill chunk of 256 tokens at positions 768..1023 through the 50%
+    shard of the 7B-shaped layer (four rotated weight/KV copies, >= 768 MB),
+    timed over ``steps`` chunks captured in HIP graphs."""
+    import torch
+
+    from paper_2607_07046_amd import pack
+    from paper_2607_07046_amd import voltron as vt
+    from synth import get
+    from synth.gen import LayerInputs
+
+    wl = get("7b_prefill")
+    dev = torch.device("cuda:0")
+    dims = vt.vt_layer_dims(hidden=wl.dims.hidden, n_heads=wl.dims.n_heads,
+                            n_kv_heads=wl.dims.n_kv_heads, head_dim=wl.dims.head_dim,
+                            ffn=wl.dims.ffn, rms_eps=wl.dims.rms_eps,
+                            rope_base=wl.dims.rope_base)
+    spec = vt.vt_shard_spec_create(dims, wl.fracs, wl.fracs, wl.device)
+    dims, info = vt.vt_shard_spec_query(spec)
+    T, pos0 = wl.chunk, wl.ctx
+    H, d, nkv, cap = dims.hidden, dims.head_dim, info.n_kv_heads, pos0 + T
+    gemm_flops, attn_flops = prefill_flops(dims, info, T, pos0)
+    nbytes = prefill_bytes(dims, info, T, pos0)
+    copies = max(1, math.ceil(MALL_DEFEAT_BYTES / nbytes))
+    layers = []
+    for c in range(copies):
+        li = LayerInputs(wl, layer=c)
+        w = pack.pack_shard(li, dims, info, dev)
+        kc = torch.zeros((nkv, cap, d), dtype=torch.float16, device=dev)
+        vc = torch.zeros_like(kc)
+        k, v = li.kv_context_heads(info.kv_head_begin, info.kv_head_begin + nkv)
+        kc[:, :pos0] = torch.from_numpy(k).to(dev)
+        vc[:, :pos0] = torch.from_numpy(v).to(dev)
+        kv = vt.vt_kv_view(k=kc.data_ptr(), v=vc.data_ptr(), capacity=cap, n_kv_heads=nkv,
+                           head_dim=d, len=pos0)
+        layers.append((w, kc, vc, kv))
+    X = torch.from_numpy(LayerInputs(wl).x_chunk(T)).to(dev)
+    outs = [torch.empty((T, H), dtype=torch.float16, device=dev) for _ in range(4)]
+    ws_bytes = vt.vt_workspace_size(spec, T, cap)
+    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device=dev)
+    io = vt.vt_layer_io(x=X.data_ptr(), peer_attn=None, peer_ffn=None,
+                        attn_partial=outs[0].data_ptr(), h=outs[1].data_ptr(),
+                        ffn_partial=outs[2].data_ptr(), y=outs[3].data_ptr())
+
+    def enqueue(i, stream):
+        w, _, _, kv = layers[i % copies]
+        kv.len = pos0  # every chunk re-runs positions pos0.. of its copy
+        vt.vt_layer_prefill_chunk(spec, w.struct, kv, io, T, pos0, vt.VT_ATTN | vt.VT_FFN,
+                                  ws.data_ptr(), ws_bytes, stream)
+
+    per_graph = copies * 4
+    reps = max(1, steps // per_graph)
+    if eager:
+        def run_reps(k):
+            for _ in range(k):
+                for i in range(per_graph):
+                    enqueue(i, torch.cuda.current_stream().cuda_stream)
+    else:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            s = torch.cuda.current_stream().cuda_stream
+            for i in range(per_graph):
+                enqueue(i, s)
+
+        def run_reps(k):
+            for _ in range(k):
+                g.replay()
+    run_reps(max(1, warmup // per_graph))
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    run_reps(reps)
+    end.record()
+    torch.cuda.synchronize()
+    n = reps * per_graph
+    ms = start.elapsed_time(end) / n
+    if not torch.isfinite(outs[3].float()).all():
+        raise SystemExit("non-finite prefill output")
+    flops = gemm_flops + attn_flops
+    return {
+        "workload": wl.key,
+        "shape": f"{T} tokens at positions {pos0}..{pos0 + T - 1}, {info.n_q_heads} q / "
+                 f"{nkv} kv heads, {info.n_cols} FFN cols, hidden {H}",
+        "chunks": n,
+        "weight_copies": copies,
+        "ms_per_chunk": round(ms, 6),
+        "tokens_s": round(T / (ms * 1e-3), 1),
+        "gflop_per_chunk": round(flops / 1e9, 3),
+        "gemm_gflop": round(gemm_flops / 1e9, 3),
+        "attention_gflop": round(attn_flops / 1e9, 3),
+        "tflops": round(flops / (ms * 1e-3) / 1e12, 2),
+        "mfma_peak_tflops": MFMA_F16_PEAK_TFLOPS,
+        "mfma_frac": round(flops / (ms * 1e-3) / 1e12 / MFMA_F16_PEAK_TFLOPS, 4),
+        "algorithmic_bytes": nbytes,
+        "hbm_GBps": round(nbytes / (ms * 1e-3) / 1e9, 1),
+        "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+        "bound_us": round(max(flops / (MFMA_F16_PEAK_TFLOPS * 1e12),
+                              nbytes / (HBM_PEAK_GBPS * 1e9)) * 1e6, 2),
+        "launch": "10 kernels per chunk, " + ("eager" if eager else "hipgraph"),
+    }
 
 
 def cpu_baseline(wl, pos, budget_s, step_bytes):

@@ -41,6 +41,11 @@ __device__ __forceinline__ void unpack8(const u32x4 v, float (&o)[8]) {
   unpack2(v.w, o[6], o[7]);
 }
 
+__device__ __forceinline__ u32x4 pack8(const uint16_t (&h)[8]) {
+  return u32x4{h[0] | (static_cast<unsigned>(h[1]) << 16), h[2] | (static_cast<unsigned>(h[3]) << 16),
+               h[4] | (static_cast<unsigned>(h[5]) << 16), h[6] | (static_cast<unsigned>(h[7]) << 16)};
+}
+
 // Raw buffer over [base, base + bytes), bytes < 2^31. A load whose per-lane
 // offset is >= bytes returns zero and touches no memory, which gives
 // branch-free masked loads (every lane issues, out-of-range lanes cost

@@ -19,6 +19,8 @@
 
 #include <algorithm>
 #include <cmath>
+#include <mutex>
+#include <vector>
 
 #include "device.hpp"
 #include "internal.hpp"
@@ -46,153 +48,206 @@ __device__ __forceinline__ u32x4 mask_cols(u32x4 w, int col, int K) {
 }
 
 // ---------------------------------------------------------------------------
-// GEMM  C[M][N] = A[M][K] . B[N][K]^T  (fp16 in, fp32 accumulate)
-// B's rows come from two matrices: rows < n1 from B1, the rest from B2.
-// Tile 128 x 128 x 32 per 256-thread workgroup; each of the four waves owns a
-// 64 x 64 quarter as 2 x 2 MFMA tiles. A and B tiles pass through LDS (rows
-// padded by 8 halves); the next k-tile is loaded into registers while the
-// current one is multiplied.
+// Split-K GEMM   P[s][m][n] = sum over k-slice s of A[m][k] * B[n][k]
+// (fp16 in, fp32 out). M is the chunk's tokens, N the shard's output
+// features, K the input features (a multiple of 8; both operands hold finite
+// values, zeros in A, in the columns up to it). The weights (B) are the large
+// operand and are streamed once; A is small and re-read from L2 by every N
+// tile. The K range is cut into ``splits`` slices so that one launch has
+// about one workgroup per compute unit; each slice writes its own fp32 slab
+// and the consumer kernel adds the slabs (no atomics, fixed summation order).
+//
+// Tile 256 tokens x 128 features x 64 k per 256-thread workgroup. Wave w
+// owns tokens 64w..64w+63 and all 128 features as 2 x 4 MFMA tiles (32 x 32
+// x 16 fp16). Two LDS stages (rows padded by 8 halves) and two register
+// stages: the loads of k-tile i+2 are issued before k-tile i is multiplied.
+// Every load is unconditional (out-of-range lanes use an offset past the
+// buffer and read zero), so the compiler's wait counts stay exact.
+//
+// B's rows come from up to three matrices (e.g. Wq, Wk, Wv) placed at
+// 8-row-aligned starts of a virtual row space (rows between them read as
+// zero). A wave loads 8 consecutive 8-aligned rows per instruction, so each
+// load has one source, chosen once per workgroup with scalar selects.
 // ---------------------------------------------------------------------------
-constexpr int BM = 128, BN = 128, BK = 32, LDK = BK + 8, GT = 256;
+constexpr int GBM = 256, GBN = 128, GBK = 64, GLD = GBK + 8, GT = 256;
+constexpr int A_CH = GBM * GBK / 8 / GT;   // 16-byte A chunks per thread per k-tile
+constexpr int B_CH = GBN * GBK / 8 / GT;   // 16-byte B chunks per thread per k-tile
+constexpr int STAGE = (GBM + GBN) * GLD;   // halves per LDS stage
+constexpr int GEMM_LDS_BYTES = 2 * STAGE * 2;
+constexpr int GEMM_TARGET_WGS = 256;       // one workgroup per compute unit
+constexpr int MAX_SPLITS = 8;
+
+struct BSrc {
+  const uint16_t* p;
+  int64_t ld;
+  int start, rows;  // virtual rows [start, start + rows); start a multiple of 8
+};
 
 struct GemmArgs {
   const uint16_t* A;
   int64_t lda;
-  const uint16_t* B1;
-  int64_t ldb1;
-  int n1;
-  const uint16_t* B2;
-  int64_t ldb2;
+  BSrc b[3];
+  int nb;
+  float* P;
+  int64_t ldp, slab;
   int M, N, K;
-  int m_tiles, n_tiles;
+  int m_tiles, n_tiles, splits, kps;  // kps: k-tiles per split
 };
 
-template <class Epi>
-__global__ void __launch_bounds__(GT) gemm_kernel(GemmArgs g, Epi epi) {
-  __shared__ __attribute__((aligned(16))) uint16_t As[BM * LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[BN * LDK];
-  // Workgroups with equal index mod 8 run on one XCD: give the M tiles of an
-  // N tile indices that differ by multiples of 8, so B is fetched once into
-  // that XCD's L2.
+__global__ void __launch_bounds__(GT) gemm_kernel(GemmArgs g) {
+  extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
+  // Workgroups with equal index mod 8 run on one XCD: the M tiles of one
+  // (N tile, split) pair get indices that differ by multiples of 8, so their
+  // B slice is fetched once into that XCD's L2.
   const int id = blockIdx.x;
   const int slot = id / 8;
-  const int n_tile = (slot / g.m_tiles) * 8 + id % 8;
+  const int unit = (slot / g.m_tiles) * 8 + id % 8;
   const int m_tile = slot % g.m_tiles;
-  if (n_tile >= g.n_tiles) return;
-  const int m0 = m_tile * BM, n0 = n_tile * BN;
-  const int t = threadIdx.x, lane = t % kWave, wave = t / kWave;
-  const int wm = wave / 2, wn = wave % 2;
+  if (unit >= g.n_tiles * g.splits) return;
+  const int n_tile = unit % g.n_tiles, split = unit / g.n_tiles;
+  const int m0 = m_tile * GBM, n0 = n_tile * GBN;
+  const int t = threadIdx.x, lane = t % kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(t / kWave);
+  const int KT = (g.K + GBK - 1) / GBK;
+  const int kt0 = split * g.kps;
+  const int kt_end = min(kt0 + g.kps, KT);
+  const int nkt = kt_end - kt0;
 
+  rsrc_t rs[3];
+#pragma unroll
+  for (int j = 0; j < 3; ++j)
+    rs[j] = make_rsrc(g.b[j].p, static_cast<uint32_t>(j < g.nb ? g.b[j].rows * g.b[j].ld * 2 : 0));
   const rsrc_t ra = make_rsrc(g.A, static_cast<uint32_t>(g.M * g.lda * 2));
-  const rsrc_t rb1 = make_rsrc(g.B1, static_cast<uint32_t>(g.n1 * g.ldb1 * 2));
-  const rsrc_t rb2 =
-      make_rsrc(g.B2, static_cast<uint32_t>(static_cast<int64_t>(g.N - g.n1) * g.ldb2 * 2));
-  // This thread's two 16-byte chunks of each tile: row id/4, column (id%4)*8.
-  int arow[2], brow[2], ccol[2];
+
+  // k-independent part of each chunk's offset; kOOB marks a row past its source
+  const int ccol = (t % 8) * 8;
+  uint32_t aoff[A_CH], boff[B_CH];
+  rsrc_t rsel[B_CH];
 #pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    const int cid = t + u * GT;
-    arow[u] = cid / 4;
-    brow[u] = cid / 4;
-    ccol[u] = (cid % 4) * 8;
+  for (int u = 0; u < A_CH; ++u) {
+    const int m = m0 + (t + u * GT) / 8;
+    aoff[u] = m < g.M ? static_cast<uint32_t>(m * g.lda * 2) : kOOB;
   }
-  auto load_a = [&](int k0, int u) -> u32x4 {
-    const int m = m0 + arow[u], k = k0 + ccol[u];
-    const bool ok = m < g.M && k < g.K;
-    const uint32_t off = ok ? static_cast<uint32_t>((m * g.lda + k) * 2) : kOOB;
-    return mask_cols(buf_load16(ra, off), k, g.K);
+#pragma unroll
+  for (int u = 0; u < B_CH; ++u) {
+    const int r0 = n0 + wave * 8 + u * 32;  // first row of this wave's 8-row group (uniform)
+    int j = 2;
+    if (r0 < g.b[1].start || g.nb < 2) j = 0;
+    else if (r0 < g.b[2].start || g.nb < 3) j = 1;
+    const BSrc src = j == 0 ? g.b[0] : (j == 1 ? g.b[1] : g.b[2]);
+    rsel[u] = j == 0 ? rs[0] : (j == 1 ? rs[1] : rs[2]);
+    const int n = n0 + (t + u * GT) / 8;
+    const int r = n - src.start;
+    boff[u] = (n < g.N && r >= 0 && r < src.rows) ? static_cast<uint32_t>(r * src.ld * 2) : kOOB;
+  }
+
+  // k-tile kt into registers; tiles past this split's range read as zero
+  auto load = [&](int kt, u32x4 (&va)[A_CH], u32x4 (&vb)[B_CH]) {
+    const int k = kt * GBK + ccol;
+    const bool kin = kt < kt_end && k < g.K;
+#pragma unroll
+    for (int u = 0; u < A_CH; ++u)
+      va[u] = buf_load16(ra, kin && aoff[u] != kOOB ? aoff[u] + k * 2 : kOOB);
+#pragma unroll
+    for (int u = 0; u < B_CH; ++u)
+      vb[u] = buf_load16(rsel[u], kin && boff[u] != kOOB ? boff[u] + k * 2 : kOOB);
   };
-  auto load_b = [&](int k0, int u) -> u32x4 {
-    const int n = n0 + brow[u], k = k0 + ccol[u];
-    const bool ok = n < g.N && k < g.K;
-    const bool first = n < g.n1;
-    const int64_t row = first ? n : n - g.n1;
-    const int64_t ld = first ? g.ldb1 : g.ldb2;
-    const uint32_t off = ok ? static_cast<uint32_t>((row * ld + k) * 2) : kOOB;
-    const u32x4 v = first ? buf_load16(rb1, off) : buf_load16(rb2, off);
-    return mask_cols(v, k, g.K);
+  auto store = [&](uint16_t* st, const u32x4 (&va)[A_CH], const u32x4 (&vb)[B_CH]) {
+#pragma unroll
+    for (int u = 0; u < A_CH; ++u)
+      *reinterpret_cast<u32x4*>(st + ((t + u * GT) / 8) * GLD + ccol) = va[u];
+#pragma unroll
+    for (int u = 0; u < B_CH; ++u)
+      *reinterpret_cast<u32x4*>(st + (GBM + (t + u * GT) / 8) * GLD + ccol) = vb[u];
   };
 
-  f32x16 acc[2][2];
+  f32x16 acc[2][4];
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
+    for (int b = 0; b < 4; ++b) acc[a][b] = f32x16{};
 
-  u32x4 ra_n[2], rb_n[2];
+  auto compute = [&](const uint16_t* st) {
 #pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    ra_n[u] = load_a(0, u);
-    rb_n[u] = load_b(0, u);
-  }
-  for (int k0 = 0; k0 < g.K; k0 += BK) {
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      *reinterpret_cast<u32x4*>(As + arow[u] * LDK + ccol[u]) = ra_n[u];
-      *reinterpret_cast<u32x4*>(Bs + brow[u] * LDK + ccol[u]) = rb_n[u];
-    }
-    __syncthreads();
-    if (k0 + BK < g.K) {
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        ra_n[u] = load_a(k0 + BK, u);
-        rb_n[u] = load_b(k0 + BK, u);
-      }
-    }
-#pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      u32x4 af[2], bf[2];
+    for (int ks = 0; ks < GBK / 16; ++ks) {
+      const int kc = ks * 16 + 8 * (lane / 32);
+      u32x4 af[2], bf[4];
 #pragma unroll
       for (int a = 0; a < 2; ++a)
-        af[a] = *reinterpret_cast<const u32x4*>(As + (wm * 64 + a * 32 + lane % 32) * LDK + ks * 16 +
-                                                8 * (lane / 32));
+        af[a] = *reinterpret_cast<const u32x4*>(st + (wave * 64 + a * 32 + lane % 32) * GLD + kc);
 #pragma unroll
-      for (int b = 0; b < 2; ++b)
-        bf[b] = *reinterpret_cast<const u32x4*>(Bs + (wn * 64 + b * 32 + lane % 32) * LDK + ks * 16 +
-                                                8 * (lane / 32));
+      for (int b = 0; b < 4; ++b)
+        bf[b] = *reinterpret_cast<const u32x4*>(st + (GBM + b * 32 + lane % 32) * GLD + kc);
 #pragma unroll
       for (int a = 0; a < 2; ++a)
 #pragma unroll
-        for (int b = 0; b < 2; ++b) acc[a][b] = mfma32(af[a], bf[b], acc[a][b]);
+        for (int b = 0; b < 4; ++b) acc[a][b] = mfma32(af[a], bf[b], acc[a][b]);
     }
+  };
+
+  uint16_t* L0 = lds;
+  uint16_t* L1 = lds + STAGE;
+  u32x4 ra0[A_CH], rb0[B_CH], ra1[A_CH], rb1[B_CH];
+  load(kt0, ra0, rb0);
+  load(kt0 + 1, ra1, rb1);
+  store(L0, ra0, rb0);
+  __syncthreads();
+  // two k-tiles per trip; an odd count runs one all-zero tile at the end
+  // (the scheduling barriers keep the prefetch loads ahead of the MFMAs)
+  for (int i = 0; i < nkt; i += 2) {
+    load(kt0 + i + 2, ra0, rb0);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(L0);
+    store(L1, ra1, rb1);
+    __syncthreads();
+    load(kt0 + i + 3, ra1, rb1);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(L1);
+    store(L0, ra0, rb0);
     __syncthreads();
   }
-  // accumulator i of lane l holds row 8(i/4) + 4(l/32) + i%4, column l%32
+
+  // accumulator i of tile (a, b): token 8(i/4) + 4(l/32) + i%4, feature l%32
+  float* out = g.P + split * g.slab;
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int b = 0; b < 4; ++b)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const int m = m0 + wm * 64 + a * 32 + 8 * (i / 4) + 4 * (lane / 32) + i % 4;
-        const int n = n0 + wn * 64 + b * 32 + lane % 32;
-        if (m < g.M && n < g.N) epi(m, n, acc[a][b][i]);
+        const int m = m0 + wave * 64 + a * 32 + 8 * (i / 4) + 4 * (lane / 32) + i % 4;
+        const int n = n0 + b * 32 + lane % 32;
+        if (m < g.M && n < g.N) out[m * g.ldp + n] = acc[a][b][i];
       }
 }
 
-struct EpiStoreF32 {  // C -> fp32 matrix with row stride ld
-  float* c;
-  int64_t ld;
-  __device__ void operator()(int m, int n, float v) const { c[m * ld + n] = v; }
-};
+// Sum over the S split-K slabs of 4 consecutive fp32 values at element i
+// (i a multiple of 4); all S loads are issued before the adds.
+template <int S>
+__device__ __forceinline__ f32x4 slab_sum4(const float* P, int64_t slab, int64_t i) {
+  f32x4 v[S];
+#pragma unroll
+  for (int s = 0; s < S; ++s) v[s] = *reinterpret_cast<const f32x4*>(P + s * slab + i);
+#pragma unroll
+  for (int s = 1; s < S; ++s) v[0] += v[s];
+  return v[0];
+}
 
-struct EpiResidual {  // partial -> fp16; out = base + partial + peer (fp16)
-  uint16_t* partial;
-  uint16_t* out;
-  const uint16_t* base;
-  const uint16_t* peer;
-  int64_t ld;
-  __device__ void operator()(int m, int n, float v) const {
-    const int64_t i = m * ld + n;
-    partial[i] = f2h(v);
-    if (out) out[i] = f2h(h2f(base[i]) + v + (peer ? h2f(peer[i]) : 0.f));
-  }
-};
+template <int S>
+__device__ __forceinline__ float slab_sum1(const float* P, int64_t slab, int64_t i) {
+  float v[S];
+#pragma unroll
+  for (int s = 0; s < S; ++s) v[s] = P[s * slab + i];
+#pragma unroll
+  for (int s = 1; s < S; ++s) v[0] += v[s];
+  return v[0];
+}
 
 // ---------------------------------------------------------------------------
 // row-wise helpers
 // ---------------------------------------------------------------------------
 constexpr int RT = 256;
+constexpr int RMAX = 16384 / 8 / RT;  // 16-byte chunks per thread at the largest hidden size
 
 // U[t] = fp16(X[t] / sqrt(mean(X[t]^2) + eps) * g), one workgroup per row.
 __global__ void __launch_bounds__(RT) rmsnorm_rows_kernel(const uint16_t* X, const uint16_t* g,
@@ -213,61 +268,138 @@ __global__ void __launch_bounds__(RT) rmsnorm_rows_kernel(const uint16_t* X, con
     float f[8], gg[8];
     unpack8(load16(x + k8 * 8), f);
     unpack8(load16(g + k8 * 8), gg);
-    u32x4 o;
     uint16_t h[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) h[e] = f2h(f[e] * rstd * gg[e]);
-    o.x = h[0] | (static_cast<unsigned>(h[1]) << 16);
-    o.y = h[2] | (static_cast<unsigned>(h[3]) << 16);
-    o.z = h[4] | (static_cast<unsigned>(h[5]) << 16);
-    o.w = h[6] | (static_cast<unsigned>(h[7]) << 16);
-    *reinterpret_cast<u32x4*>(u + k8 * 8) = o;
+    *reinterpret_cast<u32x4*>(u + k8 * 8) = pack8(h);
   }
+}
+
+// Residual epilogue of an output projection, one workgroup per token row t:
+// p = sum of the slabs, partial[t] = fp16(p), out[t] = fp16(base[t] + p +
+// peer[t]) (out may be NULL). With NORM also U[t] = fp16(RMSNorm(out[t]) * g),
+// the next sub-layer's normalised input, taken from the fp16-rounded row.
+template <bool NORM, int S>
+__device__ __forceinline__ void resid_body(const float* P, int64_t slab, const uint16_t* base,
+                                           const uint16_t* peer, uint16_t* partial, uint16_t* out,
+                                           const uint16_t* g, uint16_t* U, int H, float eps) {
+  __shared__ float red[RT / kWave];
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * H;
+  u32x4 hv[RMAX];
+  float ss = 0.f;
+#pragma unroll
+  for (int it = 0; it < RMAX; ++it) {
+    const int k8 = threadIdx.x + it * RT;
+    if (k8 >= H / 8) break;
+    const int64_t i = row + k8 * 8;
+    const f32x4 p0 = slab_sum4<S>(P, slab, i), p1 = slab_sum4<S>(P, slab, i + 4);
+    const float p[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+    float b[8], pe[8];
+    unpack8(load16(base + i), b);
+    if (peer) unpack8(load16(peer + i), pe);
+    uint16_t ph[8], oh[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      ph[e] = f2h(p[e]);
+      oh[e] = f2h(b[e] + p[e] + (peer ? pe[e] : 0.f));
+      const float o = h2f(oh[e]);
+      ss = fmaf(o, o, ss);
+    }
+    *reinterpret_cast<u32x4*>(partial + i) = pack8(ph);
+    hv[it] = pack8(oh);
+    if (out) *reinterpret_cast<u32x4*>(out + i) = hv[it];
+  }
+  if (!NORM) return;
+  ss = block_sum<RT>(ss, red);
+  const float rstd = 1.0f / sqrtf(ss / static_cast<float>(H) + eps);
+#pragma unroll
+  for (int it = 0; it < RMAX; ++it) {
+    const int k8 = threadIdx.x + it * RT;
+    if (k8 >= H / 8) break;
+    float f[8], gg[8];
+    unpack8(hv[it], f);
+    unpack8(load16(g + k8 * 8), gg);
+    uint16_t u[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) u[e] = f2h(f[e] * rstd * gg[e]);
+    *reinterpret_cast<u32x4*>(U + row + k8 * 8) = pack8(u);
+  }
+}
+
+template <int S>
+__global__ void __launch_bounds__(RT) resid_norm_kernel(const float* P, int64_t slab, const uint16_t* base,
+                                                        const uint16_t* peer, uint16_t* partial,
+                                                        uint16_t* out, const uint16_t* g, uint16_t* U,
+                                                        int H, float eps) {
+  resid_body<true, S>(P, slab, base, peer, partial, out, g, U, H, eps);
+}
+
+template <int S>
+__global__ void __launch_bounds__(RT) resid_only_kernel(const float* P, int64_t slab, const uint16_t* base,
+                                                        const uint16_t* peer, uint16_t* partial,
+                                                        uint16_t* out, const uint16_t* g, uint16_t* U,
+                                                        int H, float eps) {
+  resid_body<false, S>(P, slab, base, peer, partial, out, g, U, H, eps);
 }
 
 // From the raw projections QKV[t] = [q (nq*d) | k (nkv*d) | v (nkv*d)] of
-// token t at position pos0 + t: Q[t] = fp16(RoPE(q) / sqrt(d)); the rotated
-// k and v go to slot pos0 + t of each KV head. One workgroup per token.
-__global__ void __launch_bounds__(RT) rope_append_kernel(const float* QKV, int ldq, uint16_t* Q,
-                                                         uint16_t* kc, uint16_t* vc, int nq, int nkv,
-                                                         int d, int cap, int pos0, float base) {
+// token t at position pos0 + t (summed over the slabs): Q[t] = fp16(RoPE(q)
+// / sqrt(d)); the rotated k and v go to slot pos0 + t of each KV head. One
+// workgroup per token.
+template <int S>
+__global__ void __launch_bounds__(RT) rope_append_kernel(const float* P, int64_t slab, int ldq,
+                                                         uint16_t* Q, uint16_t* kc, uint16_t* vc, int nq,
+                                                         int nkv, int d, int cap, int pos0, float base) {
   const int t = blockIdx.x;
   const int pos = pos0 + t;
-  const float* row = QKV + static_cast<int64_t>(t) * ldq;
+  const int64_t row = static_cast<int64_t>(t) * ldq;
   const float scale = 1.0f / sqrtf(static_cast<float>(d));
-  const int half = d / 2;
-  for (int idx = threadIdx.x; idx < (nq + nkv) * half; idx += RT) {
-    const int head = idx / half, i = idx - head * half;
-    float c0, s0;
-    rope_angle(pos, i, d, base, c0, s0);
-    const float a = row[head * d + 2 * i], b = row[head * d + 2 * i + 1];
-    const float r0 = a * c0 - b * s0, r1 = a * s0 + b * c0;
+  // 4 consecutive values (2 rotary pairs) per step, d / 4 steps per head;
+  // RT is a multiple of d / 4, so a thread keeps one column group c4 for all
+  // its heads and evaluates its two angles once.
+  const int per_head = d / 4;
+  const int c4 = (threadIdx.x % per_head) * 4;
+  float ca, sa, cb, sb;
+  rope_angle(pos, c4 / 2, d, base, ca, sa);
+  rope_angle(pos, c4 / 2 + 1, d, base, cb, sb);
+  for (int head = threadIdx.x / per_head; head < nq + nkv; head += RT / per_head) {
+    const f32x4 v = slab_sum4<S>(P, slab, row + head * d + c4);
+    const float r0 = v.x * ca - v.y * sa, r1 = v.x * sa + v.y * ca;
+    const float r2 = v.z * cb - v.w * sb, r3 = v.z * sb + v.w * cb;
+    uint16_t* o;
+    float sc;
     if (head < nq) {
-      uint16_t* qo = Q + static_cast<int64_t>(t) * nq * d + head * d;
-      qo[2 * i] = f2h(r0 * scale);
-      qo[2 * i + 1] = f2h(r1 * scale);
+      o = Q + static_cast<int64_t>(t) * nq * d + head * d + c4;
+      sc = scale;
     } else {
-      const int g = head - nq;
-      uint16_t* ko = kc + (static_cast<int64_t>(g) * cap + pos) * d;
-      ko[2 * i] = f2h(r0);
-      ko[2 * i + 1] = f2h(r1);
+      o = kc + (static_cast<int64_t>(head - nq) * cap + pos) * d + c4;
+      sc = 1.f;
     }
+    const unsigned w0 = f2h(r0 * sc) | (static_cast<unsigned>(f2h(r1 * sc)) << 16);
+    const unsigned w1 = f2h(r2 * sc) | (static_cast<unsigned>(f2h(r3 * sc)) << 16);
+    *reinterpret_cast<uint2*>(o) = make_uint2(w0, w1);
   }
-  for (int idx = threadIdx.x; idx < nkv * d; idx += RT) {
-    const int g = idx / d, dd = idx - g * d;
-    vc[(static_cast<int64_t>(g) * cap + pos) * d + dd] = f2h(row[(nq + nkv) * d + idx]);
+  for (int idx = threadIdx.x; idx < nkv * d / 4; idx += RT) {
+    const int g = (idx * 4) / d, dd = idx * 4 - g * d;
+    const f32x4 v = slab_sum4<S>(P, slab, row + (nq + nkv) * d + idx * 4);
+    const unsigned w0 = f2h(v.x) | (static_cast<unsigned>(f2h(v.y)) << 16);
+    const unsigned w1 = f2h(v.z) | (static_cast<unsigned>(f2h(v.w)) << 16);
+    *reinterpret_cast<uint2*>(vc + (static_cast<int64_t>(g) * cap + pos) * d + dd) = make_uint2(w0, w1);
   }
 }
 
-// M[t][j] = fp16(silu(G[t][j]) * Up[t][j]) for j < F, zero for F <= j < ldm.
-__global__ void __launch_bounds__(RT) silu_gate_kernel(const float* GU, int ldgu, uint16_t* M, int F,
-                                                       int ldm) {
+// M[t][j] = fp16(silu(G[t][j]) * Up[t][j]) for j < F, zero for F <= j < ldm;
+// G and Up are columns j and up0 + j of the summed slabs (row stride ldp).
+template <int S>
+__global__ void __launch_bounds__(RT) silu_gate_kernel(const float* P, int64_t slab, int64_t ldp,
+                                                       int up0, uint16_t* M, int F, int ldm) {
   const int t = blockIdx.x;
-  const float* row = GU + static_cast<int64_t>(t) * ldgu;
+  const int64_t row = static_cast<int64_t>(t) * ldp;
   for (int j = threadIdx.x; j < ldm; j += RT) {
     float m = 0.f;
     if (j < F) {
-      const float gt = row[j], up = row[F + j];
+      const float gt = slab_sum1<S>(P, slab, row + j);
+      const float up = slab_sum1<S>(P, slab, row + up0 + j);
       m = gt / (1.0f + __expf(-gt)) * up;
     }
     M[static_cast<int64_t>(t) * ldm + j] = f2h(m);
@@ -277,32 +409,46 @@ __global__ void __launch_bounds__(RT) silu_gate_kernel(const float* GU, int ldgu
 // ---------------------------------------------------------------------------
 // Causal attention of the chunk (flash-style, MFMA)
 //
-// One wave per (query head j, block of 32 queries). Per block of 32 keys it
-// computes S^T = K_blk Q_blk^T with one 32x32 MFMA tile (K = head_dim), so
-// each lane owns one query (column) and 16 of the 32 keys; the partner lane
-// (l ^ 32) owns the other 16. The keys are staged into LDS with rows
-// permuted by swapping bits 2 and 3 of the row index: then the 8
-// accumulators a lane feeds into each P.V k-step are exactly the 8
-// consecutive keys the MFMA operand layout asks for, and the probabilities
-// go to the second MFMA (O^T += V_blk^T P^T) without any shuffle. V is
-// staged transposed ([dim][key]) for that MFMA's other operand. Softmax is
-// online across key blocks (running max and sum per query).
+// One workgroup of AW waves per (query head j, block of 32 queries); wave w
+// takes key blocks w, w + AW, ... and keeps its own online softmax (running
+// max and sum per query) and output; the AW partial results are merged
+// through LDS at the end. Per block of 32 keys a wave computes S^T = K_blk
+// Q_blk^T with one 32x32 MFMA tile (K = head_dim), so each lane owns one
+// query (column) and 16 of the 32 keys; the partner lane (l ^ 32) owns the
+// other 16. The keys are staged into the wave's LDS with rows permuted by
+// swapping bits 2 and 3 of the row index: then the 8 accumulators a lane
+// feeds into each P.V k-step are exactly the 8 consecutive keys the MFMA
+// operand layout asks for, and the probabilities go to the second MFMA
+// (O^T += V_blk^T P^T) without any shuffle. V is staged transposed
+// ([dim][key]) for that MFMA's other operand. A wave only touches its own
+// LDS region inside the loop, so the loop needs no workgroup barrier.
 // ---------------------------------------------------------------------------
-constexpr int QB = 32, KB = 32;
+constexpr int QB = 32, KB = 32, AW = 4;
 
 __device__ __forceinline__ int swap_bits23(int r) {
   return (r & ~0xC) | ((r & 4) << 1) | ((r & 8) >> 1);
 }
 
 template <int D>
-__global__ void __launch_bounds__(kWave) attn_prefill_kernel(const uint16_t* Q, uint16_t* O,
-                                                             const uint16_t* kc, const uint16_t* vc,
-                                                             int T, int nq, int G, int cap, int pos0) {
-  constexpr int KLD = D + 8;   // LDS row stride of the K tile (halves)
-  constexpr int VLD = KB + 8;  // LDS row stride of the transposed V tile
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[KB * KLD];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[D * VLD];
-  const int lane = threadIdx.x;
+struct AttnLds {
+  static constexpr int KLD = D + 8;   // row stride of the K tile (halves)
+  static constexpr int VLD = KB + 8;  // row stride of the transposed V tile
+  static constexpr int OLD = D + 4;   // row stride of a wave's fp32 output in the merge
+  static constexpr int WAVE_HALVES = KB * KLD + D * VLD;
+  static_assert(WAVE_HALVES * 2 >= (QB * OLD + 2 * QB) * 4, "merge buffer must fit a wave's region");
+};
+
+template <int D>
+__global__ void __launch_bounds__(AW * kWave) attn_prefill_kernel(const uint16_t* Q, uint16_t* O,
+                                                                  const uint16_t* kc, const uint16_t* vc,
+                                                                  int T, int nq, int G, int cap, int pos0) {
+  using LY = AttnLds<D>;
+  constexpr int KLD = LY::KLD, VLD = LY::VLD, OLD = LY::OLD;
+  __shared__ __attribute__((aligned(16))) uint16_t smem[AW * LY::WAVE_HALVES];
+  const int lane = threadIdx.x % kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  uint16_t* Ks = smem + wave * LY::WAVE_HALVES;
+  uint16_t* Vt = Ks + KB * KLD;
   const int nqb = (T + QB - 1) / QB;
   const int j = blockIdx.x / nqb, qb = blockIdx.x % nqb;
   const int g = j / G;
@@ -344,8 +490,8 @@ __global__ void __launch_bounds__(kWave) attn_prefill_kernel(const uint16_t* Q, 
       vreg[u] = load16(vbase + static_cast<int64_t>(p) * D + col);
     }
   };
-  fetch(0);
-  for (int kb = 0; kb < nkb; ++kb) {
+  fetch(min(wave, nkb - 1));
+  for (int kb = wave; kb < nkb; kb += AW) {
     const int p0 = kb * KB;
     // stage K (rows permuted) and V (transposed), then start the next block
 #pragma unroll
@@ -364,8 +510,11 @@ __global__ void __launch_bounds__(kWave) attn_prefill_kernel(const uint16_t* Q, 
 #pragma unroll
       for (int e = 0; e < 8; ++e) Vt[(col + e) * VLD + key] = vh[e];
     }
-    __syncthreads();
-    if (kb + 1 < nkb) fetch(kb + 1);
+    // LDS operations of one wave complete in issue order; this keeps the
+    // compiler from moving the tile reads above the writes
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    fetch(min(kb + AW, nkb - 1));
     // S^T (keys x queries)
     f32x16 s = f32x16{};
 #pragma unroll
@@ -417,16 +566,52 @@ __global__ void __launch_bounds__(kWave) attn_prefill_kernel(const uint16_t* Q, 
                                                          8 * (lane / 32));
         o[mt] = mfma32(vf, pf[s2], o[mt]);
       }
-    __syncthreads();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
   }
+
+  // merge the AW partial results: wave w's region holds its output O_w
+  // ([query][dim] fp32) and its running max and sum per query
+  __syncthreads();
+  float* Om = reinterpret_cast<float*>(Ks);
+  float* mlw = Om + QB * OLD;
   // O^T accumulator i of tile mt: dim 32 mt + 8(i/4) + 4(l/32) + i%4, query l%32
-  if (tq < T) {
-    const float inv = 1.0f / lrun;
-    uint16_t* orow = O + (static_cast<int64_t>(tq) * nq + j) * D;
 #pragma unroll
-    for (int mt = 0; mt < D / 32; ++mt)
+  for (int mt = 0; mt < D / 32; ++mt)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) orow[mt * 32 + 8 * (i / 4) + 4 * (lane / 32) + i % 4] = f2h(o[mt][i] * inv);
+    for (int i = 0; i < 16; ++i)
+      Om[(lane % 32) * OLD + mt * 32 + 8 * (i / 4) + 4 * (lane / 32) + i % 4] = o[mt][i];
+  if (lane < 32) {
+    mlw[lane] = mrun;
+    mlw[QB + lane] = lrun;
+  }
+  __syncthreads();
+  // thread -> (query, 8 consecutive dims)
+  constexpr int CPQ = D / 8;  // 8-dim chunks per query
+  for (int c = threadIdx.x; c < QB * CPQ; c += AW * kWave) {
+    const int q = c / CPQ, d0 = (c % CPQ) * 8;
+    if (t0 + q >= T) continue;
+    float mw[AW], mstar = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < AW; ++w) {
+      const float* mlv = reinterpret_cast<const float*>(smem + w * LY::WAVE_HALVES) + QB * OLD;
+      mw[w] = mlv[q];
+      mstar = fmaxf(mstar, mw[w]);
+    }
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f}, l = 0.f;
+#pragma unroll
+    for (int w = 0; w < AW; ++w) {
+      const float* ow = reinterpret_cast<const float*>(smem + w * LY::WAVE_HALVES);
+      const float sc = mw[w] == -INFINITY ? 0.f : __expf(mw[w] - mstar);
+      l += sc * ow[QB * OLD + QB + q];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] += sc * ow[q * OLD + d0 + e];
+    }
+    const float inv = 1.0f / l;
+    uint16_t h[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) h[e] = f2h(acc[e] * inv);
+    *reinterpret_cast<u32x4*>(O + (static_cast<int64_t>(t0 + q) * nq + j) * D + d0) = pack8(h);
   }
 }
 
@@ -437,8 +622,50 @@ __global__ void __launch_bounds__(kWave) attn_prefill_kernel(const uint16_t* Q, 
 // ---------------------------------------------------------------------------
 namespace {
 
+// Split-K choice of a GEMM: as many slices of whole k-tiles as keep one
+// launch at or below the target number of workgroups.
+struct Split {
+  int m_tiles, n_tiles, splits, kps;
+};
+
+Split choose_split(int M, int N, int K) {
+  Split s;
+  s.m_tiles = (M + pf::GBM - 1) / pf::GBM;
+  s.n_tiles = (N + pf::GBN - 1) / pf::GBN;
+  const int KT = std::max(1, (K + pf::GBK - 1) / pf::GBK);
+  const int tiles = std::max(1, s.m_tiles * s.n_tiles);
+  const int want = std::max(1, std::min({KT, pf::MAX_SPLITS, pf::GEMM_TARGET_WGS / tiles}));
+  s.kps = (KT + want - 1) / want;
+  s.splits = (KT + s.kps - 1) / s.kps;
+  return s;
+}
+
+// The shard's prefill GEMMs for T tokens: QKV, O, gate/up, down. N counts
+// virtual rows of B (the up rows start at the 8-aligned row after the gate
+// rows); K is rounded up to a multiple of 8 (the padding multiplies zeros).
+struct PrefillGemms {
+  int M, N[4], K[4], up0;
+};
+
+PrefillGemms prefill_gemms(const vt_shard_spec& s, int32_t T) {
+  const vt_shard_info& in = s.info;
+  const int H = s.dims.hidden, d = s.dims.head_dim;
+  PrefillGemms g;
+  g.M = T;
+  g.N[0] = (in.n_q_heads + 2 * in.n_kv_heads) * d;
+  g.K[0] = H;
+  g.N[1] = H;
+  g.K[1] = in.n_q_heads * d;
+  g.up0 = (in.n_cols + 7) / 8 * 8;
+  g.N[2] = g.up0 + in.n_cols;
+  g.K[2] = H;
+  g.N[3] = H;
+  g.K[3] = std::max(8, g.up0);
+  return g;
+}
+
 struct PrefillWs {
-  size_t u, qkv, q, o, gu, m, total;
+  size_t u, q, o, m, part, total;
 };
 
 inline int64_t rup(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
@@ -446,8 +673,13 @@ inline int64_t rup(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 PrefillWs prefill_layout(const vt_shard_spec& s, int32_t T) {
   const vt_shard_info& in = s.info;
   const int64_t H = s.dims.hidden, d = s.dims.head_dim;
-  const int64_t r0 = (in.n_q_heads + 2 * in.n_kv_heads) * d;
   const int64_t fpad = std::max<int64_t>(8, rup(in.n_cols, 8));
+  const PrefillGemms gm = prefill_gemms(s, T);
+  int64_t part = 0;  // one region serves the four GEMMs' slabs in turn
+  for (int i = 0; i < 4; ++i) {
+    const Split sp = choose_split(gm.M, gm.N[i], gm.K[i]);
+    part = std::max<int64_t>(part, static_cast<int64_t>(sp.splits) * T * gm.N[i] * 4);
+  }
   PrefillWs w{};
   size_t off = workspace_sync_bytes(s);  // leave the decode synchronisation words alone
   auto take = [&](int64_t bytes) {
@@ -456,26 +688,67 @@ PrefillWs prefill_layout(const vt_shard_spec& s, int32_t T) {
     return at;
   };
   w.u = take(2 * T * H);
-  w.qkv = take(4 * T * r0);
   w.q = take(2 * T * in.n_q_heads * d);
   w.o = take(2 * T * std::max<int64_t>(in.n_q_heads * d, 8));
-  w.gu = take(4 * T * 2 * in.n_cols);
   w.m = take(2 * T * fpad);
+  w.part = take(part);
   w.total = off;
   return w;
 }
 
-template <class Epi>
-vt_status launch_gemm(const pf::GemmArgs& a0, Epi epi, hipStream_t s) {
-  pf::GemmArgs a = a0;
-  a.m_tiles = (a.M + pf::BM - 1) / pf::BM;
-  a.n_tiles = (a.N + pf::BN - 1) / pf::BN;
+// Launches P = A B^T as split-K slabs; returns the slab count via *splits.
+vt_status launch_gemm(pf::GemmArgs a, float* P, hipStream_t s, int* splits) {
+  {
+    // the GEMM's dynamic LDS exceeds the default limit: raise it once per device
+    static std::mutex mu;
+    static std::vector<char> done;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(VT_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+    std::lock_guard<std::mutex> lk(mu);
+    if (static_cast<int>(done.size()) <= dev) done.resize(dev + 1, 0);
+    if (!done[dev]) {
+      e = hipFuncSetAttribute(reinterpret_cast<const void*>(pf::gemm_kernel),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, pf::GEMM_LDS_BYTES);
+      if (e != hipSuccess)
+        return fail(VT_ERR_HIP, "gemm LDS attribute: %s", hipGetErrorString(e));
+      done[dev] = 1;
+    }
+  }
+  const Split sp = choose_split(a.M, a.N, a.K);
+  a.m_tiles = sp.m_tiles;
+  a.n_tiles = sp.n_tiles;
+  a.splits = sp.splits;
+  a.kps = sp.kps;
+  a.P = P;
+  a.ldp = a.N;
+  a.slab = static_cast<int64_t>(a.M) * a.N;
+  *splits = sp.splits;
   if (a.M == 0 || a.N == 0) return VT_OK;
-  const int groups = (a.n_tiles + 7) / 8;
-  hipLaunchKernelGGL(pf::gemm_kernel<Epi>, dim3(groups * 8 * a.m_tiles), dim3(pf::GT), 0, s, a, epi);
+  const int units = sp.n_tiles * sp.splits;
+  const int groups = (units + 7) / 8;
+  hipLaunchKernelGGL(pf::gemm_kernel, dim3(groups * 8 * sp.m_tiles), dim3(pf::GT),
+                     pf::GEMM_LDS_BYTES, s, a);
   hipError_t e = hipGetLastError();
   return e == hipSuccess ? VT_OK : fail(VT_ERR_HIP, "gemm launch: %s", hipGetErrorString(e));
 }
+
+pf::BSrc bsrc(const void* p, int64_t ld, int start, int rows) {
+  return pf::BSrc{static_cast<const uint16_t*>(p), ld, start, rows};
+}
+
+// Launch helper for kernels templated on the split-K slab count.
+#define VT_SPLIT_DISPATCH(KERNEL, ...)                                           \
+  switch (splits) {                                                              \
+    case 1: hipLaunchKernelGGL(KERNEL<1>, __VA_ARGS__); break;                   \
+    case 2: hipLaunchKernelGGL(KERNEL<2>, __VA_ARGS__); break;                   \
+    case 3: hipLaunchKernelGGL(KERNEL<3>, __VA_ARGS__); break;                   \
+    case 4: hipLaunchKernelGGL(KERNEL<4>, __VA_ARGS__); break;                   \
+    case 5: hipLaunchKernelGGL(KERNEL<5>, __VA_ARGS__); break;                   \
+    case 6: hipLaunchKernelGGL(KERNEL<6>, __VA_ARGS__); break;                   \
+    case 7: hipLaunchKernelGGL(KERNEL<7>, __VA_ARGS__); break;                   \
+    default: hipLaunchKernelGGL(KERNEL<8>, __VA_ARGS__); break;                  \
+  }
 
 }  // namespace
 
@@ -523,7 +796,9 @@ extern "C" vt_status vt_layer_prefill_chunk(const vt_shard_spec* spec, const vt_
     return fail(VT_ERR_UNSUPPORTED, "prefill of a shard without heads");
   if (ffn && in.n_cols == 0)
     return fail(VT_ERR_UNSUPPORTED, "prefill of a shard without FFN columns");
-  if (static_cast<int64_t>(n_tok) * std::max<int64_t>(H, 2 * in.n_cols + 8) * 4 >= kMaxBufferBytes)
+  // activation operands of the GEMMs are read through 2 GiB buffer ranges
+  if (static_cast<int64_t>(n_tok) * std::max<int64_t>({H, in.n_q_heads * d, in.n_cols + 8}) * 2 >=
+      kMaxBufferBytes)
     return fail(VT_ERR_UNSUPPORTED, "chunk of %d tokens too large for 2 GiB activation buffers", n_tok);
   const PrefillWs L = prefill_layout(*spec, n_tok);
   if (!ws || ws_bytes < L.total)
@@ -532,113 +807,112 @@ extern "C" vt_status vt_layer_prefill_chunk(const vt_shard_spec* spec, const vt_
 
   char* base = static_cast<char*>(ws);
   uint16_t* U = reinterpret_cast<uint16_t*>(base + L.u);
-  float* QKV = reinterpret_cast<float*>(base + L.qkv);
   uint16_t* Qr = reinterpret_cast<uint16_t*>(base + L.q);
   uint16_t* Ob = reinterpret_cast<uint16_t*>(base + L.o);
-  float* GU = reinterpret_cast<float*>(base + L.gu);
   uint16_t* Mb = reinterpret_cast<uint16_t*>(base + L.m);
+  float* P = reinterpret_cast<float*>(base + L.part);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int nq = in.n_q_heads, nkv = in.n_kv_heads, F = in.n_cols;
   const int G = D.n_heads / D.n_kv_heads;
   const int64_t fpad = std::max<int64_t>(8, (F + 7) / 8 * 8);
-  hipError_t e;
+  const PrefillGemms gm = prefill_gemms(*spec, n_tok);
+  int splits = 1;
   auto check = [&](const char* what) -> vt_status {
-    e = hipGetLastError();
+    hipError_t e = hipGetLastError();
     return e == hipSuccess ? VT_OK : fail(VT_ERR_HIP, "%s launch: %s", what, hipGetErrorString(e));
   };
+  auto slab = [&](int i) { return static_cast<int64_t>(n_tok) * gm.N[i]; };
 
   if (attn) {
     hipLaunchKernelGGL(pf::rmsnorm_rows_kernel, dim3(n_tok), dim3(pf::RT), 0, s,
                        static_cast<const uint16_t*>(io->x), static_cast<const uint16_t*>(w->g_attn), U,
                        static_cast<int>(H), D.rms_eps);
     if ((st = check("rmsnorm")) != VT_OK) return st;
-    {
-      // The B operand takes rows from two matrices, so the projection runs
-      // as a [Wq; Wk] GEMM and a Wv GEMM into one fp32 buffer.
-      pf::GemmArgs a{};
-      a.A = U;
-      a.lda = H;
-      a.K = static_cast<int>(H);
-      a.M = n_tok;
-      a.B1 = static_cast<const uint16_t*>(w->wq);
-      a.ldb1 = w->ld_q;
-      a.n1 = nq * static_cast<int>(d);
-      a.B2 = static_cast<const uint16_t*>(w->wk);
-      a.ldb2 = w->ld_k;
-      a.N = (nq + nkv) * static_cast<int>(d);
-      if ((st = launch_gemm(a, pf::EpiStoreF32{QKV, (nq + 2 * nkv) * d}, s)) != VT_OK) return st;
-      a.B1 = static_cast<const uint16_t*>(w->wv);
-      a.ldb1 = w->ld_v;
-      a.n1 = nkv * static_cast<int>(d);
-      a.B2 = nullptr;
-      a.ldb2 = 0;
-      a.N = nkv * static_cast<int>(d);
-      if ((st = launch_gemm(a, pf::EpiStoreF32{QKV + (nq + nkv) * d, (nq + 2 * nkv) * d}, s)) !=
-          VT_OK)
-        return st;
-      hipLaunchKernelGGL(pf::rope_append_kernel, dim3(n_tok), dim3(pf::RT), 0, s, QKV,
-                         static_cast<int>((nq + 2 * nkv) * d), Qr, static_cast<uint16_t*>(kv->k),
-                         static_cast<uint16_t*>(kv->v), nq, nkv, static_cast<int>(d), kv->capacity,
-                         pos0, D.rope_base);
-      if ((st = check("rope_append")) != VT_OK) return st;
-      const int blocks = nq * ((n_tok + pf::QB - 1) / pf::QB);
-      if (d == 128)
-        hipLaunchKernelGGL(pf::attn_prefill_kernel<128>, dim3(blocks), dim3(kWave), 0, s, Qr, Ob,
-                           static_cast<const uint16_t*>(kv->k), static_cast<const uint16_t*>(kv->v),
-                           n_tok, nq, G, kv->capacity, pos0);
-      else
-        hipLaunchKernelGGL(pf::attn_prefill_kernel<64>, dim3(blocks), dim3(kWave), 0, s, Qr, Ob,
-                           static_cast<const uint16_t*>(kv->k), static_cast<const uint16_t*>(kv->v),
-                           n_tok, nq, G, kv->capacity, pos0);
-      if ((st = check("attention")) != VT_OK) return st;
-    }
-    pf::GemmArgs a{};
-    a.A = Ob;
-    a.lda = std::max<int64_t>(nq * d, 8);
-    a.K = nq * static_cast<int>(d);
-    a.M = n_tok;
-    a.B1 = static_cast<const uint16_t*>(w->wo);
-    a.ldb1 = w->ld_o;
-    a.n1 = static_cast<int>(H);
-    a.N = static_cast<int>(H);
-    pf::EpiResidual epi{static_cast<uint16_t*>(io->attn_partial), static_cast<uint16_t*>(io->h),
-                        static_cast<const uint16_t*>(io->x),
-                        static_cast<const uint16_t*>(io->peer_attn), H};
-    if ((st = launch_gemm(a, epi, s)) != VT_OK) return st;
-  }
-  if (ffn) {
-    hipLaunchKernelGGL(pf::rmsnorm_rows_kernel, dim3(n_tok), dim3(pf::RT), 0, s,
-                       static_cast<const uint16_t*>(io->h), static_cast<const uint16_t*>(w->g_ffn), U,
-                       static_cast<int>(H), D.rms_eps);
-    if ((st = check("rmsnorm")) != VT_OK) return st;
     pf::GemmArgs a{};
     a.A = U;
     a.lda = H;
-    a.K = static_cast<int>(H);
+    a.K = gm.K[0];
     a.M = n_tok;
-    a.B1 = static_cast<const uint16_t*>(w->wg);
-    a.ldb1 = w->ld_g;
-    a.n1 = F;
-    a.B2 = static_cast<const uint16_t*>(w->wu);
-    a.ldb2 = w->ld_u;
-    a.N = 2 * F;
-    if ((st = launch_gemm(a, pf::EpiStoreF32{GU, 2 * F}, s)) != VT_OK) return st;
-    hipLaunchKernelGGL(pf::silu_gate_kernel, dim3(n_tok), dim3(pf::RT), 0, s, GU, 2 * F, Mb, F,
-                       static_cast<int>(fpad));
+    a.N = gm.N[0];
+    const int qd = nq * static_cast<int>(d), kd = nkv * static_cast<int>(d);
+    a.b[0] = bsrc(w->wq, w->ld_q, 0, qd);
+    a.b[1] = bsrc(w->wk, w->ld_k, qd, kd);
+    a.b[2] = bsrc(w->wv, w->ld_v, qd + kd, kd);
+    a.nb = 3;
+    if ((st = launch_gemm(a, P, s, &splits)) != VT_OK) return st;
+    VT_SPLIT_DISPATCH(pf::rope_append_kernel, dim3(n_tok), dim3(pf::RT), 0, s, P, slab(0), gm.N[0], Qr,
+                      static_cast<uint16_t*>(kv->k), static_cast<uint16_t*>(kv->v), nq, nkv,
+                      static_cast<int>(d), kv->capacity, pos0, D.rope_base);
+    if ((st = check("rope_append")) != VT_OK) return st;
+    const int blocks = nq * ((n_tok + pf::QB - 1) / pf::QB);
+    if (d == 128)
+      hipLaunchKernelGGL(pf::attn_prefill_kernel<128>, dim3(blocks), dim3(pf::AW * kWave), 0, s, Qr, Ob,
+                         static_cast<const uint16_t*>(kv->k), static_cast<const uint16_t*>(kv->v),
+                         n_tok, nq, G, kv->capacity, pos0);
+    else
+      hipLaunchKernelGGL(pf::attn_prefill_kernel<64>, dim3(blocks), dim3(pf::AW * kWave), 0, s, Qr, Ob,
+                         static_cast<const uint16_t*>(kv->k), static_cast<const uint16_t*>(kv->v),
+                         n_tok, nq, G, kv->capacity, pos0);
+    if ((st = check("attention")) != VT_OK) return st;
+    pf::GemmArgs o{};
+    o.A = Ob;
+    o.lda = std::max<int64_t>(nq * d, 8);
+    o.K = gm.K[1];
+    o.M = n_tok;
+    o.N = gm.N[1];
+    o.b[0] = bsrc(w->wo, w->ld_o, 0, gm.N[1]);
+    o.nb = 1;
+    if ((st = launch_gemm(o, P, s, &splits)) != VT_OK) return st;
+    // h = x + p_attn + peer; with FFN to follow also U = RMSNorm(h) * g_ffn
+    if (ffn) {
+      VT_SPLIT_DISPATCH(pf::resid_norm_kernel, dim3(n_tok), dim3(pf::RT), 0, s, P, slab(1),
+                        static_cast<const uint16_t*>(io->x), static_cast<const uint16_t*>(io->peer_attn),
+                        static_cast<uint16_t*>(io->attn_partial), static_cast<uint16_t*>(io->h),
+                        static_cast<const uint16_t*>(w->g_ffn), U, static_cast<int>(H), D.rms_eps);
+    } else {
+      VT_SPLIT_DISPATCH(pf::resid_only_kernel, dim3(n_tok), dim3(pf::RT), 0, s, P, slab(1),
+                        static_cast<const uint16_t*>(io->x), static_cast<const uint16_t*>(io->peer_attn),
+                        static_cast<uint16_t*>(io->attn_partial), static_cast<uint16_t*>(io->h),
+                        static_cast<const uint16_t*>(nullptr), static_cast<uint16_t*>(nullptr),
+                        static_cast<int>(H), D.rms_eps);
+    }
+    if ((st = check("attention residual")) != VT_OK) return st;
+  }
+  if (ffn) {
+    if (!attn) {
+      hipLaunchKernelGGL(pf::rmsnorm_rows_kernel, dim3(n_tok), dim3(pf::RT), 0, s,
+                         static_cast<const uint16_t*>(io->h), static_cast<const uint16_t*>(w->g_ffn),
+                         U, static_cast<int>(H), D.rms_eps);
+      if ((st = check("rmsnorm")) != VT_OK) return st;
+    }
+    pf::GemmArgs a{};
+    a.A = U;
+    a.lda = H;
+    a.K = gm.K[2];
+    a.M = n_tok;
+    a.N = gm.N[2];
+    a.b[0] = bsrc(w->wg, w->ld_g, 0, F);
+    a.b[1] = bsrc(w->wu, w->ld_u, gm.up0, F);
+    a.nb = 2;
+    if ((st = launch_gemm(a, P, s, &splits)) != VT_OK) return st;
+    VT_SPLIT_DISPATCH(pf::silu_gate_kernel, dim3(n_tok), dim3(pf::RT), 0, s, P, slab(2),
+                      static_cast<int64_t>(gm.N[2]), gm.up0, Mb, F, static_cast<int>(fpad));
     if ((st = check("silu_gate")) != VT_OK) return st;
     pf::GemmArgs b{};
     b.A = Mb;
     b.lda = fpad;
-    b.K = F;
+    b.K = gm.K[3];
     b.M = n_tok;
-    b.B1 = static_cast<const uint16_t*>(w->wd);
-    b.ldb1 = w->ld_d;
-    b.n1 = static_cast<int>(H);
-    b.N = static_cast<int>(H);
-    pf::EpiResidual epi{static_cast<uint16_t*>(io->ffn_partial), static_cast<uint16_t*>(io->y),
-                        static_cast<const uint16_t*>(io->h),
-                        static_cast<const uint16_t*>(io->peer_ffn), H};
-    if ((st = launch_gemm(b, epi, s)) != VT_OK) return st;
+    b.N = gm.N[3];
+    b.b[0] = bsrc(w->wd, w->ld_d, 0, gm.N[3]);
+    b.nb = 1;
+    if ((st = launch_gemm(b, P, s, &splits)) != VT_OK) return st;
+    VT_SPLIT_DISPATCH(pf::resid_only_kernel, dim3(n_tok), dim3(pf::RT), 0, s, P, slab(3),
+                      static_cast<const uint16_t*>(io->h), static_cast<const uint16_t*>(io->peer_ffn),
+                      static_cast<uint16_t*>(io->ffn_partial), static_cast<uint16_t*>(io->y),
+                      static_cast<const uint16_t*>(nullptr), static_cast<uint16_t*>(nullptr),
+                      static_cast<int>(H), D.rms_eps);
+    if ((st = check("ffn residual")) != VT_OK) return st;
   }
   if (attn) kv->len = pos0 + n_tok;
   return VT_OK;
