@@ -35,46 +35,48 @@ __device__ __forceinline__ f32x16 mfma32(const u32x4 a, const u32x4 b, f32x16 c)
                                                 __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
 }
 
-// Zero the fp16 values at columns >= K of an 8-column chunk starting at col.
-__device__ __forceinline__ u32x4 mask_cols(u32x4 w, int col, int K) {
-  const int v = K - col;
-  if (v >= 8) return w;
-  if (v <= 0) return u32x4{0u, 0u, 0u, 0u};
-  w.x = v >= 2 ? w.x : (w.x & 0xFFFFu);
-  w.y = v >= 4 ? w.y : (v >= 3 ? (w.y & 0xFFFFu) : 0u);
-  w.z = v >= 6 ? w.z : (v >= 5 ? (w.z & 0xFFFFu) : 0u);
-  w.w = v >= 7 ? (w.w & 0xFFFFu) : 0u;
-  return w;
+// The GEMMs' activation operands (A) are stored k-step-major: the 16 k
+// values of token m in k-step s are halves [(s * M + m) * 16, +16), so the 32
+// tokens x 16 k of one MFMA fragment are one contiguous 1 KiB load. K is
+// padded with zeros to a multiple of 16.
+__device__ __forceinline__ int64_t kmajor(int k, int m, int M) {
+  return (static_cast<int64_t>(k >> 4) * M + m) * 16 + (k & 15);
 }
 
 // ---------------------------------------------------------------------------
 // Split-K GEMM   P[s][m][n] = sum over k-slice s of A[m][k] * B[n][k]
 // (fp16 in, fp32 out). M is the chunk's tokens, N the shard's output
-// features, K the input features (a multiple of 8; both operands hold finite
-// values, zeros in A, in the columns up to it). The weights (B) are the large
+// features, K the input features (a multiple of 8). A is k-step-major (see
+// kmajor) with zeros past K; B is row-major. The weights (B) are the large
 // operand and are streamed once; A is small and re-read from L2 by every N
 // tile. The K range is cut into ``splits`` slices so that one launch has
 // about one workgroup per compute unit; each slice writes its own fp32 slab
 // and the consumer kernel adds the slabs (no atomics, fixed summation order).
 //
-// Tile 256 tokens x 128 features x 64 k per 256-thread workgroup. Wave w
-// owns tokens 64w..64w+63 and all 128 features as 2 x 4 MFMA tiles (32 x 32
-// x 16 fp16). Two LDS stages (rows padded by 8 halves) and two register
-// stages: the loads of k-tile i+2 are issued before k-tile i is multiplied.
-// Every load is unconditional (out-of-range lanes use an offset past the
-// buffer and read zero), so the compiler's wait counts stay exact.
+// Tile 128 tokens x 128 features x 64 k per 256-thread workgroup, two
+// workgroups per compute unit (one's barrier and LDS waits are covered by the
+// other's MFMAs). Wave w owns tokens 32w..32w+31 and all 128 features as
+// 1 x 4 MFMA tiles (32 x 32 x 16 fp16). A wave's A fragments are its own, so they go from global
+// memory straight into registers (one contiguous 1 KiB load each, thanks to
+// the k-step-major layout), through a ring that runs 8 k-steps (two k-tiles)
+// ahead. The B tile is shared by the four waves and is staged in LDS
+// (two stages, rows padded by 8 halves; the loads of k-tile i+2 are issued
+// before k-tile i is multiplied). Staging only B halves the LDS traffic of
+// staging both. Every load is unconditional (out-of-range lanes use an offset
+// past the buffer and read zero), so the compiler's wait counts stay exact.
 //
 // B's rows come from up to three matrices (e.g. Wq, Wk, Wv) placed at
 // 8-row-aligned starts of a virtual row space (rows between them read as
 // zero). A wave loads 8 consecutive 8-aligned rows per instruction, so each
 // load has one source, chosen once per workgroup with scalar selects.
 // ---------------------------------------------------------------------------
-constexpr int GBM = 256, GBN = 128, GBK = 64, GLD = GBK + 8, GT = 256;
-constexpr int A_CH = GBM * GBK / 8 / GT;   // 16-byte A chunks per thread per k-tile
+constexpr int GBM = 128, GBN = 128, GBK = 64, GLD = GBK + 8, GT = 256;
+constexpr int KSTEPS = GBK / 16;           // MFMA k-steps per k-tile
+constexpr int RING = 2 * KSTEPS;           // A k-steps in flight
 constexpr int B_CH = GBN * GBK / 8 / GT;   // 16-byte B chunks per thread per k-tile
-constexpr int STAGE = (GBM + GBN) * GLD;   // halves per LDS stage
+constexpr int STAGE = GBN * GLD;           // halves per LDS stage
 constexpr int GEMM_LDS_BYTES = 2 * STAGE * 2;
-constexpr int GEMM_TARGET_WGS = 256;       // one workgroup per compute unit
+constexpr int GEMM_SLOTS = 512;            // two workgroups per compute unit
 constexpr int MAX_SPLITS = 8;
 
 struct BSrc {
@@ -84,8 +86,7 @@ struct BSrc {
 };
 
 struct GemmArgs {
-  const uint16_t* A;
-  int64_t lda;
+  const uint16_t* A;  // k-step-major, ceil(K / 16) k-steps of M tokens
   BSrc b[3];
   int nb;
   float* P;
@@ -94,7 +95,7 @@ struct GemmArgs {
   int m_tiles, n_tiles, splits, kps;  // kps: k-tiles per split
 };
 
-__global__ void __launch_bounds__(GT) gemm_kernel(GemmArgs g) {
+__global__ void __launch_bounds__(GT, 2) gemm_kernel(GemmArgs g) {
   extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
   // Workgroups with equal index mod 8 run on one XCD: the M tiles of one
   // (N tile, split) pair get indices that differ by multiples of 8, so their
@@ -112,22 +113,30 @@ __global__ void __launch_bounds__(GT) gemm_kernel(GemmArgs g) {
   const int kt0 = split * g.kps;
   const int kt_end = min(kt0 + g.kps, KT);
   const int nkt = kt_end - kt0;
+  const int ks_end = nkt * KSTEPS;  // k-steps of this split
 
   rsrc_t rs[3];
 #pragma unroll
   for (int j = 0; j < 3; ++j)
     rs[j] = make_rsrc(g.b[j].p, static_cast<uint32_t>(j < g.nb ? g.b[j].rows * g.b[j].ld * 2 : 0));
-  const rsrc_t ra = make_rsrc(g.A, static_cast<uint32_t>(g.M * g.lda * 2));
+  const int KS = (g.K + 15) / 16;  // k-steps of A
+  const rsrc_t ra = make_rsrc(g.A, static_cast<uint32_t>(KS * g.M * 32));
 
-  // k-independent part of each chunk's offset; kOOB marks a row past its source
+  // A fragment of this lane: token m, halves 8 (l/32).. of each k-step
+  const int am = m0 + wave * 32 + lane % 32;
+  const uint32_t aoff = am < g.M ? static_cast<uint32_t>(am * 32 + (lane / 32) * 16) : kOOB;
+  const int ks0 = kt0 * KSTEPS;            // the split's first k-step
+  auto load_a = [&](int ks, u32x4& dst) {  // k-step ks of this split
+    const int sa = ks0 + ks;
+    const bool kin = ks < ks_end && sa < KS;
+    const uint32_t koff = static_cast<uint32_t>(sa) * static_cast<uint32_t>(g.M) * 32u;
+    dst = buf_load16(ra, kin && aoff != kOOB ? aoff + koff : kOOB);
+  };
+
+  // B chunk offsets (k-independent part); kOOB marks a row past its source
   const int ccol = (t % 8) * 8;
-  uint32_t aoff[A_CH], boff[B_CH];
+  uint32_t boff[B_CH];
   rsrc_t rsel[B_CH];
-#pragma unroll
-  for (int u = 0; u < A_CH; ++u) {
-    const int m = m0 + (t + u * GT) / 8;
-    aoff[u] = m < g.M ? static_cast<uint32_t>(m * g.lda * 2) : kOOB;
-  }
 #pragma unroll
   for (int u = 0; u < B_CH; ++u) {
     const int r0 = n0 + wave * 8 + u * 32;  // first row of this wave's 8-row group (uniform)
@@ -140,85 +149,79 @@ __global__ void __launch_bounds__(GT) gemm_kernel(GemmArgs g) {
     const int r = n - src.start;
     boff[u] = (n < g.N && r >= 0 && r < src.rows) ? static_cast<uint32_t>(r * src.ld * 2) : kOOB;
   }
-
-  // k-tile kt into registers; tiles past this split's range read as zero
-  auto load = [&](int kt, u32x4 (&va)[A_CH], u32x4 (&vb)[B_CH]) {
+  auto load_b = [&](int kt, u32x4 (&vb)[B_CH]) {  // k-tile kt (absolute)
     const int k = kt * GBK + ccol;
     const bool kin = kt < kt_end && k < g.K;
-#pragma unroll
-    for (int u = 0; u < A_CH; ++u)
-      va[u] = buf_load16(ra, kin && aoff[u] != kOOB ? aoff[u] + k * 2 : kOOB);
 #pragma unroll
     for (int u = 0; u < B_CH; ++u)
       vb[u] = buf_load16(rsel[u], kin && boff[u] != kOOB ? boff[u] + k * 2 : kOOB);
   };
-  auto store = [&](uint16_t* st, const u32x4 (&va)[A_CH], const u32x4 (&vb)[B_CH]) {
-#pragma unroll
-    for (int u = 0; u < A_CH; ++u)
-      *reinterpret_cast<u32x4*>(st + ((t + u * GT) / 8) * GLD + ccol) = va[u];
+  auto store_b = [&](uint16_t* st, const u32x4 (&vb)[B_CH]) {
 #pragma unroll
     for (int u = 0; u < B_CH; ++u)
-      *reinterpret_cast<u32x4*>(st + (GBM + (t + u * GT) / 8) * GLD + ccol) = vb[u];
+      *reinterpret_cast<u32x4*>(st + ((t + u * GT) / 8) * GLD + ccol) = vb[u];
   };
 
-  f32x16 acc[2][4];
+  f32x16 acc[4];
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
-#pragma unroll
-    for (int b = 0; b < 4; ++b) acc[a][b] = f32x16{};
+  for (int b = 0; b < 4; ++b) acc[b] = f32x16{};
 
-  auto compute = [&](const uint16_t* st) {
+  u32x4 ar[RING];
+  // k-tile (from LDS stage st) with A k-steps from ring slots s0..s0+3;
+  // each slot is refilled with the k-step RING ahead right after its use.
+  // The B fragments of k-step ks+1 are read while k-step ks multiplies.
+  auto read_b = [&](const uint16_t* st, int ks, u32x4 (&bf)[4]) {
+    const int kc = ks * 16 + 8 * (lane / 32);
 #pragma unroll
-    for (int ks = 0; ks < GBK / 16; ++ks) {
-      const int kc = ks * 16 + 8 * (lane / 32);
-      u32x4 af[2], bf[4];
+    for (int b = 0; b < 4; ++b)
+      bf[b] = *reinterpret_cast<const u32x4*>(st + (b * 32 + lane % 32) * GLD + kc);
+  };
+  auto compute = [&](const uint16_t* st, int ks_base, int s0) {
+    u32x4 bf[2][4];
+    read_b(st, 0, bf[0]);
 #pragma unroll
-      for (int a = 0; a < 2; ++a)
-        af[a] = *reinterpret_cast<const u32x4*>(st + (wave * 64 + a * 32 + lane % 32) * GLD + kc);
+    for (int ks = 0; ks < KSTEPS; ++ks) {
+      if (ks + 1 < KSTEPS) read_b(st, ks + 1, bf[(ks + 1) & 1]);
 #pragma unroll
-      for (int b = 0; b < 4; ++b)
-        bf[b] = *reinterpret_cast<const u32x4*>(st + (GBM + b * 32 + lane % 32) * GLD + kc);
-#pragma unroll
-      for (int a = 0; a < 2; ++a)
-#pragma unroll
-        for (int b = 0; b < 4; ++b) acc[a][b] = mfma32(af[a], bf[b], acc[a][b]);
+      for (int b = 0; b < 4; ++b) acc[b] = mfma32(ar[s0 + ks], bf[ks & 1][b], acc[b]);
+      load_a(ks_base + ks + RING, ar[s0 + ks]);
     }
   };
 
   uint16_t* L0 = lds;
   uint16_t* L1 = lds + STAGE;
-  u32x4 ra0[A_CH], rb0[B_CH], ra1[A_CH], rb1[B_CH];
-  load(kt0, ra0, rb0);
-  load(kt0 + 1, ra1, rb1);
-  store(L0, ra0, rb0);
+  u32x4 rb0[B_CH], rb1[B_CH];
+#pragma unroll
+  for (int s = 0; s < RING; ++s) load_a(s, ar[s]);
+  load_b(kt0, rb0);
+  load_b(kt0 + 1, rb1);
+  store_b(L0, rb0);
   __syncthreads();
   // two k-tiles per trip; an odd count runs one all-zero tile at the end
-  // (the scheduling barriers keep the prefetch loads ahead of the MFMAs)
+  // (the scheduling barriers keep the B prefetch ahead of the MFMAs)
   for (int i = 0; i < nkt; i += 2) {
-    load(kt0 + i + 2, ra0, rb0);
+    load_b(kt0 + i + 2, rb0);
     __builtin_amdgcn_sched_barrier(0);
-    compute(L0);
-    store(L1, ra1, rb1);
+    compute(L0, i * KSTEPS, 0);
+    store_b(L1, rb1);
     __syncthreads();
-    load(kt0 + i + 3, ra1, rb1);
+    load_b(kt0 + i + 3, rb1);
     __builtin_amdgcn_sched_barrier(0);
-    compute(L1);
-    store(L0, ra0, rb0);
+    compute(L1, (i + 1) * KSTEPS, KSTEPS);
+    store_b(L0, rb0);
     __syncthreads();
   }
 
-  // accumulator i of tile (a, b): token 8(i/4) + 4(l/32) + i%4, feature l%32
+  // accumulator i of tile b: token 8(i/4) + 4(l/32) + i%4, feature l%32
   float* out = g.P + split * g.slab;
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int b = 0; b < 4; ++b)
 #pragma unroll
-    for (int b = 0; b < 4; ++b)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int m = m0 + wave * 64 + a * 32 + 8 * (i / 4) + 4 * (lane / 32) + i % 4;
-        const int n = n0 + b * 32 + lane % 32;
-        if (m < g.M && n < g.N) out[m * g.ldp + n] = acc[a][b][i];
-      }
+    for (int i = 0; i < 16; ++i) {
+      const int m = m0 + wave * 32 + 8 * (i / 4) + 4 * (lane / 32) + i % 4;
+      const int n = n0 + b * 32 + lane % 32;
+      if (m < g.M && n < g.N) out[m * g.ldp + n] = acc[b][i];
+    }
 }
 
 // Sum over the S split-K slabs of 4 consecutive fp32 values at element i
@@ -249,12 +252,13 @@ __device__ __forceinline__ float slab_sum1(const float* P, int64_t slab, int64_t
 constexpr int RT = 256;
 constexpr int RMAX = 16384 / 8 / RT;  // 16-byte chunks per thread at the largest hidden size
 
-// U[t] = fp16(X[t] / sqrt(mean(X[t]^2) + eps) * g), one workgroup per row.
+// U[t] = fp16(X[t] / sqrt(mean(X[t]^2) + eps) * g), one workgroup per row
+// (grid = the chunk's tokens); U is k-step-major.
 __global__ void __launch_bounds__(RT) rmsnorm_rows_kernel(const uint16_t* X, const uint16_t* g,
                                                           uint16_t* U, int H, float eps) {
   __shared__ float red[RT / kWave];
-  const uint16_t* x = X + static_cast<int64_t>(blockIdx.x) * H;
-  uint16_t* u = U + static_cast<int64_t>(blockIdx.x) * H;
+  const int t = blockIdx.x, M = gridDim.x;
+  const uint16_t* x = X + static_cast<int64_t>(t) * H;
   float ss = 0.f;
   for (int k8 = threadIdx.x; k8 < H / 8; k8 += RT) {
     float f[8];
@@ -271,14 +275,18 @@ __global__ void __launch_bounds__(RT) rmsnorm_rows_kernel(const uint16_t* X, con
     uint16_t h[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) h[e] = f2h(f[e] * rstd * gg[e]);
-    *reinterpret_cast<u32x4*>(u + k8 * 8) = pack8(h);
+    *reinterpret_cast<u32x4*>(U + kmajor(k8 * 8, t, M)) = pack8(h);
   }
+  // zero padding of the last k-step when H is not a multiple of 16
+  if ((H & 15) && threadIdx.x == 0)
+    *reinterpret_cast<u32x4*>(U + kmajor(H, t, M)) = u32x4{0u, 0u, 0u, 0u};
 }
 
 // Residual epilogue of an output projection, one workgroup per token row t:
 // p = sum of the slabs, partial[t] = fp16(p), out[t] = fp16(base[t] + p +
 // peer[t]) (out may be NULL). With NORM also U[t] = fp16(RMSNorm(out[t]) * g),
-// the next sub-layer's normalised input, taken from the fp16-rounded row.
+// the next sub-layer's normalised input (k-step-major), taken from the
+// fp16-rounded row.
 template <bool NORM, int S>
 __device__ __forceinline__ void resid_body(const float* P, int64_t slab, const uint16_t* base,
                                            const uint16_t* peer, uint16_t* partial, uint16_t* out,
@@ -322,8 +330,10 @@ __device__ __forceinline__ void resid_body(const float* P, int64_t slab, const u
     uint16_t u[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) u[e] = f2h(f[e] * rstd * gg[e]);
-    *reinterpret_cast<u32x4*>(U + row + k8 * 8) = pack8(u);
+    *reinterpret_cast<u32x4*>(U + kmajor(k8 * 8, blockIdx.x, gridDim.x)) = pack8(u);
   }
+  if ((H & 15) && threadIdx.x == 0)
+    *reinterpret_cast<u32x4*>(U + kmajor(H, blockIdx.x, gridDim.x)) = u32x4{0u, 0u, 0u, 0u};
 }
 
 template <int S>
@@ -388,21 +398,22 @@ __global__ void __launch_bounds__(RT) rope_append_kernel(const float* P, int64_t
   }
 }
 
-// M[t][j] = fp16(silu(G[t][j]) * Up[t][j]) for j < F, zero for F <= j < ldm;
-// G and Up are columns j and up0 + j of the summed slabs (row stride ldp).
+// Mg[t][j] = fp16(silu(G[t][j]) * Up[t][j]) for j < F, zero for F <= j < kpad
+// (k-step-major); G and Up are columns j and up0 + j of the summed slabs (row
+// stride ldp). One workgroup per token.
 template <int S>
 __global__ void __launch_bounds__(RT) silu_gate_kernel(const float* P, int64_t slab, int64_t ldp,
-                                                       int up0, uint16_t* M, int F, int ldm) {
+                                                       int up0, uint16_t* Mg, int F, int kpad) {
   const int t = blockIdx.x;
   const int64_t row = static_cast<int64_t>(t) * ldp;
-  for (int j = threadIdx.x; j < ldm; j += RT) {
+  for (int j = threadIdx.x; j < kpad; j += RT) {
     float m = 0.f;
     if (j < F) {
       const float gt = slab_sum1<S>(P, slab, row + j);
       const float up = slab_sum1<S>(P, slab, row + up0 + j);
       m = gt / (1.0f + __expf(-gt)) * up;
     }
-    M[static_cast<int64_t>(t) * ldm + j] = f2h(m);
+    Mg[kmajor(j, t, gridDim.x)] = f2h(m);
   }
 }
 
@@ -421,7 +432,8 @@ __global__ void __launch_bounds__(RT) silu_gate_kernel(const float* P, int64_t s
 // operand layout asks for, and the probabilities go to the second MFMA
 // (O^T += V_blk^T P^T) without any shuffle. V is staged transposed
 // ([dim][key]) for that MFMA's other operand. A wave only touches its own
-// LDS region inside the loop, so the loop needs no workgroup barrier.
+// LDS region inside the loop, so the loop needs no workgroup barrier. The
+// output O (the O projection's input) is written k-step-major.
 // ---------------------------------------------------------------------------
 constexpr int QB = 32, KB = 32, AW = 4;
 
@@ -611,7 +623,7 @@ __global__ void __launch_bounds__(AW * kWave) attn_prefill_kernel(const uint16_t
     uint16_t h[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) h[e] = f2h(acc[e] * inv);
-    *reinterpret_cast<u32x4*>(O + (static_cast<int64_t>(t0 + q) * nq + j) * D + d0) = pack8(h);
+    *reinterpret_cast<u32x4*>(O + kmajor(j * D + d0, t0 + q, T)) = pack8(h);
   }
 }
 
@@ -622,8 +634,11 @@ __global__ void __launch_bounds__(AW * kWave) attn_prefill_kernel(const uint16_t
 // ---------------------------------------------------------------------------
 namespace {
 
-// Split-K choice of a GEMM: as many slices of whole k-tiles as keep one
-// launch at or below the target number of workgroups.
+// Split-K choice of a GEMM: enough slices of whole k-tiles for about two
+// rounds of resident workgroups (GEMM_SLOTS each), at most 4. Measured on the
+// 256-token chunk of the 7B 50% shard: 4 slices beat 2, 3, 6 and 8 for the
+// gate/up, O and down GEMMs and are within 4% of 5 for QKV; more slices add
+// fp32 slab traffic, fewer leave compute units idle.
 struct Split {
   int m_tiles, n_tiles, splits, kps;
 };
@@ -634,7 +649,7 @@ Split choose_split(int M, int N, int K) {
   s.n_tiles = (N + pf::GBN - 1) / pf::GBN;
   const int KT = std::max(1, (K + pf::GBK - 1) / pf::GBK);
   const int tiles = std::max(1, s.m_tiles * s.n_tiles);
-  const int want = std::max(1, std::min({KT, pf::MAX_SPLITS, pf::GEMM_TARGET_WGS / tiles}));
+  const int want = std::max(1, std::min({KT, 4, (2 * pf::GEMM_SLOTS + tiles - 1) / tiles}));
   s.kps = (KT + want - 1) / want;
   s.splits = (KT + s.kps - 1) / s.kps;
   return s;
@@ -673,7 +688,6 @@ inline int64_t rup(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 PrefillWs prefill_layout(const vt_shard_spec& s, int32_t T) {
   const vt_shard_info& in = s.info;
   const int64_t H = s.dims.hidden, d = s.dims.head_dim;
-  const int64_t fpad = std::max<int64_t>(8, rup(in.n_cols, 8));
   const PrefillGemms gm = prefill_gemms(s, T);
   int64_t part = 0;  // one region serves the four GEMMs' slabs in turn
   for (int i = 0; i < 4; ++i) {
@@ -687,10 +701,11 @@ PrefillWs prefill_layout(const vt_shard_spec& s, int32_t T) {
     off += static_cast<size_t>(rup(std::max<int64_t>(bytes, 16), 256));
     return at;
   };
-  w.u = take(2 * T * H);
+  // k-step-major activation operands, K padded to a multiple of 16
+  w.u = take(2 * T * rup(H, 16));
   w.q = take(2 * T * in.n_q_heads * d);
-  w.o = take(2 * T * std::max<int64_t>(in.n_q_heads * d, 8));
-  w.m = take(2 * T * fpad);
+  w.o = take(2 * T * std::max<int64_t>(rup(in.n_q_heads * d, 16), 16));
+  w.m = take(2 * T * std::max<int64_t>(rup(in.n_cols, 16), 16));
   w.part = take(part);
   w.total = off;
   return w;
@@ -797,7 +812,7 @@ extern "C" vt_status vt_layer_prefill_chunk(const vt_shard_spec* spec, const vt_
   if (ffn && in.n_cols == 0)
     return fail(VT_ERR_UNSUPPORTED, "prefill of a shard without FFN columns");
   // activation operands of the GEMMs are read through 2 GiB buffer ranges
-  if (static_cast<int64_t>(n_tok) * std::max<int64_t>({H, in.n_q_heads * d, in.n_cols + 8}) * 2 >=
+  if (static_cast<int64_t>(n_tok) * std::max<int64_t>({H + 16, in.n_q_heads * d, in.n_cols + 16}) * 2 >=
       kMaxBufferBytes)
     return fail(VT_ERR_UNSUPPORTED, "chunk of %d tokens too large for 2 GiB activation buffers", n_tok);
   const PrefillWs L = prefill_layout(*spec, n_tok);
@@ -814,7 +829,7 @@ extern "C" vt_status vt_layer_prefill_chunk(const vt_shard_spec* spec, const vt_
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int nq = in.n_q_heads, nkv = in.n_kv_heads, F = in.n_cols;
   const int G = D.n_heads / D.n_kv_heads;
-  const int64_t fpad = std::max<int64_t>(8, (F + 7) / 8 * 8);
+  const int kpad_f = std::max(16, (F + 15) / 16 * 16);  // k-step-major width of the SiLU-gate output
   const PrefillGemms gm = prefill_gemms(*spec, n_tok);
   int splits = 1;
   auto check = [&](const char* what) -> vt_status {
@@ -830,7 +845,6 @@ extern "C" vt_status vt_layer_prefill_chunk(const vt_shard_spec* spec, const vt_
     if ((st = check("rmsnorm")) != VT_OK) return st;
     pf::GemmArgs a{};
     a.A = U;
-    a.lda = H;
     a.K = gm.K[0];
     a.M = n_tok;
     a.N = gm.N[0];
@@ -856,7 +870,6 @@ extern "C" vt_status vt_layer_prefill_chunk(const vt_shard_spec* spec, const vt_
     if ((st = check("attention")) != VT_OK) return st;
     pf::GemmArgs o{};
     o.A = Ob;
-    o.lda = std::max<int64_t>(nq * d, 8);
     o.K = gm.K[1];
     o.M = n_tok;
     o.N = gm.N[1];
@@ -887,7 +900,6 @@ extern "C" vt_status vt_layer_prefill_chunk(const vt_shard_spec* spec, const vt_
     }
     pf::GemmArgs a{};
     a.A = U;
-    a.lda = H;
     a.K = gm.K[2];
     a.M = n_tok;
     a.N = gm.N[2];
@@ -896,11 +908,10 @@ extern "C" vt_status vt_layer_prefill_chunk(const vt_shard_spec* spec, const vt_
     a.nb = 2;
     if ((st = launch_gemm(a, P, s, &splits)) != VT_OK) return st;
     VT_SPLIT_DISPATCH(pf::silu_gate_kernel, dim3(n_tok), dim3(pf::RT), 0, s, P, slab(2),
-                      static_cast<int64_t>(gm.N[2]), gm.up0, Mb, F, static_cast<int>(fpad));
+                      static_cast<int64_t>(gm.N[2]), gm.up0, Mb, F, kpad_f);
     if ((st = check("silu_gate")) != VT_OK) return st;
     pf::GemmArgs b{};
     b.A = Mb;
-    b.lda = fpad;
     b.K = gm.K[3];
     b.M = n_tok;
     b.N = gm.N[3];
