@@ -325,14 +325,12 @@ __device__ __forceinline__ void stage_rmsnorm_f(const float* v, const uint16_t* 
   constexpr int MAXP = 16;  // float pairs held per thread
   const int npair = n / 2;
   float a[MAXP], b[MAXP];
-  // Indices are clamped rather than the loads guarded: a guarded coherent
-  // load is compiled into its own branch with a full wait, which would
-  // serialise the 16 round trips.
+  // Unconditional coherent buffer loads: pairs past n read zero without
+  // memory traffic (a guarded load would get a branch and a full wait each).
+  const rsrc_t rv = make_rsrc(v, static_cast<uint32_t>(npair) * 8u);
 #pragma unroll
-  for (int u = 0; u < MAXP; ++u) {
-    const int i = min(static_cast<int>(threadIdx.x) + u * NT, npair - 1);
-    ld_shared2(v + 2 * i, a[u], b[u]);
-  }
+  for (int u = 0; u < MAXP; ++u)
+    buf_ld_shared2(rv, static_cast<uint32_t>(threadIdx.x + u * NT) * 8u, a[u], b[u]);
   const rsrc_t rg = make_rsrc(g, static_cast<uint32_t>(n) * 2u);
   uint32_t gw[MAXP];  // the two fp16 gains of each pair (zero past n)
 #pragma unroll
@@ -367,13 +365,12 @@ __device__ __forceinline__ void stage_rmsnorm_f(const float* v, const uint16_t* 
 __device__ __forceinline__ void stage_copy_f(const float* v, int n, int npad, uint16_t* xs) {
   constexpr int MAXP = 16;
   const int npair = (n + 1) / 2;
+  const rsrc_t rv = make_rsrc(v, static_cast<uint32_t>(npair) * 8u);
   for (int c0 = 0; c0 < npair; c0 += MAXP * NT) {
     float a[MAXP], b[MAXP];
 #pragma unroll
-    for (int u = 0; u < MAXP; ++u) {  // clamped, not guarded (see stage_rmsnorm_f)
-      const int i = min(c0 + static_cast<int>(threadIdx.x) + u * NT, npair - 1);
-      ld_shared2(v + 2 * i, a[u], b[u]);
-    }
+    for (int u = 0; u < MAXP; ++u)  // unconditional, zero past the end (see stage_rmsnorm_f)
+      buf_ld_shared2(rv, static_cast<uint32_t>(c0 + threadIdx.x + u * NT) * 8u, a[u], b[u]);
 #pragma unroll
     for (int u = 0; u < MAXP; ++u) {
       const int i = c0 + threadIdx.x + u * NT;
@@ -577,16 +574,18 @@ __device__ __forceinline__ void phase_attn(const Params& P, float* lds, bool wai
       // (m, l, value[dd]) in batches of 16 (one round trip each) and keeps a
       // running (max, sum l, sum value) under the log-sum-exp rescaling; the
       // ngrp partial triples of each dd are then merged in a fixed order.
-      const float* rj = P.part + static_cast<int64_t>(j) * P.nchunk * RW;
+      const rsrc_t rj = make_rsrc(P.part + static_cast<int64_t>(j) * P.nchunk * RW,
+                                  static_cast<uint32_t>(P.nchunk * RW) * 4u);
       const int ngrp = NT / d, grp = t / d, dd = t % d;
       float M = -INFINITY, Ls = 0.f, A = 0.f;
       for (int c0 = grp; grp < ngrp && c0 < P.nchunk; c0 += 16 * ngrp) {
         float mv[16], lv[16], ov[16];
 #pragma unroll
-        for (int u = 0; u < 16; ++u) {  // clamped, not guarded
-          const int cc = min(c0 + u * ngrp, P.nchunk - 1);
-          ld_shared2(rj + cc * RW + d, mv[u], lv[u]);
-          ov[u] = ld_shared(rj + cc * RW + dd);
+        for (int u = 0; u < 16; ++u) {  // unconditional; chunks past the last read zero
+          const int cc = c0 + u * ngrp;
+          const uint32_t rec = cc < P.nchunk ? static_cast<uint32_t>(cc * RW) * 4u : kOOB;
+          buf_ld_shared2(rj, rec == kOOB ? kOOB : rec + d * 4u, mv[u], lv[u]);
+          ov[u] = buf_ld_shared(rj, rec == kOOB ? kOOB : rec + dd * 4u);
         }
 #pragma unroll
         for (int u = 0; u < 16; ++u) {

@@ -147,6 +147,25 @@ __device__ __forceinline__ float ld_shared(const float* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// The same agent-scope coherent loads (cache policy sc1, as a relaxed
+// agent-scope atomic load compiles to) through a buffer resource: an offset
+// past the buffer reads zero with no memory traffic, so lanes with nothing to
+// load need neither a branch nor a clamped (and then shared, hot) address.
+// The 8-byte result is split from the whole 64 bits: bit-casting one element
+// of the returned ext-vector makes this compiler reuse element 0.
+constexpr int kCoherent = 16;  // sc1
+
+__device__ __forceinline__ void buf_ld_shared2(rsrc_t r, uint32_t off, float& a, float& b) {
+  const uint64_t w =
+      __builtin_bit_cast(uint64_t, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kCoherent));
+  a = __builtin_bit_cast(float, static_cast<uint32_t>(w));
+  b = __builtin_bit_cast(float, static_cast<uint32_t>(w >> 32));
+}
+
+__device__ __forceinline__ float buf_ld_shared(rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kCoherent));
+}
+
 // Two consecutive floats (8-byte aligned) written by other workgroups.
 __device__ __forceinline__ void ld_shared2(const float* p, float& a, float& b) {
   const uint64_t v = __hip_atomic_load(reinterpret_cast<const uint64_t*>(p), __ATOMIC_RELAXED,

@@ -430,12 +430,14 @@ __global__ void __launch_bounds__(RT) silu_gate_kernel(const float* P, int64_t s
 // swapping bits 2 and 3 of the row index: then the 8 accumulators a lane
 // feeds into each P.V k-step are exactly the 8 consecutive keys the MFMA
 // operand layout asks for, and the probabilities go to the second MFMA
-// (O^T += V_blk^T P^T) without any shuffle. V is staged transposed
-// ([dim][key]) for that MFMA's other operand. A wave only touches its own
-// LDS region inside the loop, so the loop needs no workgroup barrier. The
-// output O (the O projection's input) is written k-step-major.
+// (O^T += V_blk^T P^T) without any shuffle. V is staged row-major like K
+// (16-byte writes) and that MFMA's V^T operand (8 keys of one dimension per
+// lane) is gathered with eight 2-byte reads; with rows of D + 8 halves the
+// two half-waves of each read fall 32 banks apart. A wave only touches its
+// own LDS region inside the loop, so the loop needs no workgroup barrier.
+// The output O (the O projection's input) is written k-step-major.
 // ---------------------------------------------------------------------------
-constexpr int QB = 32, KB = 32, AW = 4;
+constexpr int QB = 32, KB = 32, AW = 8;
 
 __device__ __forceinline__ int swap_bits23(int r) {
   return (r & ~0xC) | ((r & 4) << 1) | ((r & 8) >> 1);
@@ -443,10 +445,9 @@ __device__ __forceinline__ int swap_bits23(int r) {
 
 template <int D>
 struct AttnLds {
-  static constexpr int KLD = D + 8;   // row stride of the K tile (halves)
-  static constexpr int VLD = KB + 8;  // row stride of the transposed V tile
+  static constexpr int KLD = D + 8;   // row stride of the K and V tiles (halves)
   static constexpr int OLD = D + 4;   // row stride of a wave's fp32 output in the merge
-  static constexpr int WAVE_HALVES = KB * KLD + D * VLD;
+  static constexpr int WAVE_HALVES = 2 * KB * KLD;
   static_assert(WAVE_HALVES * 2 >= (QB * OLD + 2 * QB) * 4, "merge buffer must fit a wave's region");
 };
 
@@ -455,14 +456,18 @@ __global__ void __launch_bounds__(AW * kWave) attn_prefill_kernel(const uint16_t
                                                                   const uint16_t* kc, const uint16_t* vc,
                                                                   int T, int nq, int G, int cap, int pos0) {
   using LY = AttnLds<D>;
-  constexpr int KLD = LY::KLD, VLD = LY::VLD, OLD = LY::OLD;
+  constexpr int KLD = LY::KLD, OLD = LY::OLD;
   __shared__ __attribute__((aligned(16))) uint16_t smem[AW * LY::WAVE_HALVES];
   const int lane = threadIdx.x % kWave;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   uint16_t* Ks = smem + wave * LY::WAVE_HALVES;
-  uint16_t* Vt = Ks + KB * KLD;
+  uint16_t* Vs = Ks + KB * KLD;
+  // Workgroups with equal index mod 8 run on one XCD: the query blocks of a
+  // head get indices that differ by multiples of 8, so the head's K/V comes
+  // from HBM once into that XCD's L2.
   const int nqb = (T + QB - 1) / QB;
-  const int j = blockIdx.x / nqb, qb = blockIdx.x % nqb;
+  const int j = blockIdx.x % 8 + 8 * (blockIdx.x / (8 * nqb)), qb = (blockIdx.x / 8) % nqb;
+  if (j >= nq) return;
   const int g = j / G;
   const int t0 = qb * QB;
   const int tq = t0 + lane % 32;  // this lane's query (token index)
@@ -505,7 +510,7 @@ __global__ void __launch_bounds__(AW * kWave) attn_prefill_kernel(const uint16_t
   fetch(min(wave, nkb - 1));
   for (int kb = wave; kb < nkb; kb += AW) {
     const int p0 = kb * KB;
-    // stage K (rows permuted) and V (transposed), then start the next block
+    // stage K (rows permuted) and V (row-major), then start the next block
 #pragma unroll
     for (int u = 0; u < CPL; ++u) {
       const int c = lane + u * kWave;
@@ -514,13 +519,7 @@ __global__ void __launch_bounds__(AW * kWave) attn_prefill_kernel(const uint16_t
       const u32x4 kv = live ? kreg[u] : u32x4{0u, 0u, 0u, 0u};
       const u32x4 vv = live ? vreg[u] : u32x4{0u, 0u, 0u, 0u};
       *reinterpret_cast<u32x4*>(Ks + swap_bits23(key) * KLD + col) = kv;
-      const uint16_t vh[8] = {
-          static_cast<uint16_t>(vv.x), static_cast<uint16_t>(vv.x >> 16),
-          static_cast<uint16_t>(vv.y), static_cast<uint16_t>(vv.y >> 16),
-          static_cast<uint16_t>(vv.z), static_cast<uint16_t>(vv.z >> 16),
-          static_cast<uint16_t>(vv.w), static_cast<uint16_t>(vv.w >> 16)};
-#pragma unroll
-      for (int e = 0; e < 8; ++e) Vt[(col + e) * VLD + key] = vh[e];
+      *reinterpret_cast<u32x4*>(Vs + key * KLD + col) = vv;
     }
     // LDS operations of one wave complete in issue order; this keeps the
     // compiler from moving the tile reads above the writes
@@ -570,13 +569,17 @@ __global__ void __launch_bounds__(AW * kWave) attn_prefill_kernel(const uint16_t
       pf[s2].z = ph[8 * s2 + 4] | (static_cast<unsigned>(ph[8 * s2 + 5]) << 16);
       pf[s2].w = ph[8 * s2 + 6] | (static_cast<unsigned>(ph[8 * s2 + 7]) << 16);
     }
+    // V^T operand for dimension tile mt, key step s2: lane l takes dimension
+    // 32 mt + l%32 of keys 16 s2 + 8 (l/32) .. +7
 #pragma unroll
     for (int mt = 0; mt < D / 32; ++mt)
 #pragma unroll
       for (int s2 = 0; s2 < 2; ++s2) {
-        const u32x4 vf = *reinterpret_cast<const u32x4*>(Vt + (mt * 32 + lane % 32) * VLD + s2 * 16 +
-                                                         8 * (lane / 32));
-        o[mt] = mfma32(vf, pf[s2], o[mt]);
+        const uint16_t* vcol = Vs + (s2 * 16 + 8 * (lane / 32)) * KLD + mt * 32 + lane % 32;
+        uint16_t vh[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) vh[e] = vcol[e * KLD];
+        o[mt] = mfma32(pack8(vh), pf[s2], o[mt]);
       }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -858,7 +861,7 @@ extern "C" vt_status vt_layer_prefill_chunk(const vt_shard_spec* spec, const vt_
                       static_cast<uint16_t*>(kv->k), static_cast<uint16_t*>(kv->v), nq, nkv,
                       static_cast<int>(d), kv->capacity, pos0, D.rope_base);
     if ((st = check("rope_append")) != VT_OK) return st;
-    const int blocks = nq * ((n_tok + pf::QB - 1) / pf::QB);
+    const int blocks = (nq + 7) / 8 * 8 * ((n_tok + pf::QB - 1) / pf::QB);
     if (d == 128)
       hipLaunchKernelGGL(pf::attn_prefill_kernel<128>, dim3(blocks), dim3(pf::AW * kWave), 0, s, Qr, Ob,
                          static_cast<const uint16_t*>(kv->k), static_cast<const uint16_t*>(kv->v),
