@@ -18,6 +18,9 @@ What it follows (paper: Voltron, arXiv 2607.07046):
     results are aggregated on the main device.
   * Sec. 4.2.1: shards are assigned to devices greedily by performance,
     i.e. unevenly; ``apportion`` is the reading of that used here.
+  * Sec. 4.3.2 with Sec. 4.2.2 (Communication Scaling, importance-ordered
+    lowering): ``comm`` plans and encodes the transmission precision of a
+    shard's partial sums (FP16 / INT8 / INT4 / pruned blocks).
 
 The paper does not define the decoder's internals (normalisation, rotary
 embedding, FFN form); the readings used here are the Llama layer:
