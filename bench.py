@@ -12,7 +12,9 @@ position 1024 of its copy. Inputs are resident in HBM before timing starts.
 
 Prints one JSON line. ``value`` is tokens/s (steps per second), the HBM
 figure is algorithmic bytes per step / time per step, and ``roofline``
-reports the decode kernel against the 8 TB/s HBM peak. ``cpu_baseline`` is
+reports the decode kernel against the 8 TB/s HBM peak. The ``prefill``
+section times the 256-token prefill chunk (MFMA utilisation) and the
+``comm`` section the partial-sum transmission kernels. ``cpu_baseline`` is
 the fp64 oracle timed on the host cores on a bounded sample of the same
 workload (a reference, not the target).
 """
@@ -87,6 +89,8 @@ def parse():
                     help="host time budget of the oracle baseline (0: skip)")
     ap.add_argument("--prefill-steps", type=int, default=200,
                     help="timed prefill chunks of the prefill section (0: skip)")
+    ap.add_argument("--comm-steps", type=int, default=400,
+                    help="timed calls of each partial-sum transmission kernel (0: skip)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="instead of the bench: copy MIB MiB device-to-device 10 times "
                          "(the known-size kernel that scales the HBM byte counters)")
@@ -273,9 +277,69 @@ def main():
     if args.prefill_steps > 0:
         out["prefill"] = prefill_section(args.prefill_steps, max(1, args.prefill_steps // 10),
                                          args.eager)
+    if args.comm_steps > 0:
+        out["comm"] = comm_section(args.comm_steps)
     if args.cpu_seconds > 0:
         out["cpu_baseline"] = cpu_baseline(wl, pos, args.cpu_seconds, step_bytes)
     print(json.dumps(out), flush=True)
+
+
+def comm_section(steps):
+    """Transmission scaling of partial sums (vt_partial_encode /
+    vt_partial_decode_add) for one decode partial (hidden 4096) and one
+    256-token prefill partial, under a plan that halves the message
+    (importance drawn per block, budget = half the FP16 size). 50 calls are
+    captured per HIP graph; about ``steps`` calls are timed."""
+    import numpy as np
+    import torch
+
+    from paper_2607_07046_amd import voltron as vt
+    from synth.gen import vector
+
+    res = {}
+    for name, n in (("decode_partial_4096", 4096), ("prefill_partial_256x4096", 256 * 4096)):
+        nb = n // 32
+        rng = np.random.default_rng(11)
+        prec, offs, total = vt.vt_qplan(rng.random(nb).astype(np.float32), nb * 64 // 2)
+        p = torch.from_numpy(vector(21, n, 2.0)).cuda()
+        base = torch.from_numpy(vector(22, n, 2.0)).cuda()
+        out = torch.empty_like(base)
+        prd, ofd = torch.from_numpy(prec).cuda(), torch.from_numpy(offs).cuda()
+        msg = torch.zeros(max(16, total), dtype=torch.uint8, device="cuda")
+        calls = {
+            "encode": lambda s: vt.vt_partial_encode(p.data_ptr(), n, prd.data_ptr(), ofd.data_ptr(),
+                                                     msg.data_ptr(), total, s),
+            "decode_add": lambda s: vt.vt_partial_decode_add(msg.data_ptr(), total, n,
+                                                             prd.data_ptr(), ofd.data_ptr(),
+                                                             base.data_ptr(), out.data_ptr(), s),
+        }
+        bytes_moved = {"encode": 2 * n + total + 5 * nb, "decode_add": total + 4 * n + 5 * nb}
+        entry = {"n": n, "message_bytes": total, "fp16_bytes": 2 * n,
+                 "levels": {k: int((prec == v).sum()) for k, v in
+                            (("fp16", 0), ("int8", 1), ("int4", 2), ("pruned", 3))}}
+        per_graph = 50  # calls captured per graph, so host launch cost does not dominate
+        reps = max(1, steps // per_graph)
+        for cname, fn in calls.items():
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                for _ in range(per_graph):
+                    fn(torch.cuda.current_stream().cuda_stream)
+            g.replay()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                g.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / (reps * per_graph)
+            entry[cname] = {"us_per_call": round(us, 3),
+                            "GBps": round(bytes_moved[cname] / (us * 1e-6) / 1e9, 1),
+                            "hbm_frac": round(bytes_moved[cname] / (us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)}
+        res[name] = entry
+    res["note"] = ("bytes = fp16 input + message + plan for encode; message + plan + fp16 base "
+                   "and output for decode_add; the 4096-value case is launch-bound")
+    return res
 
 
 def prefill_flops(dims, info, T, pos0):

@@ -208,6 +208,49 @@ vt_status vt_layer_prefill_chunk(const vt_shard_spec* spec, const vt_layer_weigh
                                  int32_t pos0, uint32_t phases, void* ws, size_t ws_bytes,
                                  void* stream);
 
+/* ---- Communication scaling of the partial sums (paper Sec. 4.3.2) ----
+ * To cut the bytes a device sends for the aggregation, its partial sums go
+ * out in blocks of 32 activations, each at one precision; precisions are
+ * lowered in ascending order of importance (Sec. 4.3.2 with the
+ * importance-ordered lowering of Sec. 4.2.2) until the message fits a byte
+ * budget, and pruned blocks are not sent at all.
+ * Block wire format, blocks in index order, block b at offsets[b]:
+ *   VT_PREC_FP16   64 bytes: the 32 fp16 values
+ *   VT_PREC_INT8   36 bytes: fp32 scale s, 32 int8 codes; value = code * s
+ *   VT_PREC_INT4   20 bytes: fp32 scale s, 16 bytes of 4-bit two's-complement
+ *                  codes, element 2k in the low nibble of byte k
+ *   VT_PREC_PRUNED  0 bytes: value 0
+ * Quantisation of a block (symmetric absmax, fp32): s = absmax / Q with
+ * Q = 127 (INT8) or 7 (INT4); code = clamp(rint(x / s), -Q, Q), rint
+ * rounding half to even; an all-zero block has s = 0 and codes 0. */
+enum { VT_PREC_FP16 = 0, VT_PREC_INT8 = 1, VT_PREC_INT4 = 2, VT_PREC_PRUNED = 3 };
+
+/* Host-only plan for n_blocks blocks (1..2^24) with importance scores
+ * importance[b] (finite; higher = more important; the caller sums, per
+ * block, the importance of the weight shards that produce its activations).
+ * All blocks start at FP16; in ascending importance (ties: lower index
+ * first) blocks go FP16 -> INT8 one at a time until the message is at most
+ * budget_bytes; if it is still larger, INT8 -> INT4 in the same order, then
+ * INT4 -> pruned. Writes prec[n_blocks] (VT_PREC_*), offsets[n_blocks]
+ * (bytes) and *total_bytes. All pointers are host memory. */
+vt_status vt_qplan(const float* importance, int32_t n_blocks, int64_t budget_bytes,
+                   uint8_t* prec, int32_t* offsets, int64_t* total_bytes);
+
+/* Encode the fp16 partial sums p[n] (n a positive multiple of 32) into the
+ * message msg[msg_bytes] (device) under a plan held in device memory
+ * (prec[n/32], offsets[n/32], as vt_qplan wrote them). msg must be non-NULL
+ * (16 bytes suffice for an all-pruned plan); nothing is written outside
+ * [msg, msg + msg_bytes) whatever the plan holds. Bytes of msg not covered
+ * by a block are left as they are. */
+vt_status vt_partial_encode(const void* p, int32_t n, const uint8_t* prec, const int32_t* offsets,
+                            void* msg, size_t msg_bytes, void* stream);
+
+/* Receiver side: out[i] = fp16(base[i] + value[i]) for i < n, value as in the
+ * wire format (code * s in fp32, then an fp32 add; base NULL reads as 0).
+ * Reads outside [msg, msg + msg_bytes) return zero. out may equal base. */
+vt_status vt_partial_decode_add(const void* msg, size_t msg_bytes, int32_t n, const uint8_t* prec,
+                                const int32_t* offsets, const void* base, void* out, void* stream);
+
 /* Static text of a status code. */
 const char* vt_status_string(vt_status s);
 

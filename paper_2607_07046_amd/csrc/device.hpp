@@ -93,14 +93,29 @@ __device__ __forceinline__ float wave_sum(float v) {
   return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
 }
 
+// Maximum over the 64 lanes of a wave; every lane gets it (same DPP pattern
+// as wave_sum; -inf is the identity, so masked-off rows add nothing).
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
-  return v;
+  v = fmaxf(v, dpp_f<0xB1>(-INFINITY, v));
+  v = fmaxf(v, dpp_f<0x4E>(-INFINITY, v));
+  v = fmaxf(v, dpp_f<0x141>(-INFINITY, v));
+  v = fmaxf(v, dpp_f<0x140>(-INFINITY, v));
+  v = fmaxf(v, dpp_f<0x142, 0xA>(-INFINITY, v));
+  v = fmaxf(v, dpp_f<0x143, 0xC>(-INFINITY, v));
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
 }
 
-// Sum over groups of ``width`` consecutive lanes (width a power of two <= 64).
+// Sum over groups of ``width`` consecutive lanes; every lane of a group gets
+// the group's sum. Widths 8 and 16 use DPP within a row (quad swaps, then
+// the half-row and row mirrors); other powers of two <= 64 use lane shuffles.
 __device__ __forceinline__ float group_sum(float v, int width) {
+  if (width == 8 || width == 16) {
+    v += dpp_f<0xB1>(0.f, v);    // quad_perm [1,0,3,2]
+    v += dpp_f<0x4E>(0.f, v);    // quad_perm [2,3,0,1]
+    v += dpp_f<0x141>(0.f, v);   // row_half_mirror: the other quad of the half-row
+    if (width == 16) v += dpp_f<0x140>(0.f, v);  // row_mirror: the other half-row
+    return v;
+  }
   for (int o = width >> 1; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
   return v;
 }

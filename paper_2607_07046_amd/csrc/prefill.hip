@@ -126,11 +126,14 @@ __global__ void __launch_bounds__(GT, 2) gemm_kernel(GemmArgs g) {
   const int am = m0 + wave * 32 + lane % 32;
   const uint32_t aoff = am < g.M ? static_cast<uint32_t>(am * 32 + (lane / 32) * 16) : kOOB;
   const int ks0 = kt0 * KSTEPS;            // the split's first k-step
+  // A uniform "out of range" is ORed in as kOOB (valid offsets are below
+  // 2^31): a select on a uniform condition would otherwise become a branch,
+  // which splits the loop into blocks the scheduler cannot interleave.
   auto load_a = [&](int ks, u32x4& dst) {  // k-step ks of this split
     const int sa = ks0 + ks;
-    const bool kin = ks < ks_end && sa < KS;
+    const uint32_t out = (ks < ks_end && sa < KS) ? 0u : kOOB;
     const uint32_t koff = static_cast<uint32_t>(sa) * static_cast<uint32_t>(g.M) * 32u;
-    dst = buf_load16(ra, kin && aoff != kOOB ? aoff + koff : kOOB);
+    dst = buf_load16(ra, (aoff + koff) | out | (aoff & kOOB));
   };
 
   // B chunk offsets (k-independent part); kOOB marks a row past its source
@@ -151,10 +154,10 @@ __global__ void __launch_bounds__(GT, 2) gemm_kernel(GemmArgs g) {
   }
   auto load_b = [&](int kt, u32x4 (&vb)[B_CH]) {  // k-tile kt (absolute)
     const int k = kt * GBK + ccol;
-    const bool kin = kt < kt_end && k < g.K;
+    const uint32_t out = (kt < kt_end && k < g.K) ? 0u : kOOB;
 #pragma unroll
     for (int u = 0; u < B_CH; ++u)
-      vb[u] = buf_load16(rsel[u], kin && boff[u] != kOOB ? boff[u] + k * 2 : kOOB);
+      vb[u] = buf_load16(rsel[u], (boff[u] + static_cast<uint32_t>(k) * 2u) | out | (boff[u] & kOOB));
   };
   auto store_b = [&](uint16_t* st, const u32x4 (&vb)[B_CH]) {
 #pragma unroll

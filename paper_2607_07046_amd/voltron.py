@@ -25,9 +25,12 @@ VT_ATTN = 1
 VT_FFN = 2
 VT_STAGED = 0x100
 
+VT_PREC_FP16, VT_PREC_INT8, VT_PREC_INT4, VT_PREC_PRUNED = 0, 1, 2, 3
+
 # every symbol include/voltron.h declares
 EXPORTS = ("vt_shard_spec_create", "vt_shard_spec_query", "vt_shard_spec_destroy",
            "vt_kv_append", "vt_workspace_size", "vt_layer_decode", "vt_layer_prefill_chunk",
+           "vt_qplan", "vt_partial_encode", "vt_partial_decode_add",
            "vt_status_string", "vt_last_error")
 
 
@@ -105,8 +108,13 @@ def load_library(path=None):
     lib.vt_layer_prefill_chunk.argtypes = [P, ctypes.POINTER(vt_layer_weights),
                                            ctypes.POINTER(vt_kv_view),
                                            ctypes.POINTER(vt_layer_io), I32, I32, U32, P, SZ, P]
+    I64 = ctypes.c_int64
+    lib.vt_qplan.argtypes = [P, I32, I64, P, P, ctypes.POINTER(I64)]
+    lib.vt_partial_encode.argtypes = [P, I32, P, P, P, SZ, P]
+    lib.vt_partial_decode_add.argtypes = [P, SZ, I32, P, P, P, P, P]
     for name in ("vt_shard_spec_create", "vt_shard_spec_query", "vt_kv_append",
-                 "vt_workspace_size", "vt_layer_decode", "vt_layer_prefill_chunk"):
+                 "vt_workspace_size", "vt_layer_decode", "vt_layer_prefill_chunk",
+                 "vt_qplan", "vt_partial_encode", "vt_partial_decode_add"):
         getattr(lib, name).restype = ctypes.c_int
     lib.vt_status_string.argtypes = [ctypes.c_int]
     lib.vt_status_string.restype = ctypes.c_char_p
@@ -182,3 +190,25 @@ def vt_layer_prefill_chunk(spec: ShardSpec, w: vt_layer_weights, kv, io: vt_laye
                                                  ctypes.byref(kv) if kv is not None else None,
                                                  ctypes.byref(io), n_tok, pos0, phases, ws,
                                                  ws_bytes, stream))
+
+
+def vt_qplan(importance, budget_bytes):
+    """Host plan: returns (prec uint8 [nb], offsets int32 [nb], total bytes)."""
+    import numpy as np
+    imp = np.ascontiguousarray(np.asarray(importance, dtype=np.float32))
+    nb = imp.shape[0]
+    prec = np.zeros(nb, dtype=np.uint8)
+    offs = np.zeros(nb, dtype=np.int32)
+    total = ctypes.c_int64(0)
+    _check(load_library().vt_qplan(imp.ctypes.data, nb, int(budget_bytes), prec.ctypes.data,
+                                   offs.ctypes.data, ctypes.byref(total)))
+    return prec, offs, total.value
+
+
+def vt_partial_encode(p, n, prec, offsets, msg, msg_bytes, stream=None):
+    _check(load_library().vt_partial_encode(p, n, prec, offsets, msg, msg_bytes, stream))
+
+
+def vt_partial_decode_add(msg, msg_bytes, n, prec, offsets, base, out, stream=None):
+    _check(load_library().vt_partial_decode_add(msg, msg_bytes, n, prec, offsets, base, out,
+                                                stream))

@@ -151,3 +151,9 @@ class LayerInputs:
 
 def layer_inputs(wl: Workload, layer: int = 0) -> LayerInputs:
     return LayerInputs(wl, layer)
+
+
+def vector(tag: int, n: int, scale: float = 1.0, seed_id: int = 99) -> np.ndarray:
+    """A seeded fp16 vector N(0, scale) of length n, for tests of the
+    partial-sum transmission (``tag`` distinguishes vectors)."""
+    return _normal([ROOT_SEED, seed_id, 0, 1000 + tag, 0], (n,), scale)
