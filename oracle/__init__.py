@@ -21,6 +21,9 @@ What it follows (paper: Voltron, arXiv 2607.07046):
   * Sec. 4.3.2 with Sec. 4.2.2 (Communication Scaling, importance-ordered
     lowering): ``comm`` plans and encodes the transmission precision of a
     shard's partial sums (FP16 / INT8 / INT4 / pruned blocks).
+  * Sec. 2.2, 4.2.2, 4.3.1 (mixed precision, precision scaling):
+    ``wquant`` quantises a shard's weight rows to INT8 / INT4 blocks and
+    gives the values the quantised shard stands for.
 
 The paper does not define the decoder's internals (normalisation, rotary
 embedding, FFN form); the readings used here are the Llama layer:
