@@ -20,9 +20,12 @@ once here and in the design notes):
   small that absmax / Q underflows fp16) has all codes 0;
 * value = code * s;
 * storage of a row: INT8 codes as two's-complement bytes, byte k = column
-  k; INT4 codes as offset-binary nibbles u = code + 8 (1..15), column 2k in
-  the low nibble of byte k, column 2k + 1 in the high nibble; the codes of
-  a row's padded tail are 0. Scales: one fp16 per block, in column order.
+  k; INT4 codes as offset-binary nibbles u = code + 8 (1..15), in groups of
+  8 columns per 4 bytes: column 8g + i (i < 4) in the low nibble of byte
+  4g + i, column 8g + 4 + i in its high nibble (so the low nibbles of a
+  32-bit word are 4 consecutive columns, and so are the high ones); the
+  codes of a row's padded tail are 0. Scales: one fp16 per block, in column
+  order.
 
 Floating-point steps that decide an integer (the codes) are taken in fp32,
 the precision the device kernels use.
@@ -75,7 +78,9 @@ def pack_codes(codes, level):
     if level == INT8:
         return (codes & 0xFF).astype(np.uint8)
     u = (codes + 8).astype(np.uint8)
-    return (u[:, 0::2] | (u[:, 1::2] << 4)).astype(np.uint8)
+    rows, n = u.shape
+    g = u.reshape(rows, n // 8, 2, 4)            # [group][low half / high half][i]
+    return (g[:, :, 0, :] | (g[:, :, 1, :] << 4)).reshape(rows, n // 2).astype(np.uint8)
 
 
 def unpack_codes(packed, level):
@@ -83,10 +88,10 @@ def unpack_codes(packed, level):
     b = np.asarray(packed, dtype=np.uint8).astype(np.int64)
     if level == INT8:
         return np.where(b > 127, b - 256, b)
-    out = np.empty((b.shape[0], b.shape[1] * 2), dtype=np.int64)
-    out[:, 0::2] = (b & 0xF) - 8
-    out[:, 1::2] = (b >> 4) - 8
-    return out
+    rows, nb = b.shape
+    g = b.reshape(rows, nb // 4, 1, 4)
+    out = np.concatenate([(g & 0xF) - 8, (g >> 4) - 8], axis=2)   # [group][half][i]
+    return out.reshape(rows, nb * 2)
 
 
 def dequantized(w, level):

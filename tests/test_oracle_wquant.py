@@ -100,14 +100,14 @@ def test_packing(level):
     packed = W.pack_codes(codes, level)
     assert packed.shape == (6, W.code_bytes_per_row(96, level))
     assert np.array_equal(W.unpack_codes(packed, level), codes)
-    # one non-zero code per row: it lands in byte j (INT8) or in the low /
-    # high nibble of byte j // 2 (INT4); every other nibble is the zero code
+    # one non-zero code per row: it lands in byte j (INT8), or (INT4) column
+    # 8g + i in the low nibble of byte 4g + i and column 8g + 4 + i in its
+    # high nibble; every other nibble is the zero code
     one = np.zeros((2, 64), np.int64)
-    one[0, 10], one[1, 11] = -3, 5
+    one[0, 10], one[1, 13] = -3, 5          # 10 = 8 + 2 (low of byte 6), 13 = 8 + 4 + 1 (high of byte 5)
     p = W.pack_codes(one, level)
     if level == W.INT8:
-        assert p[0, 10] == 253 and p[1, 11] == 5 and np.count_nonzero(p) == 2
+        assert p[0, 10] == 253 and p[1, 13] == 5 and np.count_nonzero(p) == 2
     else:
-        assert p[0, 5] == 0x80 | 5 and p[1, 5] == (13 << 4) | 8
-        rest = np.delete(p, 5, axis=1)
-        assert np.all(rest == 0x88)
+        assert p[0, 6] == 0x80 | 5 and p[1, 5] == (13 << 4) | 8
+        assert np.all(np.delete(p[0], 6) == 0x88) and np.all(np.delete(p[1], 5) == 0x88)
