@@ -14,7 +14,8 @@ Prints one JSON line. ``value`` is tokens/s (steps per second), the HBM
 figure is algorithmic bytes per step / time per step, and ``roofline``
 reports the decode kernel against the 8 TB/s HBM peak. The ``prefill``
 section times the 256-token prefill chunk (MFMA utilisation) and the
-``comm`` section the partial-sum transmission kernels. ``cpu_baseline`` is
+``comm`` section the partial-sum transmission kernels, the ``quant`` section
+the same decode over INT8 and INT4 block-quantised weights. ``cpu_baseline`` is
 the fp64 oracle timed on the host cores on a bounded sample of the same
 workload (a reference, not the target).
 """
@@ -91,6 +92,8 @@ def parse():
                     help="timed prefill chunks of the prefill section (0: skip)")
     ap.add_argument("--comm-steps", type=int, default=400,
                     help="timed calls of each partial-sum transmission kernel (0: skip)")
+    ap.add_argument("--quant-steps", type=int, default=1000,
+                    help="timed decode steps over INT8 and INT4 weight shards (0: skip)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="instead of the bench: copy MIB MiB device-to-device 10 times "
                          "(the known-size kernel that scales the HBM byte counters)")
@@ -279,9 +282,110 @@ def main():
                                          args.eager)
     if args.comm_steps > 0:
         out["comm"] = comm_section(args.comm_steps)
+    if args.quant_steps > 0:
+        out["quant"] = quant_section(spec, dims, info, wl, args.quant_steps,
+                                     max(1, args.quant_steps // 10), layers[0][0], args.eager)
     if args.cpu_seconds > 0:
         out["cpu_baseline"] = cpu_baseline(wl, pos, args.cpu_seconds, step_bytes)
     print(json.dumps(out), flush=True)
+
+
+def quant_bytes(dims, info, pos, prec):
+    """Bytes a decode step over block-quantised weights moves: each matrix's
+    codes (32 or 16 bytes per block of 32 columns) and fp16 scales, the K/V
+    read and written, the gains, x and the four fp16 outputs."""
+    H, d = dims.hidden, dims.head_dim
+    qd, kd, F = info.n_q_heads * d, info.n_kv_heads * d, info.n_cols
+    per_block = (32 if prec == 1 else 16) + 2
+    nb = lambda k: (k + 31) // 32
+    weights = per_block * (qd * nb(H) + 2 * kd * nb(H) + H * nb(qd) + 2 * F * nb(H) + H * nb(F))
+    return weights + 4 * kd * (pos + 1) + 2 * H * (2 + 1 + 4)
+
+
+def quant_section(spec, dims, info, wl, steps, warmup, fp16_weights, eager=False):
+    """Decode over the same shard with INT8 and INT4 block-quantised weights
+    (vt_layer_decode_q). The codes are made once by vt_quantize_rows from
+    the first fp16 copy and cloned into enough distinct copies (>= 768 MB)
+    to keep the Infinity Cache from serving them; steps chain y -> x."""
+    import torch
+
+    from paper_2607_07046_amd import pack
+    from paper_2607_07046_amd import voltron as vt
+    from synth.gen import LayerInputs
+
+    pos, H, d, nkv = wl.ctx, dims.hidden, dims.head_dim, info.n_kv_heads
+    cap = pos + 1
+    li = LayerInputs(wl)
+    k, v = li.kv_context_heads(info.kv_head_begin, info.kv_head_begin + nkv)
+    ws_bytes = vt.vt_workspace_size(spec, 1, cap)
+    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device="cuda")
+    x0 = torch.from_numpy(li.x(0)).cuda()
+    res = {}
+    for name, prec in (("int8", vt.VT_W_INT8), ("int4", vt.VT_W_INT4)):
+        step_bytes = quant_bytes(dims, info, pos, prec)
+        copies = max(1, math.ceil(MALL_DEFEAT_BYTES / step_bytes))
+        q0 = pack.quantize_shard(fp16_weights, dims, info, prec)
+        layers = []
+        for c in range(copies):
+            qc = pack.clone_qshard(q0) if c else q0
+            st = qc.struct
+            kc = torch.zeros((nkv, cap, d), dtype=torch.float16, device="cuda")
+            vc = torch.zeros_like(kc)
+            kc[:, :pos] = torch.from_numpy(k).cuda()
+            vc[:, :pos] = torch.from_numpy(v).cuda()
+            kv = vt.vt_kv_view(k=kc.data_ptr(), v=vc.data_ptr(), capacity=cap, n_kv_heads=nkv,
+                               head_dim=d, len=pos)
+            layers.append((qc, st, kc, vc, kv))
+        bufs = [x0.clone(), torch.empty_like(x0)]
+        p_attn, h, p_ffn = (torch.empty(H, dtype=torch.float16, device="cuda") for _ in range(3))
+
+        def enqueue(i, stream):
+            _, st, _, _, kv = layers[i % copies]
+            kv.len = pos
+            io = vt.vt_layer_io(x=bufs[i % 2].data_ptr(), peer_attn=None, peer_ffn=None,
+                                attn_partial=p_attn.data_ptr(), h=h.data_ptr(),
+                                ffn_partial=p_ffn.data_ptr(), y=bufs[(i + 1) % 2].data_ptr())
+            vt.vt_layer_decode_q(spec, st, kv, io, pos, vt.VT_ATTN | vt.VT_FFN, ws.data_ptr(),
+                                 ws_bytes, stream)
+
+        group = copies * (2 if copies % 2 else 1)
+        per_graph = group * max(1, 64 // group)
+        g = None
+        if not eager:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                for i in range(per_graph):
+                    enqueue(i, torch.cuda.current_stream().cuda_stream)
+
+        def run(n):
+            if g is None:
+                for i in range(n):
+                    enqueue(i, torch.cuda.current_stream().cuda_stream)
+                return n
+            reps = max(1, n // per_graph)
+            for _ in range(reps):
+                g.replay()
+            return reps * per_graph
+
+        run(warmup)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        n = run(steps)
+        e1.record()
+        torch.cuda.synchronize()
+        ms_step = e0.elapsed_time(e1) / n
+        if not torch.isfinite(bufs[0].float()).all():
+            raise SystemExit(f"non-finite output of the {name} decode steps")
+        gbps = step_bytes / (ms_step * 1e-3) / 1e9
+        res[name] = {"ms_per_step": round(ms_step, 6), "tokens_s": round(1e3 / ms_step, 1),
+                     "bytes_per_step": step_bytes, "hbm_GBps": round(gbps, 1),
+                     "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4), "weight_copies": copies,
+                     "steps": n}
+        del layers, q0
+    res["note"] = ("same shard and position as the headline; bytes = codes + fp16 block scales "
+                   "+ K/V + vectors; the format is the library's own 32-column block format")
+    return res
 
 
 def comm_section(steps):

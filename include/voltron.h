@@ -208,6 +208,68 @@ vt_status vt_layer_prefill_chunk(const vt_shard_spec* spec, const vt_layer_weigh
                                  int32_t pos0, uint32_t phases, void* ws, size_t ws_bytes,
                                  void* stream);
 
+/* ---- Block-quantised weight shards (paper Sec. 2.2 precision
+ * heterogeneity, Sec. 4.2.2 importance-aware mixed precision, Sec. 4.3.1
+ * precision scaling) ----
+ * A layer's weights may be held at INT8 or INT4 instead of FP16; which
+ * precision a layer gets is the caller's choice (the paper picks it per
+ * layer by importance under a memory budget). The paper's own block
+ * formats are not defined in it; this library's format is:
+ *  - each row is cut into blocks of 32 consecutive input columns (the last
+ *    block may be partial; its missing columns count as zero);
+ *  - a block has one fp16 scale s = fp16(absmax / Q) (fp32 division, round
+ *    to nearest even; Q = 127 for INT8, 7 for INT4) and codes
+ *    c = clamp(rint(w / s), -Q, Q) (fp32 division, ties to even); s = 0
+ *    (an all-zero block, or absmax / Q below the fp16 range) gives c = 0;
+ *    the weight it stands for is c * s;
+ *  - row r's codes start at codes + r * ld_codes (bytes): INT8 one
+ *    two's-complement byte per column; INT4 offset-binary nibbles c + 8, 8
+ *    columns per 4 bytes, column 8g + i (i < 4) in the low nibble of byte
+ *    4g + i and column 8g + 4 + i in its high nibble. The codes of a row's
+ *    last block past its columns are 0. ld_codes is a multiple of 16 and at
+ *    least 32 (INT8) or 16 (INT4) bytes per block;
+ *  - row r's scales (fp16, one per block in column order) start at
+ *    scales + r * ld_scales (elements); ld_scales >= the block count; the
+ *    scales pointer needs 2-byte alignment only. */
+enum { VT_W_INT8 = 1, VT_W_INT4 = 2 };
+
+typedef struct vt_qmat {
+  const void* codes;
+  int64_t ld_codes;  /* bytes */
+  const void* scales;
+  int64_t ld_scales; /* fp16 elements */
+} vt_qmat;
+
+/* A shard's weights in the block format, all seven matrices at one
+ * precision ``prec`` (VT_W_INT8 or VT_W_INT4). Shapes and slicing as in
+ * vt_layer_weights (wd's row length is the shard's column count; no
+ * further padding is needed: its last block is padded by the format). The
+ * RMSNorm gains stay fp16. */
+typedef struct vt_layer_qweights {
+  int32_t prec;
+  const void* g_attn;
+  vt_qmat wq, wk, wv, wo;
+  const void* g_ffn;
+  vt_qmat wg, wu, wd;
+} vt_layer_qweights;
+
+/* Quantise the fp16 matrix w (rows x cols, row stride ld elements) into
+ * ``prec`` blocks: writes the code bytes of each row's blocks and their
+ * scales; bytes past them (up to ld_codes / ld_scales) are left as they
+ * are. codes holds rows * ld_codes bytes and scales rows * ld_scales fp16
+ * elements (device). */
+vt_status vt_quantize_rows(const void* w, int64_t ld, int32_t rows, int32_t cols, int32_t prec,
+                           void* codes, int64_t ld_codes, void* scales, int64_t ld_scales,
+                           void* stream);
+
+/* vt_layer_decode over block-quantised weights: the same step, every
+ * projection computed as sum over blocks of s * sum(c * x) with the fp16
+ * input x and fp32 accumulation. Same arguments, errors and outputs; in
+ * addition VT_ERR_UNSUPPORTED if a matrix row has more than 16384 columns. */
+vt_status vt_layer_decode_q(const vt_shard_spec* spec, const vt_layer_qweights* w,
+                            vt_kv_view* kv, const vt_layer_io* io, int32_t pos,
+                            uint32_t phases, void* ws, size_t ws_bytes, void* stream);
+
 /* ---- Communication scaling of the partial sums (paper Sec. 4.3.2) ----
  * To cut the bytes a device sends for the aggregation, its partial sums go
  * out in blocks of 32 activations, each at one precision; precisions are

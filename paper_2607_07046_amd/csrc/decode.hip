@@ -35,7 +35,6 @@ namespace dec {
 
 constexpr int NT = 512;          // threads per workgroup (8 waves)
 constexpr int NW = NT / kWave;   // waves per workgroup
-constexpr int SEG = 512;         // fp16 elements per piece (64 lanes x 8)
 constexpr int PF = 16;           // pieces in flight per wave
 constexpr int PRE = 16;          // of which issued before the phase's barrier wait
 constexpr int MAX_SLOTS = 4096;  // pieces per workgroup round (one float each)
@@ -51,8 +50,13 @@ enum { SW_BAR = 0, SW_EXIT = 1024, SW_ERR = 2048, SW_GROUP = 3072, SW_GROUP_STRI
 struct Params {
   int H, d, nq, nkv, G, ncols, pos, cap, nchunk, cl;
   float eps, rope_base;
-  const uint16_t *g_attn, *wq, *wk, *wv, *wo, *g_ffn, *wg, *wu, *wd;
+  const uint16_t *g_attn, *g_ffn;
+  // Weight matrices: fp16 values, or block codes (FMT_Q8 / FMT_Q4) with
+  // their fp16 block scales; row strides in bytes.
+  const uint8_t *wq, *wk, *wv, *wo, *wg, *wu, *wd;
   int64_t ld_q, ld_k, ld_v, ld_o, ld_g, ld_u, ld_d;
+  const uint16_t *sq, *sk, *sv, *so, *sg, *su, *sd;
+  int64_t lds_q, lds_k, lds_v, lds_o, lds_g, lds_u, lds_d;
   uint16_t *kc, *vc;
   uint32_t kv_bytes;  // bytes of each of kc, vc (n_kv * cap * d * 2)
   const uint16_t *x, *peer_a, *peer_f;
@@ -95,47 +99,58 @@ __device__ __forceinline__ void grid_wait(unsigned* sync, unsigned target) {
 // index is wave-uniform, so the buffer selection stays in scalar registers.
 // ---------------------------------------------------------------------------
 struct Mat {
-  rsrc_t r;
-  uint32_t ld;  // row stride in bytes
+  rsrc_t r;      // values or codes
+  uint32_t ld;   // row stride in bytes
+  rsrc_t s;      // block scales (quantised formats)
+  uint32_t lds;  // row stride of the scales in bytes
 };
 
-__device__ __forceinline__ Mat make_mat(const uint16_t* w, int64_t ld, int64_t rows) {
-  return Mat{make_rsrc(w, static_cast<uint32_t>(rows * ld * 2)), static_cast<uint32_t>(ld * 2)};
+__device__ __forceinline__ Mat make_mat(const uint8_t* w, int64_t ld, int64_t rows, const uint16_t* sc,
+                                        int64_t lds) {
+  return Mat{make_rsrc(w, static_cast<uint32_t>(rows * ld)), static_cast<uint32_t>(ld),
+             make_rsrc(sc, static_cast<uint32_t>(rows * lds)), static_cast<uint32_t>(lds)};
+}
+
+// Row r of a row source: the buffer and byte offset of its values / codes
+// and of its block scales.
+struct RowAt {
+  rsrc_t rs, ss;
+  uint32_t off, soff;
+};
+
+__device__ __forceinline__ RowAt mat_row(const Mat& m, int r) {
+  return RowAt{m.r, m.s, static_cast<uint32_t>(r) * m.ld, static_cast<uint32_t>(r) * m.lds};
 }
 
 struct RowsQKV {
   Mat q, k, v;
   int nqd, nkd;
-  __device__ __forceinline__ void at(int r, rsrc_t& rs, uint32_t& off) const {
-    if (r < nqd) {
-      rs = q.r;
-      off = static_cast<uint32_t>(r) * q.ld;
-    } else if (r < nqd + nkd) {
-      rs = k.r;
-      off = static_cast<uint32_t>(r - nqd) * k.ld;
-    } else {
-      rs = v.r;
-      off = static_cast<uint32_t>(r - nqd - nkd) * v.ld;
-    }
+  __device__ __forceinline__ RowAt at(int r) const {
+    return r < nqd ? mat_row(q, r) : r < nqd + nkd ? mat_row(k, r - nqd) : mat_row(v, r - nqd - nkd);
   }
 };
 
 struct RowsOne {
   Mat m;
-  __device__ __forceinline__ void at(int r, rsrc_t& rs, uint32_t& off) const {
-    rs = m.r;
-    off = static_cast<uint32_t>(r) * m.ld;
-  }
+  __device__ __forceinline__ RowAt at(int r) const { return mat_row(m, r); }
 };
 
 struct RowsPair {  // row 2j -> a[j], row 2j+1 -> b[j]
   Mat a, b;
-  __device__ __forceinline__ void at(int r, rsrc_t& rs, uint32_t& off) const {
-    const bool odd = r & 1;
-    rs = odd ? b.r : a.r;
-    off = static_cast<uint32_t>(r >> 1) * (odd ? b.ld : a.ld);
-  }
+  __device__ __forceinline__ RowAt at(int r) const { return (r & 1) ? mat_row(b, r >> 1) : mat_row(a, r >> 1); }
 };
+
+// Weight formats of the GEMV phases: fp16 values, or blocks of 32 columns
+// with an fp16 scale and INT8 / INT4 codes. A piece is 16 bytes per lane;
+// EPL is the number of columns a lane covers in it.
+enum { FMT_F16 = 0, FMT_Q8 = 1, FMT_Q4 = 2 };
+template <int F>
+struct Fmt {
+  static constexpr int EPL = F == FMT_F16 ? 8 : F == FMT_Q8 ? 16 : 32;
+  static constexpr int SEGC = 64 * EPL;  // columns per piece
+};
+
+__host__ __device__ __forceinline__ int seg_cols(int fmt) { return fmt == FMT_F16 ? 512 : fmt == FMT_Q8 ? 1024 : 2048; }
 
 // Zero the fp16 weights of columns >= K in a lane's 8-column chunk starting
 // at ``col`` (row padding may hold anything).
@@ -184,30 +199,100 @@ __device__ __forceinline__ int div_rcp(int q, uint32_t rcp) {
   return static_cast<int>((static_cast<uint64_t>(static_cast<uint32_t>(q)) * rcp) >> 24);
 }
 
-template <int U, class Rows, class Stage, class Epi>
-__device__ __forceinline__ void gemv_phase(const Rows& rows, int units, int K, const uint16_t* xs16,
-                                           float* slots, Stage stage, Epi epi) {
+// Codes to fp16 pairs. A byte u placed under the high byte 0x64 is the fp16
+// number 1024 + u exactly; v_perm_b32 builds two such halves from bytes
+// ``i`` and ``j`` of ``src`` (selector bytes 0-3 pick from its second
+// operand, 4 from the first: 0x64), then the offset (1024 plus the code's
+// bias) is subtracted exactly.
+__device__ __forceinline__ f16x2 code_pair(uint32_t src, uint32_t sel, _Float16 off) {
+  const uint32_t w = __builtin_amdgcn_perm(0x64646464u, src, sel);
+  return __builtin_bit_cast(f16x2, w) - f16x2{off, off};
+}
+constexpr uint32_t kSel01 = 0x04010400u;  // bytes 0 and 1 -> (1024 + b0, 1024 + b1)
+constexpr uint32_t kSel23 = 0x04030402u;  // bytes 2 and 3
+
+__device__ __forceinline__ float dot2h(f16x2 a, uint32_t x, float acc) {
+  return __builtin_amdgcn_fdot2(a, __builtin_bit_cast(f16x2, x), acc, false);
+}
+
+// Sum of 16 INT8 codes (two's complement, column order) times 16 fp16
+// inputs (xa: columns 0-7, xb: 8-15).
+__device__ __forceinline__ float dot_q8(const u32x4 w, const u32x4 xa, const u32x4 xb) {
+  const uint32_t wv[4] = {w.x, w.y, w.z, w.w};
+  const uint32_t xv[8] = {xa.x, xa.y, xa.z, xa.w, xb.x, xb.y, xb.z, xb.w};
+  float acc = 0.f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t t = wv[j] ^ 0x80808080u;  // code + 128 in each byte
+    acc = dot2h(code_pair(t, kSel01, 1152), xv[2 * j], acc);
+    acc = dot2h(code_pair(t, kSel23, 1152), xv[2 * j + 1], acc);
+  }
+  return acc;
+}
+
+// Sum of 32 INT4 codes (offset-binary nibbles; in each 32-bit word the low
+// nibbles are columns 0-3 and the high nibbles columns 4-7 of its group of
+// 8) times 32 fp16 inputs x[0..3] (8 columns each).
+__device__ __forceinline__ float dot_q4(const u32x4 w, const u32x4 (&x)[4]) {
+  const uint32_t wv[4] = {w.x, w.y, w.z, w.w};
+  float acc = 0.f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t lo = wv[j] & 0x0F0F0F0Fu, hi = (wv[j] >> 4) & 0x0F0F0F0Fu;
+    acc = dot2h(code_pair(lo, kSel01, 1032), x[j].x, acc);
+    acc = dot2h(code_pair(lo, kSel23, 1032), x[j].y, acc);
+    acc = dot2h(code_pair(hi, kSel01, 1032), x[j].z, acc);
+    acc = dot2h(code_pair(hi, kSel23, 1032), x[j].w, acc);
+  }
+  return acc;
+}
+
+// Block scales of a quantised format are staged per round in LDS (the
+// rows' scale vectors, up to SC_ROW_WORDS 32-bit words a row per lane):
+// a 2-byte load per piece and lane would double the memory instructions of
+// the weight stream, and the CU's memory pipeline is limited by those.
+constexpr int SC_ROWS = 32;       // scale rows per round (a workgroup)
+constexpr int SC_ROW_WORDS = 4;   // 32-bit words per lane and row: up to 512 blocks (K <= 16384)
+constexpr int SC_LDS_HALFS = SC_ROWS * SC_ROW_WORDS * 2 * kWave;  // 32 rows x 512 scales
+// (a phase is compiled for 1, 2 and 4 words per lane and row, and runs the
+// smallest that holds its rows' blocks: every load, even one that reads
+// past its buffer, costs the memory pipeline an instruction)
+constexpr int SC_PER_WAVE = (SC_ROWS + NW - 1) / NW;
+
+template <int U, int F, int SCW, class Rows, class Stage, class Epi>
+__device__ __forceinline__ void gemv_impl(const Rows& rows, int units, int K, const uint16_t* xs16,
+                                          float* slots, uint16_t* scl, Stage stage, Epi epi) {
+  constexpr int EPL = Fmt<F>::EPL, SEGC = Fmt<F>::SEGC;
+  constexpr bool QUANT = F != FMT_F16;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int lane = threadIdx.x % kWave;
   const int u0 = static_cast<int>(static_cast<int64_t>(units) * blockIdx.x / gridDim.x);
   const int u1 = static_cast<int>(static_cast<int64_t>(units) * (blockIdx.x + 1) / gridDim.x);
-  const int nseg = max(1, (K + SEG - 1) / SEG);
+  const int nseg = max(1, (K + SEGC - 1) / SEGC);
   const uint32_t rcp = (1u << 24) / static_cast<uint32_t>(nseg) + 1u;
-  const int tail = K - (nseg - 1) * SEG;  // columns in a row's last segment
+  const int tail = K - (nseg - 1) * SEGC;  // columns in a row's last segment
   const uint32_t lane16 = static_cast<uint32_t>(lane) * 16u;
-  const bool lane_in_tail = lane * 8 < tail;
-  const int upr = max(1, MAX_SLOTS / (U * nseg));
-  // Load piece p (row p / nseg, segment p % nseg of this round) into a register
-  // quad; p >= q1 (past the wave's run) reads zero without memory traffic.
+  const bool lane_in_tail = lane * EPL < tail;
+  // scale rows in LDS: nbp fp16 per row (the row's blocks, rounded up to
+  // whole 32-bit words of every lane's share)
+  const int nb = (K + 31) / 32;
+  const int sc_words = (nb + 2 * kWave - 1) / (2 * kWave);  // 32-bit loads per lane and row
+  const int nbp = sc_words * 2 * kWave;
+  int upr = max(1, MAX_SLOTS / (U * nseg));
+  if constexpr (QUANT) upr = max(1, min(upr, SC_ROWS / U));
+  // Load piece p (row p / nseg, segment p % nseg of this round) into a
+  // register quad; p >= q1 (past the wave's run) reads zero without memory
+  // traffic. kOOB is OR-ed in arithmetically: a select here can become a
+  // branch around the load, and the branch a full wait for every load in
+  // flight.
   auto issue = [&](int row0, int p, int q1) -> u32x4 {
     const int lr = div_rcp(p, rcp);
     const int sg = p - lr * nseg;
-    rsrc_t rs;
-    uint32_t roff;
-    rows.at(row0 + lr, rs, roff);
-    const uint32_t base = __builtin_amdgcn_readfirstlane(roff + static_cast<uint32_t>(sg) * (SEG * 2u));
+    const RowAt ra = rows.at(row0 + lr);
+    const uint32_t base = __builtin_amdgcn_readfirstlane(ra.off + static_cast<uint32_t>(sg) * 1024u);
     const bool ok = (p < q1) && (sg != nseg - 1 || lane_in_tail);
-    return __builtin_amdgcn_raw_buffer_load_b128(rs, ok ? base + lane16 : kOOB, 0, 0);
+    const uint32_t oob = static_cast<uint32_t>(!ok) << 31;
+    return __builtin_amdgcn_raw_buffer_load_b128(ra.rs, (base + lane16) | oob, 0, 0);
   };
   bool staged = false;
   int ua = u0;
@@ -218,6 +303,27 @@ __device__ __forceinline__ void gemv_phase(const Rows& rows, int units, int K, c
     const int q1 = __builtin_amdgcn_readfirstlane(static_cast<int>(static_cast<int64_t>(np) * (wave + 1) / NW));
     const int row0 = ua * U;
     for (int i = threadIdx.x; i < np; i += NT) slots[i] = 0.f;
+    // The round's scale rows go out first (row vr on wave vr % NW), so they
+    // return ahead of the weight pieces queued behind them.
+    uint32_t sreg[QUANT ? SC_PER_WAVE : 1][SCW];
+    if constexpr (QUANT) {
+      const int nr = K > 0 ? (ub - ua) * U : 0;
+#pragma unroll
+      for (int k = 0; k < SC_PER_WAVE; ++k) {
+        const int vr = wave + k * NW;
+        const RowAt ra = rows.at(row0 + min(vr, max(nr - 1, 0)));
+#pragma unroll
+        for (int w = 0; w < SCW; ++w) {
+          const int idx = w * kWave + lane;  // word of the row: scales 2 idx, 2 idx + 1
+          const uint32_t oob = static_cast<uint32_t>(!(vr < nr && 2 * idx < nb)) << 31;
+          const uint32_t v =
+              __builtin_amdgcn_raw_buffer_load_b32(ra.ss, (ra.soff + static_cast<uint32_t>(idx) * 4u) | oob, 0, 0);
+          // past the row's last block the scale is 0 (the codes there are 0
+          // or unread, and 0 * 0 must stay 0 whatever the padding holds)
+          sreg[k][w] = 2 * idx + 1 < nb ? v : (v & 0xFFFFu);
+        }
+      }
+    }
     u32x4 buf[PF];
     // A few pieces go out before the barrier wait: they cover its latency
     // without queueing so much traffic that the staging loads behind them
@@ -232,27 +338,61 @@ __device__ __forceinline__ void gemv_phase(const Rows& rows, int units, int K, c
     }
 #pragma unroll
     for (int i = PRE; i < PF; ++i) buf[i] = issue(row0, q0 + i, q1);
+    // The scale rows go to LDS once the input is staged: their loads left
+    // first, so they have landed by now and the wait costs nothing.
+    if constexpr (QUANT) {  // scale rows to LDS: row vr at scl + vr * nbp
+      const int nr = K > 0 ? (ub - ua) * U : 0;
+#pragma unroll
+      for (int k = 0; k < SC_PER_WAVE; ++k) {
+        const int vr = wave + k * NW;
+        if (vr < nr) {
+          uint32_t* dst = reinterpret_cast<uint32_t*>(scl + vr * nbp);
+#pragma unroll
+          for (int w = 0; w < SCW; ++w)
+            if (w < sc_words) dst[w * kWave + lane] = sreg[k][w];
+        }
+      }
+      lds_barrier();
+    }
+    // The wave's run in trips of PF pieces; every trip but the last reloads
+    // the ring (a load past the run reads zero but still costs the memory
+    // pipeline an instruction).
     float acc = 0.f;
-    for (int base = q0; base < q1; base += PF) {
+    const int ntrip = (q1 - q0 + PF - 1) / PF;
+    auto trip = [&](int base, bool reload) {
 #pragma unroll
       for (int i = 0; i < PF; ++i) {
         const int q = base + i;
         if (q < q1) {
-          const int cs = q - div_rcp(q, rcp) * nseg;
-          u32x4 w = buf[i];
-          const int col = cs * SEG + lane * 8;
-          const u32x4 x = *reinterpret_cast<const u32x4*>(xs16 + col);
-          if (cs == nseg - 1 && tail < SEG) w = mask_tail(w, col, K);
-          acc = dot8(w, x, acc);
+          const int lr = div_rcp(q, rcp);
+          const int cs = q - lr * nseg;
+          const int col = cs * SEGC + lane * EPL;
+          const u32x4* xp = reinterpret_cast<const u32x4*>(xs16 + col);
+          if constexpr (F == FMT_F16) {
+            u32x4 w = buf[i];
+            if (cs == nseg - 1 && tail < SEGC) w = mask_tail(w, col, K);
+            acc = dot8(w, xp[0], acc);
+          } else {
+            // codes past K are zero by the format, and so is the input
+            const float sc = h2f(scl[lr * nbp + col / 32]);
+            if constexpr (F == FMT_Q8) {
+              acc = fmaf(sc, dot_q8(buf[i], xp[0], xp[1]), acc);
+            } else {
+              const u32x4 xq[4] = {xp[0], xp[1], xp[2], xp[3]};
+              acc = fmaf(sc, dot_q4(buf[i], xq), acc);
+            }
+          }
           if (cs == nseg - 1 || q == q1 - 1) {
             const float t = wave_sum(acc);
             if (lane == 0) slots[q] = t;
             acc = 0.f;
           }
         }
-        buf[i] = issue(row0, q + PF, q1);
+        if (reload) buf[i] = issue(row0, q + PF, q1);
       }
-    }
+    };
+    for (int tr = 0; tr + 1 < ntrip; ++tr) trip(q0 + tr * PF, true);
+    if (ntrip > 0) trip(q0 + (ntrip - 1) * PF, false);
     lds_barrier();  // every slot written
     for (int lu = threadIdx.x; lu < ub - ua; lu += NT) {
       float v[U];
@@ -267,9 +407,25 @@ __device__ __forceinline__ void gemv_phase(const Rows& rows, int units, int K, c
       }
       epi(ua + lu, v);
     }
-    lds_barrier();  // slots and xs free for reuse
+    lds_barrier();  // slots, scales and xs free for reuse
     ua = ub;
   } while (ua < u1);
+}
+
+template <int U, int F, class Rows, class Stage, class Epi>
+__device__ __forceinline__ void gemv_phase(const Rows& rows, int units, int K, const uint16_t* xs16,
+                                           float* slots, uint16_t* scl, Stage stage, Epi epi) {
+  if constexpr (F == FMT_F16) {
+    gemv_impl<U, F, 1>(rows, units, K, xs16, slots, scl, stage, epi);
+  } else {
+    const int words = ((K + 31) / 32 + 2 * kWave - 1) / (2 * kWave);  // per lane and scale row
+    if (words <= 1)
+      gemv_impl<U, F, 1>(rows, units, K, xs16, slots, scl, stage, epi);
+    else if (words <= 2)
+      gemv_impl<U, F, 2>(rows, units, K, xs16, slots, scl, stage, epi);
+    else
+      gemv_impl<U, F, SC_ROW_WORDS>(rows, units, K, xs16, slots, scl, stage, epi);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -384,7 +540,11 @@ __device__ __forceinline__ void stage_copy_f(const float* v, int n, int npad, ui
   __syncthreads();
 }
 
-__host__ __device__ __forceinline__ int padded(int K) { return ((K + SEG - 1) / SEG) * SEG; }
+// K rounded up to whole pieces of the format's segment.
+__host__ __device__ __forceinline__ int padded(int K, int fmt) {
+  const int sc = seg_cols(fmt);
+  return ((K + sc - 1) / sc) * sc;
+}
 
 // ---------------------------------------------------------------------------
 // phase 1: attention
@@ -637,26 +797,28 @@ __device__ __forceinline__ void phase_attn(const Params& P, float* lds, bool wai
 // the kernel
 // ---------------------------------------------------------------------------
 // One phase; ``wait`` / ``target`` describe the grid barrier in front of it.
-template <int PH>
+template <int PH, int F>
 __device__ __forceinline__ void run_phase(const Params& P, float* lds, uint16_t* xs, float* slots,
                                           float* red, bool wait, unsigned target) {
+  uint16_t* scl = reinterpret_cast<uint16_t*>(red + 16);  // block scales (quantised formats)
   if constexpr (PH == PH_QKV) {
-    RowsQKV rows{make_mat(P.wq, P.ld_q, P.nq * P.d), make_mat(P.wk, P.ld_k, P.nkv * P.d),
-                 make_mat(P.wv, P.ld_v, P.nkv * P.d), P.nq * P.d, P.nkv * P.d};
-    gemv_phase<1>(
-        rows, (P.nq + 2 * P.nkv) * P.d, P.H, xs, slots,
-        [&]() { stage_rmsnorm_h(P.x, P.g_attn, P.H, padded(P.H), P.eps, xs, red); },
+    RowsQKV rows{make_mat(P.wq, P.ld_q, P.nq * P.d, P.sq, P.lds_q),
+                 make_mat(P.wk, P.ld_k, P.nkv * P.d, P.sk, P.lds_k),
+                 make_mat(P.wv, P.ld_v, P.nkv * P.d, P.sv, P.lds_v), P.nq * P.d, P.nkv * P.d};
+    gemv_phase<1, F>(
+        rows, (P.nq + 2 * P.nkv) * P.d, P.H, xs, slots, scl,
+        [&]() { stage_rmsnorm_h(P.x, P.g_attn, P.H, padded(P.H, F), P.eps, xs, red); },
         [&](int r, const float* v) { st_shared(P.qkv + r, v[0]); });
   } else if constexpr (PH == PH_ATTN) {
     phase_attn(P, lds, wait, target);
   } else if constexpr (PH == PH_O) {
-    RowsOne rows{make_mat(P.wo, P.ld_o, P.H)};
+    RowsOne rows{make_mat(P.wo, P.ld_o, P.H, P.so, P.lds_o)};
     const int K = P.nq * P.d;
-    gemv_phase<1>(
-        rows, P.H, K, xs, slots,
+    gemv_phase<1, F>(
+        rows, P.H, K, xs, slots, scl,
         [&]() {
           if (wait) grid_wait(P.sync, target);
-          stage_copy_f(P.o, K, padded(K), xs);
+          stage_copy_f(P.o, K, padded(K, F), xs);
         },
         [&](int r, const float* v) {
           const float pa = v[0];
@@ -666,28 +828,29 @@ __device__ __forceinline__ void run_phase(const Params& P, float* lds, uint16_t*
           st_shared(P.hbuf + r, hv);
         });
   } else if constexpr (PH == PH_GATEUP) {
-    RowsPair rows{make_mat(P.wg, P.ld_g, P.ncols), make_mat(P.wu, P.ld_u, P.ncols)};
-    gemv_phase<2>(
-        rows, P.ncols, P.H, xs, slots,
+    RowsPair rows{make_mat(P.wg, P.ld_g, P.ncols, P.sg, P.lds_g),
+                  make_mat(P.wu, P.ld_u, P.ncols, P.su, P.lds_u)};
+    gemv_phase<2, F>(
+        rows, P.ncols, P.H, xs, slots, scl,
         [&]() {
           if (wait) grid_wait(P.sync, target);
           if (P.h_from_ws)
-            stage_rmsnorm_f(P.hbuf, P.g_ffn, P.H, padded(P.H), P.eps, xs, red);
+            stage_rmsnorm_f(P.hbuf, P.g_ffn, P.H, padded(P.H, F), P.eps, xs, red);
           else
-            stage_rmsnorm_h(P.h, P.g_ffn, P.H, padded(P.H), P.eps, xs, red);
+            stage_rmsnorm_h(P.h, P.g_ffn, P.H, padded(P.H, F), P.eps, xs, red);
         },
         [&](int j, const float* v) {
           const float gt = v[0], up = v[1];
           st_shared(P.m + j, gt / (1.0f + __expf(-gt)) * up);
         });
   } else {
-    RowsOne rows{make_mat(P.wd, P.ld_d, P.H)};
+    RowsOne rows{make_mat(P.wd, P.ld_d, P.H, P.sd, P.lds_d)};
     const int K = P.ncols;
-    gemv_phase<1>(
-        rows, P.H, K, xs, slots,
+    gemv_phase<1, F>(
+        rows, P.H, K, xs, slots, scl,
         [&]() {
           if (wait) grid_wait(P.sync, target);
-          stage_copy_f(P.m, K, padded(K), xs);
+          stage_copy_f(P.m, K, padded(K, F), xs);
         },
         [&](int r, const float* v) {
           const float pf = v[0];
@@ -700,28 +863,29 @@ __device__ __forceinline__ void run_phase(const Params& P, float* lds, uint16_t*
   }
 }
 
-template <int PH, int PE, int PB>
+template <int PH, int PE, int PB, int F>
 __device__ __forceinline__ void run_phases(const Params& P, float* lds, uint16_t* xs, float* slots,
                                            float* red) {
-  run_phase<PH>(P, lds, xs, slots, red, PH > PB, static_cast<unsigned>(PH - PB) * gridDim.x);
+  run_phase<PH, F>(P, lds, xs, slots, red, PH > PB, static_cast<unsigned>(PH - PB) * gridDim.x);
   if constexpr (PH < PE) {
     grid_arrive(P.sync);
-    run_phases<PH + 1, PE, PB>(P, lds, xs, slots, red);
+    run_phases<PH + 1, PE, PB, F>(P, lds, xs, slots, red);
   }
 }
 
 // Phases PB..PE of one decode step. PB < PE needs every workgroup resident
 // (one per CU): grid barriers separate the phases.
-template <int PB, int PE>
+template <int PB, int PE, int F>
 __global__ void __launch_bounds__(NT) decode_kernel(Params P) {
   extern __shared__ float lds[];
-  // LDS: xs / attention scratch (aliased) | slots[MAX_SLOTS] | red[NW]
-  const int kmax = max(max(padded(P.H), padded(P.nq * P.d)), padded(P.ncols));
+  // LDS: xs / attention scratch (aliased) | slots[MAX_SLOTS] | red[16] |
+  // block scales (quantised formats)
+  const int kmax = max(max(padded(P.H, F), padded(P.nq * P.d, F)), padded(P.ncols, F));
   const int attn = attn_lds_floats(P.d, P.nchunk);
   uint16_t* xs = reinterpret_cast<uint16_t*>(lds);  // fp16 GEMV input (kmax halfs)
   float* slots = lds + max(kmax / 2, attn);
   float* red = slots + MAX_SLOTS;
-  run_phases<PB, PE, PB>(P, lds, xs, slots, red);
+  run_phases<PB, PE, PB, F>(P, lds, xs, slots, red);
   if constexpr (PE > PB) {  // the last workgroup out clears the barrier words
     __syncthreads();
     if (threadIdx.x == 0) {
@@ -738,18 +902,28 @@ __global__ void __launch_bounds__(NT) decode_kernel(Params P) {
 typedef void (*DecodeKernel)(Params);
 
 // Instantiations: the whole step, each sub-layer, and each phase alone.
-__host__ inline DecodeKernel decode_kernel_for(int pb, int pe) {
-  if (pb == PH_QKV && pe == PH_DOWN) return decode_kernel<PH_QKV, PH_DOWN>;
-  if (pb == PH_QKV && pe == PH_O) return decode_kernel<PH_QKV, PH_O>;
-  if (pb == PH_GATEUP && pe == PH_DOWN) return decode_kernel<PH_GATEUP, PH_DOWN>;
+template <int F>
+__host__ inline DecodeKernel decode_kernel_fmt(int pb, int pe) {
+  if (pb == PH_QKV && pe == PH_DOWN) return decode_kernel<PH_QKV, PH_DOWN, F>;
+  if (pb == PH_QKV && pe == PH_O) return decode_kernel<PH_QKV, PH_O, F>;
+  if (pb == PH_GATEUP && pe == PH_DOWN) return decode_kernel<PH_GATEUP, PH_DOWN, F>;
   if (pb == pe) {
     switch (pb) {
-      case PH_QKV: return decode_kernel<PH_QKV, PH_QKV>;
-      case PH_ATTN: return decode_kernel<PH_ATTN, PH_ATTN>;
-      case PH_O: return decode_kernel<PH_O, PH_O>;
-      case PH_GATEUP: return decode_kernel<PH_GATEUP, PH_GATEUP>;
-      case PH_DOWN: return decode_kernel<PH_DOWN, PH_DOWN>;
+      case PH_QKV: return decode_kernel<PH_QKV, PH_QKV, F>;
+      case PH_ATTN: return decode_kernel<PH_ATTN, PH_ATTN, F>;
+      case PH_O: return decode_kernel<PH_O, PH_O, F>;
+      case PH_GATEUP: return decode_kernel<PH_GATEUP, PH_GATEUP, F>;
+      case PH_DOWN: return decode_kernel<PH_DOWN, PH_DOWN, F>;
     }
+  }
+  return nullptr;
+}
+
+__host__ inline DecodeKernel decode_kernel_for(int pb, int pe, int fmt) {
+  switch (fmt) {
+    case FMT_F16: return decode_kernel_fmt<FMT_F16>(pb, pe);
+    case FMT_Q8: return decode_kernel_fmt<FMT_Q8>(pb, pe);
+    case FMT_Q4: return decode_kernel_fmt<FMT_Q4>(pb, pe);
   }
   return nullptr;
 }
@@ -812,10 +986,11 @@ vt_status device_info(DeviceInfo** out) {
     // Allow dynamic LDS up to the device limit; a refusal surfaces as a
     // launch error for the shapes that would need it.
     const int ranges[][2] = {{0, 4}, {0, 2}, {3, 4}, {0, 0}, {1, 1}, {2, 2}, {3, 3}, {4, 4}};
-    for (const auto& r : ranges)
-      (void)hipFuncSetAttribute(reinterpret_cast<const void*>(dec::decode_kernel_for(r[0], r[1])),
-                                hipFuncAttributeMaxDynamicSharedMemorySize,
-                                static_cast<int>(di.max_lds));
+    for (int fmt : {dec::FMT_F16, dec::FMT_Q8, dec::FMT_Q4})
+      for (const auto& r : ranges)
+        (void)hipFuncSetAttribute(reinterpret_cast<const void*>(dec::decode_kernel_for(r[0], r[1], fmt)),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize,
+                                  static_cast<int>(di.max_lds));
     (void)hipGetLastError();
     di.lds_attr_set = true;
   }
@@ -917,6 +1092,66 @@ vt_status check_weights(const vt_shard_spec& s, const vt_layer_weights* w, bool 
   return VT_OK;
 }
 
+// Block-quantised weights: per matrix the codes (16-byte aligned rows of at
+// least the row's code bytes) and the scales (2-byte aligned, at least one
+// per block), each within the 2 GiB a buffer resource addresses.
+static vt_status check_qweights(const vt_shard_spec& s, const vt_layer_qweights* w, bool attn, bool ffn) {
+  if (!w) return fail(VT_ERR_ARG, "null weights");
+  if (w->prec != VT_W_INT8 && w->prec != VT_W_INT4)
+    return fail(VT_ERR_ARG, "weight precision %d is neither VT_W_INT8 nor VT_W_INT4", w->prec);
+  const int H = s.dims.hidden, d = s.dims.head_dim;
+  const vt_shard_info& in = s.info;
+  // a row's block scales are staged in LDS, at most 512 of them
+  const int64_t kmax = std::max({static_cast<int64_t>(H), static_cast<int64_t>(in.n_q_heads) * d,
+                                 static_cast<int64_t>(in.n_cols)});
+  if (kmax > 16384)
+    return fail(VT_ERR_UNSUPPORTED, "quantised rows of %lld columns; at most 16384",
+                static_cast<long long>(kmax));
+  auto mat = [&](const vt_qmat& m, int64_t rowlen, int64_t rows, const char* name) -> vt_status {
+    const int64_t nb = (rowlen + 31) / 32;
+    const int64_t need = nb * (w->prec == VT_W_INT8 ? 32 : 16);
+    if (!m.codes || !m.scales) return fail(VT_ERR_ARG, "codes or scales of %s are NULL", name);
+    if (!aligned16(m.codes)) return fail(VT_ERR_ALIGN, "codes of %s are not 16-byte aligned", name);
+    if (reinterpret_cast<uintptr_t>(m.scales) % 2)
+      return fail(VT_ERR_ALIGN, "scales of %s are not 2-byte aligned", name);
+    if (m.ld_codes < need || m.ld_codes % 16)
+      return fail(VT_ERR_ARG, "ld_codes of %s (%lld) must be a multiple of 16 and >= %lld", name,
+                  static_cast<long long>(m.ld_codes), static_cast<long long>(need));
+    if (m.ld_scales < nb)
+      return fail(VT_ERR_ARG, "ld_scales of %s (%lld) < %lld blocks", name,
+                  static_cast<long long>(m.ld_scales), static_cast<long long>(nb));
+    if (rows * m.ld_codes >= kMaxBufferBytes || rows * m.ld_scales * 2 >= kMaxBufferBytes)
+      return fail(VT_ERR_UNSUPPORTED, "weight %s spans 2 GiB or more; the kernels address < 2 GiB", name);
+    return VT_OK;
+  };
+  auto gain = [&](const void* p, const char* name) -> vt_status {
+    if (!p) return fail(VT_ERR_ARG, "gain %s is NULL", name);
+    if (!aligned16(p)) return fail(VT_ERR_ALIGN, "gain %s is not 16-byte aligned", name);
+    return VT_OK;
+  };
+  vt_status st;
+  if (attn) {
+    if ((st = gain(w->g_attn, "g_attn")) != VT_OK) return st;
+    if (in.n_q_heads > 0) {
+      const int64_t qd = static_cast<int64_t>(in.n_q_heads) * d;
+      const int64_t kd = static_cast<int64_t>(in.n_kv_heads) * d;
+      if ((st = mat(w->wq, H, qd, "wq")) != VT_OK) return st;
+      if ((st = mat(w->wk, H, kd, "wk")) != VT_OK) return st;
+      if ((st = mat(w->wv, H, kd, "wv")) != VT_OK) return st;
+      if ((st = mat(w->wo, qd, H, "wo")) != VT_OK) return st;
+    }
+  }
+  if (ffn) {
+    if ((st = gain(w->g_ffn, "g_ffn")) != VT_OK) return st;
+    if (in.n_cols > 0) {
+      if ((st = mat(w->wg, H, in.n_cols, "wg")) != VT_OK) return st;
+      if ((st = mat(w->wu, H, in.n_cols, "wu")) != VT_OK) return st;
+      if ((st = mat(w->wd, in.n_cols, H, "wd")) != VT_OK) return st;
+    }
+  }
+  return VT_OK;
+}
+
 vt_status check_kv(const vt_shard_spec& s, const vt_kv_view* kv, int32_t pos, int32_t n_tok) {
   if (!kv) return fail(VT_ERR_ARG, "null KV view");
   if (kv->n_kv_heads != s.info.n_kv_heads || kv->head_dim != s.dims.head_dim)
@@ -981,18 +1216,77 @@ extern "C" vt_status vt_kv_append(vt_kv_view* kv, const void* k, const void* v, 
   return VT_OK;
 }
 
+// The weights of a decode call in a format-neutral view: per matrix (q, k,
+// v, o, gate, up, down) the values or codes and their row stride in bytes,
+// and for the quantised formats the block scales and their stride in bytes.
+struct WeightView {
+  int fmt;
+  const void *g_attn, *g_ffn;
+  const void* w[7];
+  int64_t ld[7];
+  const void* sc[7];
+  int64_t lds[7];
+};
+
+static vt_status decode_impl(const vt_shard_spec* spec, const WeightView& W, vt_kv_view* kv,
+                             const vt_layer_io* io, int32_t pos, uint32_t phases, void* ws,
+                             size_t ws_bytes, void* stream);
+
+static vt_status check_phases(const vt_shard_spec* spec, const vt_layer_io* io, uint32_t phases) {
+  if (!spec || !io) return fail(VT_ERR_ARG, "null spec or io");
+  if (phases & ~(VT_ATTN | VT_FFN | VT_STAGED)) return fail(VT_ERR_ARG, "unknown phase bits 0x%x", phases);
+  if (!(phases & (VT_ATTN | VT_FFN))) return fail(VT_ERR_ARG, "no phase selected");
+  return VT_OK;
+}
+
 extern "C" vt_status vt_layer_decode(const vt_shard_spec* spec, const vt_layer_weights* w,
                                      vt_kv_view* kv, const vt_layer_io* io, int32_t pos,
                                      uint32_t phases, void* ws, size_t ws_bytes, void* stream) {
   clear_error();
-  if (!spec || !io) return fail(VT_ERR_ARG, "null spec or io");
-  if (phases & ~(VT_ATTN | VT_FFN | VT_STAGED)) return fail(VT_ERR_ARG, "unknown phase bits 0x%x", phases);
+  vt_status st = check_phases(spec, io, phases);
+  if (st != VT_OK) return st;
+  if ((st = check_weights(*spec, w, phases & VT_ATTN, phases & VT_FFN)) != VT_OK) return st;
+  WeightView W{};
+  W.fmt = dec::FMT_F16;
+  W.g_attn = w->g_attn;
+  W.g_ffn = w->g_ffn;
+  const void* ptrs[7] = {w->wq, w->wk, w->wv, w->wo, w->wg, w->wu, w->wd};
+  const int64_t lds[7] = {w->ld_q, w->ld_k, w->ld_v, w->ld_o, w->ld_g, w->ld_u, w->ld_d};
+  for (int i = 0; i < 7; ++i) {
+    W.w[i] = ptrs[i];
+    W.ld[i] = lds[i] * 2;
+  }
+  return decode_impl(spec, W, kv, io, pos, phases, ws, ws_bytes, stream);
+}
+
+extern "C" vt_status vt_layer_decode_q(const vt_shard_spec* spec, const vt_layer_qweights* w,
+                                       vt_kv_view* kv, const vt_layer_io* io, int32_t pos,
+                                       uint32_t phases, void* ws, size_t ws_bytes, void* stream) {
+  clear_error();
+  vt_status st = check_phases(spec, io, phases);
+  if (st != VT_OK) return st;
+  if ((st = check_qweights(*spec, w, phases & VT_ATTN, phases & VT_FFN)) != VT_OK) return st;
+  WeightView W{};
+  W.fmt = w->prec == VT_W_INT8 ? dec::FMT_Q8 : dec::FMT_Q4;
+  W.g_attn = w->g_attn;
+  W.g_ffn = w->g_ffn;
+  const vt_qmat* m[7] = {&w->wq, &w->wk, &w->wv, &w->wo, &w->wg, &w->wu, &w->wd};
+  for (int i = 0; i < 7; ++i) {
+    W.w[i] = m[i]->codes;
+    W.ld[i] = m[i]->ld_codes;
+    W.sc[i] = m[i]->scales;
+    W.lds[i] = m[i]->ld_scales * 2;
+  }
+  return decode_impl(spec, W, kv, io, pos, phases, ws, ws_bytes, stream);
+}
+
+static vt_status decode_impl(const vt_shard_spec* spec, const WeightView& W, vt_kv_view* kv,
+                             const vt_layer_io* io, int32_t pos, uint32_t phases, void* ws,
+                             size_t ws_bytes, void* stream) {
   const bool attn = phases & VT_ATTN, ffn = phases & VT_FFN, staged = phases & VT_STAGED;
-  if (!attn && !ffn) return fail(VT_ERR_ARG, "no phase selected");
   const vt_layer_dims& D = spec->dims;
   const vt_shard_info& in = spec->info;
-  vt_status st = check_weights(*spec, w, attn, ffn);
-  if (st != VT_OK) return st;
+  vt_status st = VT_OK;
   if (attn) {
     if ((st = check_kv(*spec, kv, pos, 1)) != VT_OK) return st;
     if ((st = check_io_vec(io->x, "x", true)) != VT_OK) return st;
@@ -1026,22 +1320,18 @@ extern "C" vt_status vt_layer_decode(const vt_shard_spec* spec, const vt_layer_w
   attn_chunking(D.head_dim, in.n_q_heads, ctx, di->cus, &P.cl, &P.nchunk);
   P.eps = D.rms_eps;
   P.rope_base = D.rope_base;
-  P.g_attn = static_cast<const uint16_t*>(w->g_attn);
-  P.wq = static_cast<const uint16_t*>(w->wq);
-  P.wk = static_cast<const uint16_t*>(w->wk);
-  P.wv = static_cast<const uint16_t*>(w->wv);
-  P.wo = static_cast<const uint16_t*>(w->wo);
-  P.g_ffn = static_cast<const uint16_t*>(w->g_ffn);
-  P.wg = static_cast<const uint16_t*>(w->wg);
-  P.wu = static_cast<const uint16_t*>(w->wu);
-  P.wd = static_cast<const uint16_t*>(w->wd);
-  P.ld_q = w->ld_q;
-  P.ld_k = w->ld_k;
-  P.ld_v = w->ld_v;
-  P.ld_o = w->ld_o;
-  P.ld_g = w->ld_g;
-  P.ld_u = w->ld_u;
-  P.ld_d = w->ld_d;
+  P.g_attn = static_cast<const uint16_t*>(W.g_attn);
+  P.g_ffn = static_cast<const uint16_t*>(W.g_ffn);
+  const uint8_t** wp[7] = {&P.wq, &P.wk, &P.wv, &P.wo, &P.wg, &P.wu, &P.wd};
+  int64_t* ldp[7] = {&P.ld_q, &P.ld_k, &P.ld_v, &P.ld_o, &P.ld_g, &P.ld_u, &P.ld_d};
+  const uint16_t** sp[7] = {&P.sq, &P.sk, &P.sv, &P.so, &P.sg, &P.su, &P.sd};
+  int64_t* lsp[7] = {&P.lds_q, &P.lds_k, &P.lds_v, &P.lds_o, &P.lds_g, &P.lds_u, &P.lds_d};
+  for (int i = 0; i < 7; ++i) {
+    *wp[i] = static_cast<const uint8_t*>(W.w[i]);
+    *ldp[i] = W.ld[i];
+    *sp[i] = static_cast<const uint16_t*>(W.sc[i]);
+    *lsp[i] = W.lds[i];
+  }
   P.kc = kv ? static_cast<uint16_t*>(kv->k) : nullptr;
   P.vc = kv ? static_cast<uint16_t*>(kv->v) : nullptr;
   P.kv_bytes = kv ? static_cast<uint32_t>(static_cast<int64_t>(kv->n_kv_heads) * kv->capacity *
@@ -1063,10 +1353,11 @@ extern "C" vt_status vt_layer_decode(const vt_shard_spec* spec, const vt_layer_w
   P.hbuf = reinterpret_cast<float*>(base + L.hbuf);
   P.h_from_ws = attn ? 1 : 0;
 
-  const int kmax = std::max({dec::padded(P.H), dec::padded(P.nq * P.d),
-                             dec::padded(P.ncols)});
+  const int kmax = std::max({dec::padded(P.H, W.fmt), dec::padded(P.nq * P.d, W.fmt),
+                             dec::padded(P.ncols, W.fmt)});
   const int attn_f = dec::attn_lds_floats(P.d, P.nchunk);
-  const size_t lds = sizeof(float) * (std::max(kmax / 2, attn_f) + dec::MAX_SLOTS + dec::NW);
+  const size_t lds = sizeof(float) * (std::max(kmax / 2, attn_f) + dec::MAX_SLOTS + 16) +
+                     (W.fmt == dec::FMT_F16 ? 0 : sizeof(uint16_t) * dec::SC_LDS_HALFS);
   if (lds > di->max_lds)
     return fail(VT_ERR_UNSUPPORTED, "shape needs %zu bytes of LDS, device has %zu", lds, di->max_lds);
 
@@ -1077,7 +1368,7 @@ extern "C" vt_status vt_layer_decode(const vt_shard_spec* spec, const vt_layer_w
   if (staged) {
     for (int ph = pb; ph <= pe && e == hipSuccess; ++ph) {
       P.phase_begin = P.phase_end = ph;
-      hipLaunchKernelGGL(dec::decode_kernel_for(ph, ph), dim3(di->cus), dim3(dec::NT), lds, s, P);
+      hipLaunchKernelGGL(dec::decode_kernel_for(ph, ph, W.fmt), dim3(di->cus), dim3(dec::NT), lds, s, P);
       e = hipGetLastError();
     }
   } else {
@@ -1086,7 +1377,7 @@ extern "C" vt_status vt_layer_decode(const vt_shard_spec* spec, const vt_layer_w
     // launch is used (the cooperative launch API adds ~20 us per launch);
     // the barrier's bounded wait reports rather than hangs if another
     // kernel were to hold CUs.
-    const dec::DecodeKernel kern = dec::decode_kernel_for(pb, pe);
+    const dec::DecodeKernel kern = dec::decode_kernel_for(pb, pe, W.fmt);
     int per_cu = 0;
     e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, dec::NT, lds);
     if (e != hipSuccess) return fail(VT_ERR_HIP, "occupancy query: %s", hipGetErrorString(e));

@@ -62,3 +62,56 @@ def struct_of(t, dims, info, ld_d):
         ld_v=H, wo=p(t["wo"]), ld_o=max(8, info.n_q_heads * dims.head_dim),
         g_ffn=p(t["g_ffn"]), wg=p(t["wg"]), ld_g=H, wu=p(t["wu"]), ld_u=H, wd=p(t["wd"]),
         ld_d=ld_d)
+
+
+@dataclass
+class QShardWeightsDev:
+    tensors: dict
+    struct: vt.vt_layer_qweights
+    layout: dict = None   # name -> (code bytes of a row, row stride in bytes)
+    prec: int = 0
+
+
+def quantize_shard(sw: ShardWeightsDev, dims: vt.vt_layer_dims, info: vt.vt_shard_info, prec,
+                   stream=None) -> QShardWeightsDev:
+    """The shard's seven matrices in the library's INT8 / INT4 block format,
+    quantised on the device by vt_quantize_rows (allocation and the calls
+    only; the gains stay fp16). Each row holds its codes followed by its
+    block scales (one buffer per matrix, rows padded to 16 bytes), so a
+    row's scales share its codes' pages."""
+    H, d = dims.hidden, dims.head_dim
+    qd, kd, nc = info.n_q_heads * d, info.n_kv_heads * d, info.n_cols
+    shapes = {"wq": (qd, H), "wk": (kd, H), "wv": (kd, H), "wo": (H, qd), "wg": (nc, H),
+              "wu": (nc, H), "wd": (H, nc)}
+    per_block = 32 if prec == vt.VT_W_INT8 else 16
+    t = {"g_attn": sw.tensors["g_attn"], "g_ffn": sw.tensors["g_ffn"]}
+    layout = {}
+    for name, (rows, cols) in shapes.items():
+        src = sw.tensors[name]
+        nb = max(1, (cols + 31) // 32)
+        code_bytes = nb * per_block
+        ld = round_up(code_bytes + 2 * nb, 16)
+        buf = torch.zeros((rows, ld), dtype=torch.uint8, device=src.device)
+        if rows > 0 and cols > 0:
+            vt.vt_quantize_rows(src.data_ptr(), src.shape[1], rows, cols, prec, buf.data_ptr(), ld,
+                                buf.data_ptr() + code_bytes, ld // 2, stream)
+        t[name] = buf
+        layout[name] = (code_bytes, ld)
+    return QShardWeightsDev(t, _qstruct(t, layout, prec), layout, prec)
+
+
+def _qstruct(t, layout, prec):
+    p = lambda x: x.data_ptr() if x.numel() else None
+    mats = {}
+    for name, (code_bytes, ld) in layout.items():
+        b = t[name]
+        mats[name] = vt.vt_qmat(codes=p(b), ld_codes=ld,
+                                scales=(b.data_ptr() + code_bytes) if b.numel() else None,
+                                ld_scales=ld // 2)
+    return vt.vt_layer_qweights(prec=prec, g_attn=p(t["g_attn"]), g_ffn=p(t["g_ffn"]), **mats)
+
+
+def clone_qshard(q: QShardWeightsDev) -> QShardWeightsDev:
+    """A copy of the quantised shard in new device buffers (same layout)."""
+    t = {n: x.clone() for n, x in q.tensors.items()}
+    return QShardWeightsDev(t, _qstruct(t, q.layout, q.prec), q.layout, q.prec)

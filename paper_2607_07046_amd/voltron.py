@@ -26,12 +26,13 @@ VT_FFN = 2
 VT_STAGED = 0x100
 
 VT_PREC_FP16, VT_PREC_INT8, VT_PREC_INT4, VT_PREC_PRUNED = 0, 1, 2, 3
+VT_W_INT8, VT_W_INT4 = 1, 2
 
 # every symbol include/voltron.h declares
 EXPORTS = ("vt_shard_spec_create", "vt_shard_spec_query", "vt_shard_spec_destroy",
            "vt_kv_append", "vt_workspace_size", "vt_layer_decode", "vt_layer_prefill_chunk",
            "vt_qplan", "vt_partial_encode", "vt_partial_decode_add",
-           "vt_status_string", "vt_last_error")
+           "vt_status_string", "vt_last_error", "vt_quantize_rows", "vt_layer_decode_q")
 
 
 class VoltronError(RuntimeError):
@@ -64,6 +65,18 @@ class vt_layer_weights(ctypes.Structure):
                 ("wg", ctypes.c_void_p), ("ld_g", ctypes.c_int64),
                 ("wu", ctypes.c_void_p), ("ld_u", ctypes.c_int64),
                 ("wd", ctypes.c_void_p), ("ld_d", ctypes.c_int64)]
+
+
+class vt_qmat(ctypes.Structure):
+    _fields_ = [("codes", ctypes.c_void_p), ("ld_codes", ctypes.c_int64),
+                ("scales", ctypes.c_void_p), ("ld_scales", ctypes.c_int64)]
+
+
+class vt_layer_qweights(ctypes.Structure):
+    _fields_ = [("prec", ctypes.c_int32), ("g_attn", ctypes.c_void_p),
+                ("wq", vt_qmat), ("wk", vt_qmat), ("wv", vt_qmat), ("wo", vt_qmat),
+                ("g_ffn", ctypes.c_void_p),
+                ("wg", vt_qmat), ("wu", vt_qmat), ("wd", vt_qmat)]
 
 
 class vt_kv_view(ctypes.Structure):
@@ -112,9 +125,14 @@ def load_library(path=None):
     lib.vt_qplan.argtypes = [P, I32, I64, P, P, ctypes.POINTER(I64)]
     lib.vt_partial_encode.argtypes = [P, I32, P, P, P, SZ, P]
     lib.vt_partial_decode_add.argtypes = [P, SZ, I32, P, P, P, P, P]
+    lib.vt_quantize_rows.argtypes = [P, I64, I32, I32, I32, P, I64, P, I64, P]
+    lib.vt_layer_decode_q.argtypes = [P, ctypes.POINTER(vt_layer_qweights),
+                                      ctypes.POINTER(vt_kv_view), ctypes.POINTER(vt_layer_io),
+                                      I32, U32, P, SZ, P]
     for name in ("vt_shard_spec_create", "vt_shard_spec_query", "vt_kv_append",
                  "vt_workspace_size", "vt_layer_decode", "vt_layer_prefill_chunk",
-                 "vt_qplan", "vt_partial_encode", "vt_partial_decode_add"):
+                 "vt_qplan", "vt_partial_encode", "vt_partial_decode_add",
+                 "vt_quantize_rows", "vt_layer_decode_q"):
         getattr(lib, name).restype = ctypes.c_int
     lib.vt_status_string.argtypes = [ctypes.c_int]
     lib.vt_status_string.restype = ctypes.c_char_p
@@ -212,3 +230,15 @@ def vt_partial_encode(p, n, prec, offsets, msg, msg_bytes, stream=None):
 def vt_partial_decode_add(msg, msg_bytes, n, prec, offsets, base, out, stream=None):
     _check(load_library().vt_partial_decode_add(msg, msg_bytes, n, prec, offsets, base, out,
                                                 stream))
+
+
+def vt_quantize_rows(w, ld, rows, cols, prec, codes, ld_codes, scales, ld_scales, stream=None):
+    _check(load_library().vt_quantize_rows(w, ld, rows, cols, prec, codes, ld_codes, scales,
+                                           ld_scales, stream))
+
+
+def vt_layer_decode_q(spec: ShardSpec, w: vt_layer_qweights, kv, io: vt_layer_io, pos, phases,
+                      ws, ws_bytes, stream=None):
+    _check(load_library().vt_layer_decode_q(spec.handle, ctypes.byref(w),
+                                            ctypes.byref(kv) if kv is not None else None,
+                                            ctypes.byref(io), pos, phases, ws, ws_bytes, stream))

@@ -98,3 +98,14 @@ def tiny_workload(seed_id, hidden, n_heads, n_kv, head_dim, ffn, fracs, device, 
                                    head_dim=head_dim, ffn=ffn),
                     fracs=tuple(fracs), device=device, weight_sigma=sigma, ctx=ctx,
                     chunk=chunk)
+
+
+def oracle_qshard_weights(li: LayerInputs, r, level) -> oracle.ShardWeights:
+    """The shard's weights as its INT8 / INT4 blocks stand for them: each
+    sliced matrix quantised and dequantised by the oracle (fp64); the gains
+    stay fp16."""
+    from oracle import wquant
+    w = oracle_shard_weights(li, r)
+    q = lambda m: wquant.dequantized(m, level) if m.size else np.asarray(m, np.float64)
+    return oracle.ShardWeights(g_attn=w.g_attn, wq=q(w.wq), wk=q(w.wk), wv=q(w.wv), wo=q(w.wo),
+                               g_ffn=w.g_ffn, wg=q(w.wg), wu=q(w.wu), wd=q(w.wd))

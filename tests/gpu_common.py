@@ -31,7 +31,7 @@ class GpuShard:
     """Device ``device`` of workload ``wl``: packed weights, KV cache, workspace."""
 
     def __init__(self, wl, device=None, layer=0, li=None, capacity=None, fill_ctx=True,
-                 max_tokens=1, fracs=None):
+                 max_tokens=1, fracs=None, prec=None):
         self.wl = wl
         self.li = li or LayerInputs(wl, layer)
         fr = fracs or wl.fracs
@@ -39,6 +39,10 @@ class GpuShard:
                                             wl.device if device is None else device)
         self.dims, self.info = vt.vt_shard_spec_query(self.spec)
         self.w = pack.pack_shard(self.li, self.dims, self.info)
+        # prec (VT_W_INT8 / VT_W_INT4): decode through the block-quantised
+        # weights the library's quantiser makes from the fp16 shard
+        self.prec = prec
+        self.qw = pack.quantize_shard(self.w, self.dims, self.info, prec) if prec else None
         d, nkv = self.dims.head_dim, self.info.n_kv_heads
         self.cap = capacity or wl.capacity
         sent = torch.full((nkv, self.cap, d), SENTINEL, dtype=torch.int16, device="cuda")
@@ -79,8 +83,12 @@ class GpuShard:
         io = vt.vt_layer_io(x=ptr(xt), peer_attn=ptr(pa), peer_ffn=ptr(pf),
                             attn_partial=ptr(out["p_attn"]), h=ptr(out["h"]),
                             ffn_partial=ptr(out["p_ffn"]), y=ptr(out["y"]) if want_y else None)
-        vt.vt_layer_decode(self.spec, self.w.struct, self.kv, io, pos, phases, ptr(self.ws),
-                           self.ws_bytes, None)
+        if self.qw is not None:
+            vt.vt_layer_decode_q(self.spec, self.qw.struct, self.kv, io, pos, phases,
+                                 ptr(self.ws), self.ws_bytes, None)
+        else:
+            vt.vt_layer_decode(self.spec, self.w.struct, self.kv, io, pos, phases, ptr(self.ws),
+                               self.ws_bytes, None)
         torch.cuda.synchronize()
         return {k: v.float().cpu().numpy().astype(np.float64) for k, v in out.items()}
 

@@ -185,3 +185,73 @@ def test_kv_append_validation_errors(lib):
 def test_status_strings(lib):
     for s in range(-7, 1):
         assert vt.status_string(s) not in ("", "unknown status")
+
+
+def _fake_qmat(addr, ld_codes, ld_scales):
+    return vt.vt_qmat(codes=addr, ld_codes=ld_codes, scales=addr, ld_scales=ld_scales)
+
+
+def _fake_qweights(prec=vt.VT_W_INT8, addr=1 << 20):
+    # tiny 50% shard: 4 heads x 64 (256), 688 columns; INT8 rows of K columns
+    # need ceil(K / 32) * 32 code bytes, INT4 half that
+    def m(k):
+        nb = (k + 31) // 32
+        return _fake_qmat(addr, nb * (32 if prec == vt.VT_W_INT8 else 16), nb)
+    return vt.vt_layer_qweights(prec=prec, g_attn=addr, wq=m(512), wk=m(512), wv=m(512),
+                                wo=m(256), g_ffn=addr, wg=m(512), wu=m(512), wd=m(688))
+
+
+def test_decode_q_validation_errors(lib):
+    spec = _tiny_spec()
+    ws_need = vt.vt_workspace_size(spec, 1, 129)
+    A = 1 << 20
+    kv = vt.vt_kv_view(k=A, v=A, capacity=200, n_kv_heads=4, head_dim=64, len=128)
+
+    def call(w, pos=128):
+        with pytest.raises(vt.VoltronError) as e:
+            vt.vt_layer_decode_q(spec, w, kv, _fake_io(), pos, vt.VT_ATTN | vt.VT_FFN, A, ws_need)
+        return e.value.status
+
+    for prec in (vt.VT_W_INT8, vt.VT_W_INT4):
+        assert call(_fake_qweights(prec), pos=127) == vt.VT_ERR_POS
+        w = _fake_qweights(prec)
+        w.prec = 3
+        assert call(w) == vt.VT_ERR_ARG
+        w = _fake_qweights(prec)
+        w.wd.ld_codes -= 16                      # shorter than the row's blocks
+        assert call(w) == vt.VT_ERR_ARG
+        w = _fake_qweights(prec)
+        w.wo.ld_codes += 8                       # not a multiple of 16
+        assert call(w) == vt.VT_ERR_ARG
+        w = _fake_qweights(prec)
+        w.wg.ld_scales -= 1
+        assert call(w) == vt.VT_ERR_ARG
+        w = _fake_qweights(prec)
+        w.wq.codes = A + 8
+        assert call(w) == vt.VT_ERR_ALIGN
+        w = _fake_qweights(prec)
+        w.wu.scales = A + 1
+        assert call(w) == vt.VT_ERR_ALIGN
+        w = _fake_qweights(prec)
+        w.wk.scales = None
+        assert call(w) == vt.VT_ERR_ARG
+    assert kv.len == 128
+
+
+def test_quantize_rows_validation_errors(lib):
+    A = 1 << 20
+
+    def call(*args):
+        with pytest.raises(vt.VoltronError) as e:
+            vt.vt_quantize_rows(*args)
+        return e.value.status
+
+    assert call(A, 64, 4, 64, 3, A, 64, A, 2) == vt.VT_ERR_ARG           # precision
+    assert call(A, 64, 4, 0, 1, A, 64, A, 2) == vt.VT_ERR_ARG            # no columns
+    assert call(A, 60, 4, 64, 1, A, 64, A, 2) == vt.VT_ERR_ARG           # ld < cols
+    assert call(A, 64, 4, 64, 1, A, 48, A, 2) == vt.VT_ERR_ARG           # INT8 needs 64 code bytes
+    assert call(A, 64, 4, 64, 2, A, 24, A, 2) == vt.VT_ERR_ARG           # not a multiple of 16
+    assert call(A, 64, 4, 64, 2, A, 32, A, 1) == vt.VT_ERR_ARG           # 2 scale blocks
+    assert call(A + 8, 64, 4, 64, 1, A, 64, A, 2) == vt.VT_ERR_ALIGN
+    assert call(A, 64, 4, 64, 1, A, 64, A + 1, 2) == vt.VT_ERR_ALIGN
+    vt.vt_quantize_rows(A, 64, 0, 64, 1, A, 64, A, 2)                    # no rows: nothing enqueued
