@@ -303,8 +303,21 @@ __device__ __forceinline__ void gemv_impl(const Rows& rows, int units, int K, co
     const int q1 = __builtin_amdgcn_readfirstlane(static_cast<int>(static_cast<int64_t>(np) * (wave + 1) / NW));
     const int row0 = ua * U;
     for (int i = threadIdx.x; i < np; i += NT) slots[i] = 0.f;
-    // The round's scale rows go out first (row vr on wave vr % NW), so they
-    // return ahead of the weight pieces queued behind them.
+    u32x4 buf[PF];
+    // A few pieces go out before the barrier wait: they cover its latency
+    // without queueing so much traffic that the staging loads behind them
+    // stall. The rest of the ring follows once the input is staged.
+    // in groups of 4, only as far as the run goes (a load past it still
+    // costs the memory pipeline an instruction)
+#pragma unroll
+    for (int g = 0; g < PRE / 4; ++g) {
+      if (g == 0 || q0 + 4 * g < q1) {
+#pragma unroll
+        for (int i = 4 * g; i < 4 * g + 4; ++i) buf[i] = issue(row0, q0 + i, q1);
+      }
+    }
+    // The round's scale rows (row vr on wave vr % NW); they are written to
+    // LDS once the input is staged, when they have long landed.
     uint32_t sreg[QUANT ? SC_PER_WAVE : 1][SCW];
     if constexpr (QUANT) {
       const int nr = K > 0 ? (ub - ua) * U : 0;
@@ -324,12 +337,6 @@ __device__ __forceinline__ void gemv_impl(const Rows& rows, int units, int K, co
         }
       }
     }
-    u32x4 buf[PF];
-    // A few pieces go out before the barrier wait: they cover its latency
-    // without queueing so much traffic that the staging loads behind them
-    // stall. The rest of the ring follows once the input is staged.
-#pragma unroll
-    for (int i = 0; i < PRE; ++i) buf[i] = issue(row0, q0 + i, q1);
     if (!staged) {
       stage();  // all threads; ends with a workgroup barrier
       staged = true;
@@ -480,18 +487,19 @@ __device__ __forceinline__ void stage_rmsnorm_f(const float* v, const uint16_t* 
                                                 float eps, uint16_t* xs, float* red) {
   constexpr int MAXP = 16;  // float pairs held per thread
   const int npair = n / 2;
-  float a[MAXP], b[MAXP];
-  // Unconditional coherent buffer loads: pairs past n read zero without
-  // memory traffic (a guarded load would get a branch and a full wait each).
+  float a[MAXP] = {}, b[MAXP] = {};
+  uint32_t gw[MAXP] = {};  // the two fp16 gains of each pair (zero past n)
+  // Unconditional buffer loads (coherent for the values): pairs past n read
+  // zero without memory traffic (a guarded load would get a branch and a
+  // full wait each). Each pair's value and gain loads go out together; that
+  // order measured faster than all values first, then all gains.
   const rsrc_t rv = make_rsrc(v, static_cast<uint32_t>(npair) * 8u);
-#pragma unroll
-  for (int u = 0; u < MAXP; ++u)
-    buf_ld_shared2(rv, static_cast<uint32_t>(threadIdx.x + u * NT) * 8u, a[u], b[u]);
   const rsrc_t rg = make_rsrc(g, static_cast<uint32_t>(n) * 2u);
-  uint32_t gw[MAXP];  // the two fp16 gains of each pair (zero past n)
 #pragma unroll
-  for (int u = 0; u < MAXP; ++u)
+  for (int u = 0; u < MAXP; ++u) {
+    buf_ld_shared2(rv, static_cast<uint32_t>(threadIdx.x + u * NT) * 8u, a[u], b[u]);
     gw[u] = __builtin_amdgcn_raw_buffer_load_b32(rg, static_cast<uint32_t>(threadIdx.x + u * NT) * 4u, 0, 0);
+  }
   float ss = 0.f;
 #pragma unroll
   for (int u = 0; u < MAXP; ++u) {
@@ -523,7 +531,7 @@ __device__ __forceinline__ void stage_copy_f(const float* v, int n, int npad, ui
   const int npair = (n + 1) / 2;
   const rsrc_t rv = make_rsrc(v, static_cast<uint32_t>(npair) * 8u);
   for (int c0 = 0; c0 < npair; c0 += MAXP * NT) {
-    float a[MAXP], b[MAXP];
+    float a[MAXP] = {}, b[MAXP] = {};
 #pragma unroll
     for (int u = 0; u < MAXP; ++u)  // unconditional, zero past the end (see stage_rmsnorm_f)
       buf_ld_shared2(rv, static_cast<uint32_t>(c0 + threadIdx.x + u * NT) * 8u, a[u], b[u]);
@@ -598,15 +606,17 @@ __device__ __forceinline__ void phase_attn(const Params& P, float* lds, bool wai
     const int c = valid ? u - g * P.nchunk : 0;
     const int j = g * G + jj;                 // shard-local query head
     const int p0 = c * CL;
-    u32x4 kr[MAXPASS], vr[MAXPASS];
+    u32x4 kr[MAXPASS] = {}, vr[MAXPASS] = {};
 #pragma unroll
     for (int ps = 0; ps < MAXPASS; ++ps) {
-      const int p = p0 + ps * PPP + pl;
-      const bool ok = valid && ps < NPASS && p < P.pos;
-      const uint32_t off =
-          ok ? static_cast<uint32_t>(((static_cast<int64_t>(g) * P.cap + p) * d + dc) * 2) : kOOB;
-      kr[ps] = buf_load16(rk, off);
-      vr[ps] = buf_load16(rv, off);
+      if (ps == 0 || ps < NPASS) {  // passes of the chunk only (uniform)
+        const int p = p0 + ps * PPP + pl;
+        const bool ok = valid && p < P.pos;
+        const uint32_t off =
+            ok ? static_cast<uint32_t>(((static_cast<int64_t>(g) * P.cap + p) * d + dc) * 2) : kOOB;
+        kr[ps] = buf_load16(rk, off);
+        vr[ps] = buf_load16(rv, off);
+      }
     }
     // rotation of pair t at the new position (independent of phase 0)
     const int half = d / 2;
