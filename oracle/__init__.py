@@ -24,6 +24,8 @@ What it follows (paper: Voltron, arXiv 2607.07046):
   * Sec. 2.2, 4.2.2, 4.3.1 (mixed precision, precision scaling):
     ``wquant`` quantises a shard's weight rows to INT8 / INT4 blocks and
     gives the values the quantised shard stands for.
+  * Sec. 4.3.1 (Pruning): ``prune`` gives the layer that the kept shards of
+    a pruned partition add up to.
 
 The paper does not define the decoder's internals (normalisation, rotary
 embedding, FFN form); the readings used here are the Llama layer:
