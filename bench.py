@@ -15,7 +15,8 @@ figure is algorithmic bytes per step / time per step, and ``roofline``
 reports the decode kernel against the 8 TB/s HBM peak. The ``prefill``
 section times the 256-token prefill chunk (MFMA utilisation) and the
 ``comm`` section the partial-sum transmission kernels, the ``quant`` section
-the same decode over INT8 and INT4 block-quantised weights. ``cpu_baseline`` is
+the same decode over INT8 and INT4 block-quantised weights, the ``repack``
+section the shard re-pack of an elastic re-partition. ``cpu_baseline`` is
 the fp64 oracle timed on the host cores on a bounded sample of the same
 workload (a reference, not the target).
 """
@@ -94,6 +95,8 @@ def parse():
                     help="timed calls of each partial-sum transmission kernel (0: skip)")
     ap.add_argument("--quant-steps", type=int, default=1000,
                     help="timed decode steps over INT8 and INT4 weight shards (0: skip)")
+    ap.add_argument("--repack-reps", type=int, default=20,
+                    help="timed shard packs of the re-partition section (0: skip)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="instead of the bench: copy MIB MiB device-to-device 10 times "
                          "(the known-size kernel that scales the HBM byte counters)")
@@ -282,12 +285,81 @@ def main():
                                          args.eager)
     if args.comm_steps > 0:
         out["comm"] = comm_section(args.comm_steps)
+    if args.repack_reps > 0:
+        out["repack"] = repack_section(spec, dims, info, wl, args.repack_reps, enqueue, copies)
     if args.quant_steps > 0:
         out["quant"] = quant_section(spec, dims, info, wl, args.quant_steps,
                                      max(1, args.quant_steps // 10), layers[0][0], args.eager)
     if args.cpu_seconds > 0:
         out["cpu_baseline"] = cpu_baseline(wl, pos, args.cpu_seconds, step_bytes)
     print(json.dumps(out), flush=True)
+
+
+def repack_section(spec, dims, info, wl, reps, enqueue, copies):
+    """Elastic re-partition: vt_shard_pack of the headline shard out of the
+    whole layer's device weights (its bytes read and written), alone and
+    while decode steps run on the default stream; the decode step time with
+    and without a pack running beside it on a second stream (both at the
+    default priority)."""
+    import torch
+
+    from paper_2607_07046_amd import pack
+    from paper_2607_07046_amd import voltron as vt
+    from synth.gen import LayerInputs
+
+    full = pack.upload_full(LayerInputs(wl), dims)
+    out = pack.alloc_shard(dims, info)
+    shard_bytes = sum(t.numel() * 2 for t in out.tensors.values())
+    side = torch.cuda.Stream()
+    main = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+
+    def packs(n):
+        for _ in range(n):
+            vt.vt_shard_pack(spec, full.struct, out.struct, side.cuda_stream)
+
+    def decodes(n):
+        for i in range(n):
+            enqueue(i, main.cuda_stream)
+
+    packs(2)
+    decodes(2 * copies)
+    torch.cuda.synchronize()
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    # pack alone
+    a, b = ev(), ev()
+    a.record(side)
+    packs(reps)
+    b.record(side)
+    torch.cuda.synchronize()
+    pack_us = a.elapsed_time(b) * 1e3 / reps
+    # decode alone, eager launches (as in the concurrent case)
+    nd = max(copies * 4, 40)
+    a, b = ev(), ev()
+    a.record(main)
+    decodes(nd)
+    b.record(main)
+    torch.cuda.synchronize()
+    dec_us = a.elapsed_time(b) * 1e3 / nd
+    # both: the packs on the second stream, decodes on the default one
+    a, b, c, e = ev(), ev(), ev(), ev()
+    a.record(side)
+    c.record(main)
+    packs(reps)
+    decodes(nd)
+    b.record(side)
+    e.record(main)
+    torch.cuda.synchronize()
+    pack_cc = a.elapsed_time(b) * 1e3 / reps
+    dec_cc = c.elapsed_time(e) * 1e3 / nd
+    moved = 2 * shard_bytes
+    return {"shard_bytes": shard_bytes, "pack_us": round(pack_us, 2),
+            "pack_GBps": round(moved / (pack_us * 1e-6) / 1e9, 1),
+            "pack_hbm_frac": round(moved / (pack_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+            "decode_us_alone": round(dec_us, 2), "decode_us_with_pack": round(dec_cc, 2),
+            "pack_us_with_decode": round(pack_cc, 2), "packs": reps, "decode_steps": nd,
+            "note": "eager launches; bytes = the shard's weights read from the whole layer and "
+                    "written to its own buffers"}
 
 
 def quant_bytes(dims, info, pos, prec):

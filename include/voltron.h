@@ -270,6 +270,34 @@ vt_status vt_layer_decode_q(const vt_shard_spec* spec, const vt_layer_qweights* 
                             vt_kv_view* kv, const vt_layer_io* io, int32_t pos,
                             uint32_t phases, void* ws, size_t ws_bytes, void* stream);
 
+/* ---- Elastic re-partition and shard-wise pruning (paper Sec. 4.3.1) ----
+ * When devices come and go or run short of memory, the partition changes:
+ * shards move between devices or are pruned (dropped whole, the kept
+ * shards' partial sums then add up to the layer without the dropped heads
+ * and columns). Shards are allocated separately, so a device packs its new
+ * shard into new buffers on a second stream while it keeps decoding with
+ * the old ones, and takes over the KV heads of the groups it now owns. A
+ * pruned shard is simply not run; nothing here is needed for it. */
+
+/* Gather ``spec``'s shard out of the whole layer's weights ``full`` (device,
+ * canonical out x in: wq [n_heads*head_dim][hidden], wk and wv
+ * [n_kv_heads*head_dim][hidden], wo [hidden][n_heads*head_dim], wg and wu
+ * [ffn][hidden], wd [hidden][ffn], gains [hidden]; every ld a multiple of 8)
+ * into the shard's buffers ``out`` (device, shaped as vt_layer_decode takes
+ * them; out->ld_d >= n_cols rounded up to 8: the columns from n_cols to
+ * that multiple of 8 are written as zero). Bit-exact copies enqueued on
+ * ``stream``; both structs are read on the host only. */
+vt_status vt_shard_pack(const vt_shard_spec* spec, const vt_layer_weights* full,
+                        const vt_layer_weights* out, void* stream);
+
+/* Copy positions 0..n_pos-1 of KV heads [src_head0, src_head0 + n_heads) of
+ * ``src`` into heads [dst_head0, ...) of ``dst`` (keys and values; caches of
+ * equal head_dim, any capacities >= n_pos), on ``stream``. Other slots and
+ * dst->len are left as they are (the caller sets len once every head is
+ * in place). */
+vt_status vt_kv_copy_heads(const vt_kv_view* src, int32_t src_head0, const vt_kv_view* dst,
+                           int32_t dst_head0, int32_t n_heads, int32_t n_pos, void* stream);
+
 /* ---- Communication scaling of the partial sums (paper Sec. 4.3.2) ----
  * To cut the bytes a device sends for the aggregation, its partial sums go
  * out in blocks of 32 activations, each at one precision; precisions are

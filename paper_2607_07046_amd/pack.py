@@ -115,3 +115,31 @@ def clone_qshard(q: QShardWeightsDev) -> QShardWeightsDev:
     """A copy of the quantised shard in new device buffers (same layout)."""
     t = {n: x.clone() for n, x in q.tensors.items()}
     return QShardWeightsDev(t, _qstruct(t, q.layout, q.prec), q.layout, q.prec)
+
+
+def upload_full(src, dims: vt.vt_layer_dims, device="cuda") -> ShardWeightsDev:
+    """The whole layer's weights on the device (canonical out x in, each
+    matrix contiguous): the source vt_shard_pack gathers shards from."""
+    t = {"g_attn": _dev(src.g_attn(), device), "g_ffn": _dev(src.g_ffn(), device)}
+    for name in ("wq", "wk", "wv", "wo", "wg", "wu", "wd"):
+        t[name] = _dev(src.full(name), device)
+    p = lambda x: x.data_ptr() if x.numel() else None
+    st = vt.vt_layer_weights(g_attn=p(t["g_attn"]), wq=p(t["wq"]), ld_q=t["wq"].shape[1],
+                             wk=p(t["wk"]), ld_k=t["wk"].shape[1], wv=p(t["wv"]),
+                             ld_v=t["wv"].shape[1], wo=p(t["wo"]), ld_o=t["wo"].shape[1],
+                             g_ffn=p(t["g_ffn"]), wg=p(t["wg"]), ld_g=t["wg"].shape[1],
+                             wu=p(t["wu"]), ld_u=t["wu"].shape[1], wd=p(t["wd"]),
+                             ld_d=t["wd"].shape[1])
+    return ShardWeightsDev(t, st)
+
+
+def alloc_shard(dims: vt.vt_layer_dims, info: vt.vt_shard_info, device="cuda") -> ShardWeightsDev:
+    """Separately allocated (uninitialised) buffers for one shard, laid out
+    as pack_shard lays them out: the target of vt_shard_pack."""
+    H, d = dims.hidden, dims.head_dim
+    qd, kd, nc = info.n_q_heads * d, info.n_kv_heads * d, info.n_cols
+    ld_d = max(8, round_up(nc, 8))
+    e = lambda *shape: torch.empty(shape, dtype=torch.float16, device=device)
+    t = {"g_attn": e(H), "g_ffn": e(H), "wq": e(qd, H), "wk": e(kd, H), "wv": e(kd, H),
+         "wo": e(H, qd), "wg": e(nc, H), "wu": e(nc, H), "wd": e(H, ld_d)}
+    return ShardWeightsDev(t, struct_of(t, dims, info, ld_d))

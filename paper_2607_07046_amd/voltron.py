@@ -32,7 +32,8 @@ VT_W_INT8, VT_W_INT4 = 1, 2
 EXPORTS = ("vt_shard_spec_create", "vt_shard_spec_query", "vt_shard_spec_destroy",
            "vt_kv_append", "vt_workspace_size", "vt_layer_decode", "vt_layer_prefill_chunk",
            "vt_qplan", "vt_partial_encode", "vt_partial_decode_add",
-           "vt_status_string", "vt_last_error", "vt_quantize_rows", "vt_layer_decode_q")
+           "vt_status_string", "vt_last_error", "vt_quantize_rows", "vt_layer_decode_q",
+           "vt_shard_pack", "vt_kv_copy_heads")
 
 
 class VoltronError(RuntimeError):
@@ -129,10 +130,14 @@ def load_library(path=None):
     lib.vt_layer_decode_q.argtypes = [P, ctypes.POINTER(vt_layer_qweights),
                                       ctypes.POINTER(vt_kv_view), ctypes.POINTER(vt_layer_io),
                                       I32, U32, P, SZ, P]
+    lib.vt_shard_pack.argtypes = [P, ctypes.POINTER(vt_layer_weights),
+                                  ctypes.POINTER(vt_layer_weights), P]
+    lib.vt_kv_copy_heads.argtypes = [ctypes.POINTER(vt_kv_view), I32, ctypes.POINTER(vt_kv_view),
+                                     I32, I32, I32, P]
     for name in ("vt_shard_spec_create", "vt_shard_spec_query", "vt_kv_append",
                  "vt_workspace_size", "vt_layer_decode", "vt_layer_prefill_chunk",
                  "vt_qplan", "vt_partial_encode", "vt_partial_decode_add",
-                 "vt_quantize_rows", "vt_layer_decode_q"):
+                 "vt_quantize_rows", "vt_layer_decode_q", "vt_shard_pack", "vt_kv_copy_heads"):
         getattr(lib, name).restype = ctypes.c_int
     lib.vt_status_string.argtypes = [ctypes.c_int]
     lib.vt_status_string.restype = ctypes.c_char_p
@@ -242,3 +247,13 @@ def vt_layer_decode_q(spec: ShardSpec, w: vt_layer_qweights, kv, io: vt_layer_io
     _check(load_library().vt_layer_decode_q(spec.handle, ctypes.byref(w),
                                             ctypes.byref(kv) if kv is not None else None,
                                             ctypes.byref(io), pos, phases, ws, ws_bytes, stream))
+
+
+def vt_shard_pack(spec: ShardSpec, full: vt_layer_weights, out: vt_layer_weights, stream=None):
+    _check(load_library().vt_shard_pack(spec.handle, ctypes.byref(full), ctypes.byref(out), stream))
+
+
+def vt_kv_copy_heads(src: vt_kv_view, src_head0, dst: vt_kv_view, dst_head0, n_heads, n_pos,
+                     stream=None):
+    _check(load_library().vt_kv_copy_heads(ctypes.byref(src), src_head0, ctypes.byref(dst),
+                                           dst_head0, n_heads, n_pos, stream))

@@ -255,3 +255,45 @@ def test_quantize_rows_validation_errors(lib):
     assert call(A + 8, 64, 4, 64, 1, A, 64, A, 2) == vt.VT_ERR_ALIGN
     assert call(A, 64, 4, 64, 1, A, 64, A + 1, 2) == vt.VT_ERR_ALIGN
     vt.vt_quantize_rows(A, 64, 0, 64, 1, A, 64, A, 2)                    # no rows: nothing enqueued
+
+
+def test_shard_pack_validation_errors(lib):
+    spec = _tiny_spec()                       # 512 hidden, 8 x 64 heads, 1376 FFN, device 0 of 2
+    A = 1 << 20
+
+    def full(**over):
+        f = vt.vt_layer_weights(g_attn=A, wq=A, ld_q=512, wk=A, ld_k=512, wv=A, ld_v=512, wo=A,
+                                ld_o=512, g_ffn=A, wg=A, ld_g=512, wu=A, ld_u=512, wd=A,
+                                ld_d=1376)
+        for k, v in over.items():
+            setattr(f, k, v)
+        return f
+
+    def call(f, o):
+        with pytest.raises(vt.VoltronError) as e:
+            vt.vt_shard_pack(spec, f, o)
+        return e.value.status
+
+    assert call(full(wq=None), _fake_weights()) == vt.VT_ERR_ARG
+    assert call(full(wo=A + 4), _fake_weights()) == vt.VT_ERR_ALIGN
+    assert call(full(ld_o=256), _fake_weights()) == vt.VT_ERR_ARG       # full Wo rows are 512 long
+    o = _fake_weights()
+    o.ld_d = 680                                                         # the shard's 688 columns
+    assert call(full(), o) == vt.VT_ERR_ARG
+    o = _fake_weights()
+    o.wg = A + 2
+    assert call(full(), o) == vt.VT_ERR_ALIGN
+
+
+def test_kv_copy_heads_validation_errors(lib):
+    A = 1 << 20
+    a = vt.vt_kv_view(k=A, v=A, capacity=10, n_kv_heads=2, head_dim=64, len=4)
+    b = vt.vt_kv_view(k=A, v=A, capacity=10, n_kv_heads=2, head_dim=128, len=0)
+    for args, status in (((a, 0, b, 0, 1, 4), vt.VT_ERR_ARG),          # head_dim differs
+                         ((a, 1, a, 0, 2, 4), vt.VT_ERR_ARG),          # past the source heads
+                         ((a, 0, a, 0, 1, 11), vt.VT_ERR_ARG),         # past the capacity
+                         ((a, 0, a, 0, -1, 4), vt.VT_ERR_ARG)):
+        with pytest.raises(vt.VoltronError) as e:
+            vt.vt_kv_copy_heads(*args)
+        assert e.value.status == status
+    vt.vt_kv_copy_heads(a, 0, a, 1, 1, 0)                                # nothing to copy
