@@ -18,8 +18,10 @@ def _mat(a):
 
 
 def brute_layer(w, n_q, n_kv, d, eps, base, X, k_cache, v_cache, pos0,
-                peer_attn=None, peer_ffn=None):
+                peer_attn=None, peer_ffn=None, window=0):
     """Full layer over T tokens; inputs are nested sequences or arrays.
+    ``window`` > 0: token at position p attends to positions p - window + 1
+    .. p only (sliding window).
 
     Returns dict of python lists: p_attn, h, p_ffn, y ([T][H]).
     """
@@ -79,8 +81,10 @@ def brute_layer(w, n_q, n_kv, d, eps, base, X, k_cache, v_cache, pos0,
         cat = []
         for j in range(n_q):
             g = j // group
+            first = max(0, p - window + 1) if window > 0 else 0
+            span = list(range(first, p + 1))
             scores = []
-            for pp in range(p + 1):
+            for pp in span:
                 acc = 0.0
                 for i in range(d):
                     acc += per_tok[t][j][i] * keys[g][pp][i]
@@ -89,8 +93,8 @@ def brute_layer(w, n_q, n_kv, d, eps, base, X, k_cache, v_cache, pos0,
             ex = [math.exp(s - mx) for s in scores]
             tot = sum(ex)
             o = [0.0] * d
-            for pp in range(p + 1):
-                wgt = ex[pp] / tot
+            for n, pp in enumerate(span):
+                wgt = ex[n] / tot
                 for i in range(d):
                     o[i] += wgt * vals[g][pp][i]
             cat.extend(o)

@@ -111,12 +111,14 @@ def append_kv(k_cache, v_cache, k_new, v_new, pos):
 
 
 def attn_sublayer(w: ShardWeights, n_q: int, n_kv: int, d: int, eps: float, base: float,
-                  X, k_cache, v_cache, pos0: int, peer=None):
+                  X, k_cache, v_cache, pos0: int, peer=None, window: int = 0):
     """ATTN sub-layer of a shard for T tokens at positions pos0..pos0+T-1.
 
     X: [T, H] input rows; k_cache/v_cache: [n_kv, >=pos0, d] the shard's
     cached (already rotated) keys and values. Token t attends to positions
-    0..pos0+t. Returns p_attn [T, H], h [T, H], k_new, v_new [T, n_kv, d].
+    0..pos0+t, or with ``window`` > 0 (sliding-window attention, the local
+    layers of Table 3's gemma models) to the last ``window`` of them.
+    Returns p_attn [T, H], h [T, H], k_new, v_new [T, n_kv, d].
     """
     X = _f64(X)
     T, H = X.shape
@@ -132,9 +134,10 @@ def attn_sublayer(w: ShardWeights, n_q: int, n_kv: int, d: int, eps: float, base
     O = np.zeros((T, n_q, d))
     for t in range(T):
         L = pos0 + t + 1
+        lo = max(0, L - window) if window > 0 else 0
         for j in range(n_q):
             g = j // G
-            O[t, j] = attention(Q[t, j], Kall[g, :L], Vall[g, :L])
+            O[t, j] = attention(Q[t, j], Kall[g, lo:L], Vall[g, lo:L])
     p_attn = O.reshape(T, n_q * d) @ _f64(w.wo).T
     h = X + p_attn + (0.0 if peer is None else _f64(peer))
     return p_attn, h, K, V
@@ -151,7 +154,7 @@ def ffn_sublayer(w: ShardWeights, eps: float, Hin, peer=None):
 
 
 def decode(w: ShardWeights, n_q, n_kv, d, eps, base, x, k_cache, v_cache, pos,
-           peer_attn=None, peer_ffn=None) -> dict:
+           peer_attn=None, peer_ffn=None, window=0) -> dict:
     """One batch-1 decode step of a shard at position ``pos``.
 
     x: [H]. Returns p_attn, h, p_ffn, y ([H] each) and the appended
@@ -159,15 +162,15 @@ def decode(w: ShardWeights, n_q, n_kv, d, eps, base, x, k_cache, v_cache, pos,
     """
     p_attn, h, K, V = attn_sublayer(w, n_q, n_kv, d, eps, base, _f64(x)[None], k_cache,
                                     v_cache, pos, None if peer_attn is None else
-                                    _f64(peer_attn)[None])
+                                    _f64(peer_attn)[None], window)
     p_ffn, y = ffn_sublayer(w, eps, h, None if peer_ffn is None else _f64(peer_ffn)[None])
     return dict(p_attn=p_attn[0], h=h[0], p_ffn=p_ffn[0], y=y[0], k_new=K[0], v_new=V[0])
 
 
 def prefill(w: ShardWeights, n_q, n_kv, d, eps, base, X, k_cache, v_cache, pos0,
-            peer_attn=None, peer_ffn=None) -> dict:
+            peer_attn=None, peer_ffn=None, window=0) -> dict:
     """A prefill chunk of T tokens of a shard at positions pos0..pos0+T-1."""
     p_attn, h, K, V = attn_sublayer(w, n_q, n_kv, d, eps, base, X, k_cache, v_cache, pos0,
-                                    peer_attn)
+                                    peer_attn, window)
     p_ffn, y = ffn_sublayer(w, eps, h, peer_ffn)
     return dict(p_attn=p_attn, h=h, p_ffn=p_ffn, y=y, k_new=K, v_new=V)
