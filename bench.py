@@ -40,12 +40,14 @@ MALL_DEFEAT_BYTES = 768 * 2 ** 20
 
 def algorithmic_bytes(dims, info, pos):
     """Bytes the decode step must move: every shard weight once, the cached
-    K/V of positions 0..pos-1 read plus the new K/V written, the gains, x in,
-    and the four fp16 output vectors."""
+    K/V of the attended positions (0..pos-1, or a sliding window's) read
+    plus the new K/V written, the gains, x in, and the four fp16 output
+    vectors."""
     H, d = dims.hidden, dims.head_dim
     nq, nkv, F = info.n_q_heads, info.n_kv_heads, info.n_cols
     weights = 2 * ((nq + 2 * nkv) * d * H + H * nq * d + 3 * F * H)
-    kv = 4 * nkv * d * (pos + 1)
+    span = min(pos + 1, dims.window) if dims.window > 0 else pos + 1  # positions attended
+    kv = 4 * nkv * d * span
     vectors = 2 * H * (2 + 1 + 4)  # gains, x, attn_partial/h/ffn_partial/y
     return weights + kv + vectors
 
@@ -141,7 +143,7 @@ def main():
     dims = vt.vt_layer_dims(hidden=wl.dims.hidden, n_heads=wl.dims.n_heads,
                             n_kv_heads=wl.dims.n_kv_heads, head_dim=wl.dims.head_dim,
                             ffn=wl.dims.ffn, rms_eps=wl.dims.rms_eps,
-                            rope_base=wl.dims.rope_base)
+                            rope_base=wl.dims.rope_base, window=wl.dims.window)
     spec = vt.vt_shard_spec_create(dims, wl.fracs, wl.fracs, wl.device)
     dims, info = vt.vt_shard_spec_query(spec)
     pos = wl.ctx
@@ -371,7 +373,8 @@ def quant_bytes(dims, info, pos, prec):
     per_block = (32 if prec == 1 else 16) + 2
     nb = lambda k: (k + 31) // 32
     weights = per_block * (qd * nb(H) + 2 * kd * nb(H) + H * nb(qd) + 2 * F * nb(H) + H * nb(F))
-    return weights + 4 * kd * (pos + 1) + 2 * H * (2 + 1 + 4)
+    span = min(pos + 1, dims.window) if dims.window > 0 else pos + 1
+    return weights + 4 * kd * span + 2 * H * (2 + 1 + 4)
 
 
 def quant_section(spec, dims, info, wl, steps, warmup, fp16_weights, eager=False):
@@ -555,7 +558,7 @@ def prefill_section(steps, warmup, eager=False):
     dims = vt.vt_layer_dims(hidden=wl.dims.hidden, n_heads=wl.dims.n_heads,
                             n_kv_heads=wl.dims.n_kv_heads, head_dim=wl.dims.head_dim,
                             ffn=wl.dims.ffn, rms_eps=wl.dims.rms_eps,
-                            rope_base=wl.dims.rope_base)
+                            rope_base=wl.dims.rope_base, window=wl.dims.window)
     spec = vt.vt_shard_spec_create(dims, wl.fracs, wl.fracs, wl.device)
     dims, info = vt.vt_shard_spec_query(spec)
     T, pos0 = wl.chunk, wl.ctx
@@ -669,7 +672,7 @@ def cpu_baseline(wl, pos, budget_s, step_bytes):
     t0 = time.perf_counter()
     while True:
         oracle.decode(w, r.n_q_heads, r.n_kv_heads, dd, d.rms_eps, d.rope_base, li.x(n), kc, vc,
-                      pos)
+                      pos, window=d.window)
         n += 1
         el = time.perf_counter() - t0
         if el >= budget_s:

@@ -58,7 +58,10 @@ typedef enum vt_status {
 } vt_status;
 
 /* Shape of the whole (unsharded) layer. head_dim must be 64 or 128;
- * hidden a multiple of 8; n_heads a multiple of n_kv_heads. */
+ * hidden a multiple of 8; n_heads a multiple of n_kv_heads. ``window`` > 0
+ * makes the layer's attention a sliding window (a token at position p
+ * attends to positions p - window + 1 .. p only, the local layers of the
+ * gemma models of the paper's Table 3); 0 is full causal attention. */
 typedef struct vt_layer_dims {
   int32_t hidden;
   int32_t n_heads;
@@ -67,6 +70,7 @@ typedef struct vt_layer_dims {
   int32_t ffn;
   float rms_eps;
   float rope_base;
+  int32_t window;
 } vt_layer_dims;
 
 /* One device's shard: query heads [q_head_begin, +n_q_heads), KV heads
@@ -200,7 +204,8 @@ vt_status vt_layer_decode(const vt_shard_spec* spec, const vt_layer_weights* w,
 /* Prefill of a chunk of n_tok tokens at positions pos0..pos0+n_tok-1 (paper
  * Sec. 2.1: prompt tokens are processed in parallel). All n_tok keys and
  * values are appended (pos0 must equal kv->len); token t attends to
- * positions 0..pos0+t. Activations in io are [n_tok][hidden]. The
+ * positions 0..pos0+t (the last dims.window of them in a sliding-window
+ * layer). Activations in io are [n_tok][hidden]. The
  * projections run as fp16 matrix-core (MFMA) GEMMs with fp32 accumulation;
  * their activation operands are rounded to fp16 first. */
 vt_status vt_layer_prefill_chunk(const vt_shard_spec* spec, const vt_layer_weights* w,

@@ -49,6 +49,7 @@ enum { SW_BAR = 0, SW_EXIT = 1024, SW_ERR = 2048, SW_GROUP = 3072, SW_GROUP_STRI
 
 struct Params {
   int H, d, nq, nkv, G, ncols, pos, cap, nchunk, cl;
+  int p_first;  // first position attended (a sliding window's start, else 0)
   float eps, rope_base;
   const uint16_t *g_attn, *g_ffn;
   // Weight matrices: fp16 values, or block codes (FMT_Q8 / FMT_Q4) with
@@ -605,7 +606,7 @@ __device__ __forceinline__ void phase_attn(const Params& P, float* lds, bool wai
     const int g = valid ? u / P.nchunk : 0;
     const int c = valid ? u - g * P.nchunk : 0;
     const int j = g * G + jj;                 // shard-local query head
-    const int p0 = c * CL;
+    const int p0 = P.p_first + c * CL;
     u32x4 kr[MAXPASS] = {}, vr[MAXPASS] = {};
 #pragma unroll
     for (int ps = 0; ps < MAXPASS; ++ps) {
@@ -1310,6 +1311,8 @@ static vt_status decode_impl(const vt_shard_spec* spec, const WeightView& W, vt_
     if ((st = check_io_vec(io->y, "y", false)) != VT_OK) return st;
   }
   const int ctx = attn ? pos + 1 : 1;
+  // a sliding window attends to the last D.window positions only
+  const int p_first = (attn && D.window > 0) ? std::max(0, pos + 1 - D.window) : 0;
   const DecodeWs L = decode_ws_layout(*spec, ctx);
   if (!ws || ws_bytes < L.total)
     return fail(VT_ERR_WORKSPACE, "workspace %zu bytes, need %zu", ws_bytes, L.total);
@@ -1326,8 +1329,9 @@ static vt_status decode_impl(const vt_shard_spec* spec, const WeightView& W, vt_
   P.G = D.n_heads / D.n_kv_heads;
   P.ncols = in.n_cols;
   P.pos = pos;
+  P.p_first = p_first;
   P.cap = kv ? kv->capacity : 0;
-  attn_chunking(D.head_dim, in.n_q_heads, ctx, di->cus, &P.cl, &P.nchunk);
+  attn_chunking(D.head_dim, in.n_q_heads, ctx - p_first, di->cus, &P.cl, &P.nchunk);
   P.eps = D.rms_eps;
   P.rope_base = D.rope_base;
   P.g_attn = static_cast<const uint16_t*>(W.g_attn);

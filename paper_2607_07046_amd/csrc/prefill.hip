@@ -457,7 +457,8 @@ struct AttnLds {
 template <int D>
 __global__ void __launch_bounds__(AW * kWave) attn_prefill_kernel(const uint16_t* Q, uint16_t* O,
                                                                   const uint16_t* kc, const uint16_t* vc,
-                                                                  int T, int nq, int G, int cap, int pos0) {
+                                                                  int T, int nq, int G, int cap, int pos0,
+                                                                  int window) {
   using LY = AttnLds<D>;
   constexpr int KLD = LY::KLD, OLD = LY::OLD;
   __shared__ __attribute__((aligned(16))) uint16_t smem[AW * LY::WAVE_HALVES];
@@ -492,6 +493,8 @@ __global__ void __launch_bounds__(AW * kWave) attn_prefill_kernel(const uint16_t
 
   const int last_key = pos0 + min(t0 + QB, T) - 1;  // largest position any query sees
   const int nkb = last_key / KB + 1;
+  // a sliding window: the block's first query sees nothing before this key
+  const int kb0 = window > 0 ? max(0, pos0 + t0 - window + 1) / KB : 0;
   const uint16_t* kbase = kc + static_cast<int64_t>(g) * cap * D;
   const uint16_t* vbase = vc + static_cast<int64_t>(g) * cap * D;
   constexpr int CH = KB * D / 8;     // 16-byte chunks per K (or V) tile
@@ -510,8 +513,8 @@ __global__ void __launch_bounds__(AW * kWave) attn_prefill_kernel(const uint16_t
       vreg[u] = load16(vbase + static_cast<int64_t>(p) * D + col);
     }
   };
-  fetch(min(wave, nkb - 1));
-  for (int kb = wave; kb < nkb; kb += AW) {
+  fetch(min(kb0 + wave, nkb - 1));
+  for (int kb = kb0 + wave; kb < nkb; kb += AW) {
     const int p0 = kb * KB;
     // stage K (rows permuted) and V (row-major), then start the next block
 #pragma unroll
@@ -542,7 +545,7 @@ __global__ void __launch_bounds__(AW * kWave) attn_prefill_kernel(const uint16_t
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const int key = swap_bits23(8 * (i / 4) + 4 * (lane / 32) + i % 4);
-      if (p0 + key > qpos || tq >= T) s[i] = -INFINITY;
+      if (p0 + key > qpos || tq >= T || (window > 0 && p0 + key <= qpos - window)) s[i] = -INFINITY;
       bm = fmaxf(bm, s[i]);
     }
     bm = fmaxf(bm, __shfl_xor(bm, 32, kWave));
@@ -868,11 +871,11 @@ extern "C" vt_status vt_layer_prefill_chunk(const vt_shard_spec* spec, const vt_
     if (d == 128)
       hipLaunchKernelGGL(pf::attn_prefill_kernel<128>, dim3(blocks), dim3(pf::AW * kWave), 0, s, Qr, Ob,
                          static_cast<const uint16_t*>(kv->k), static_cast<const uint16_t*>(kv->v),
-                         n_tok, nq, G, kv->capacity, pos0);
+                         n_tok, nq, G, kv->capacity, pos0, D.window);
     else
       hipLaunchKernelGGL(pf::attn_prefill_kernel<64>, dim3(blocks), dim3(pf::AW * kWave), 0, s, Qr, Ob,
                          static_cast<const uint16_t*>(kv->k), static_cast<const uint16_t*>(kv->v),
-                         n_tok, nq, G, kv->capacity, pos0);
+                         n_tok, nq, G, kv->capacity, pos0, D.window);
     if ((st = check("attention")) != VT_OK) return st;
     pf::GemmArgs o{};
     o.A = Ob;

@@ -46,6 +46,7 @@ vt_status check_layer_dims(const vt_layer_dims& d) {
     return fail(VT_ERR_ARG, "rms_eps must be finite and >= 0");
   if (!(d.rope_base > 0.0f) || !std::isfinite(d.rope_base))
     return fail(VT_ERR_ARG, "rope_base must be finite and > 0");
+  if (d.window < 0) return fail(VT_ERR_ARG, "window %d < 0", d.window);
   return VT_OK;
 }
 

@@ -47,7 +47,7 @@ class vt_layer_dims(ctypes.Structure):
     _fields_ = [("hidden", ctypes.c_int32), ("n_heads", ctypes.c_int32),
                 ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("ffn", ctypes.c_int32), ("rms_eps", ctypes.c_float),
-                ("rope_base", ctypes.c_float)]
+                ("rope_base", ctypes.c_float), ("window", ctypes.c_int32)]
 
 
 class vt_shard_info(ctypes.Structure):

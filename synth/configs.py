@@ -19,6 +19,7 @@ class LayerDims:
     ffn: int
     rms_eps: float = 1e-5
     rope_base: float = 10000.0
+    window: int = 0          # sliding-window attention span (0: full causal)
 
     @property
     def group(self) -> int:
@@ -73,6 +74,13 @@ WORKLOADS = {
               "4 devices 25% each, decode at 4096",
         dims=LayerDims(hidden=8192, n_heads=64, n_kv_heads=8, head_dim=128, ffn=28672),
         fracs=(0.25, 0.25, 0.25, 0.25), device=0, weight_sigma=0.015, ctx=4096),
+    "7b_swa": Workload(
+        key="7b_swa", seed_id=6,
+        title="7B-shaped layer with sliding-window attention (window 1024): 30% shard, "
+              "decode at 4096",
+        dims=LayerDims(hidden=4096, n_heads=32, n_kv_heads=32, head_dim=128, ffn=11008,
+                       window=1024),
+        fracs=(0.5, 0.3, 0.2), device=1, weight_sigma=0.02, ctx=4096),
     "7b_prefill": Workload(
         key="7b_prefill", seed_id=5,
         title="prefill chunk on the 7B-shaped layer: 50% shard, 256 tokens at positions 768..1023",

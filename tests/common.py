@@ -88,7 +88,7 @@ def oracle_decode(wl: Workload, li: LayerInputs, r, x, kc, vc, pos, peer_attn=No
     d = wl.dims
     w = w if w is not None else oracle_shard_weights(li, r)
     return oracle.decode(w, r.n_q_heads, r.n_kv_heads, d.head_dim, d.rms_eps, d.rope_base,
-                         x, kc, vc, pos, peer_attn, peer_ffn)
+                         x, kc, vc, pos, peer_attn, peer_ffn, window=d.window)
 
 
 def tiny_workload(seed_id, hidden, n_heads, n_kv, head_dim, ffn, fracs, device, ctx,

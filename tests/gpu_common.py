@@ -16,7 +16,7 @@ SENTINEL = 0x3C01  # fp16 bit pattern left in unused cache slots
 def lib_dims(wd) -> vt.vt_layer_dims:
     return vt.vt_layer_dims(hidden=wd.hidden, n_heads=wd.n_heads, n_kv_heads=wd.n_kv_heads,
                             head_dim=wd.head_dim, ffn=wd.ffn, rms_eps=wd.rms_eps,
-                            rope_base=wd.rope_base)
+                            rope_base=wd.rope_base, window=wd.window)
 
 
 def h16(a):

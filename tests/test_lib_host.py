@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(lib):
 def _dims(wd):
     return vt.vt_layer_dims(hidden=wd.hidden, n_heads=wd.n_heads, n_kv_heads=wd.n_kv_heads,
                             head_dim=wd.head_dim, ffn=wd.ffn, rms_eps=wd.rms_eps,
-                            rope_base=wd.rope_base)
+                            rope_base=wd.rope_base, window=wd.window)
 
 
 @pytest.mark.parametrize("key", sorted(WORKLOADS))
@@ -297,3 +297,13 @@ def test_kv_copy_heads_validation_errors(lib):
             vt.vt_kv_copy_heads(*args)
         assert e.value.status == status
     vt.vt_kv_copy_heads(a, 0, a, 1, 1, 0)                                # nothing to copy
+
+
+def test_window_validation(lib):
+    base = dict(hidden=512, n_heads=8, n_kv_heads=8, head_dim=64, ffn=1376, rms_eps=1e-5,
+                rope_base=1e4)
+    with pytest.raises(vt.VoltronError) as e:
+        vt.vt_shard_spec_create(vt.vt_layer_dims(window=-1, **base), (1.0,), (1.0,), 0)
+    assert e.value.status == vt.VT_ERR_ARG
+    spec = vt.vt_shard_spec_create(vt.vt_layer_dims(window=64, **base), (1.0,), (1.0,), 0)
+    assert vt.vt_shard_spec_query(spec)[0].window == 64
