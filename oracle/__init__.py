@@ -26,6 +26,8 @@ What it follows (paper: Voltron, arXiv 2607.07046):
     gives the values the quantised shard stands for.
   * Sec. 4.3.1 (Pruning): ``prune`` gives the layer that the kept shards of
     a pruned partition add up to.
+  * Sec. 2.1 (FFN variants) and Table 3: ``moe`` is a mixture-of-experts
+    FFN sub-layer (top-k routing) and a device's column share of it.
 
 The paper does not define the decoder's internals (normalisation, rotary
 embedding, FFN form); the readings used here are the Llama layer:

@@ -90,3 +90,31 @@ WORKLOADS = {
 
 def get(key: str) -> Workload:
     return WORKLOADS[key]
+
+
+@dataclass(frozen=True)
+class MoEWorkload:
+    """An MoE FFN sub-layer (routed experts, SwiGLU each) and one device's
+    share of every expert's columns."""
+    key: str
+    seed_id: int
+    title: str
+    hidden: int
+    n_experts: int
+    expert_ffn: int
+    top_k: int
+    fracs: tuple
+    device: int
+    weight_sigma: float = 0.02
+    router_sigma: float = 0.02
+    rms_eps: float = 1e-5
+
+
+MOE_WORKLOADS = {
+    "moe": MoEWorkload(
+        key="moe", seed_id=7,
+        title="MoE FFN shaped like Qwen1.5-MoE-A2.7B's routed experts: hidden 2048, 60 experts "
+              "of 1408 columns, top-4, 4 devices 25% (352 columns of every expert)",
+        hidden=2048, n_experts=60, expert_ffn=1408, top_k=4, fracs=(0.25, 0.25, 0.25, 0.25),
+        device=0),
+}

@@ -157,3 +157,38 @@ def vector(tag: int, n: int, scale: float = 1.0, seed_id: int = 99) -> np.ndarra
     """A seeded fp16 vector N(0, scale) of length n, for tests of the
     partial-sum transmission (``tag`` distinguishes vectors)."""
     return _normal([ROOT_SEED, seed_id, 0, 1000 + tag, 0], (n,), scale)
+
+
+# MoE tensors (ids past the dense layer's): router [E, H], per expert e the
+# gate and up [F_e, H] and down [H, F_e] matrices, the FFN gain and input h
+T_MOE_G, T_MOE_WR, T_MOE_H = 20, 21, 22
+T_MOE_WG, T_MOE_WU, T_MOE_WD = 23, 24, 25
+
+
+class MoEInputs:
+    """Draws the fp16 tensors of an MoE FFN workload (same seeding scheme:
+    expert e's tensor t from PCG64(SeedSequence([7046, seed_id, e, t, 0])))."""
+
+    def __init__(self, wl):
+        self.wl = wl
+
+    def _seed(self, e, tensor, block=0):
+        return [ROOT_SEED, self.wl.seed_id, e, tensor, block]
+
+    def g_ffn(self) -> np.ndarray:
+        return _normal(self._seed(0, T_MOE_G), (self.wl.hidden,), 0.1, 1.0)
+
+    def router(self) -> np.ndarray:
+        return _normal(self._seed(0, T_MOE_WR), (self.wl.n_experts, self.wl.hidden),
+                       self.wl.router_sigma)
+
+    def h(self, token: int = 0) -> np.ndarray:
+        return _normal(self._seed(token, T_MOE_H), (self.wl.hidden,), 1.0)
+
+    def expert(self, name: str, e: int) -> np.ndarray:
+        """Expert e's canonical "wg" / "wu" [F_e, H] or "wd" [H, F_e]."""
+        w = self.wl
+        tid, shape = {"wg": (T_MOE_WG, (w.expert_ffn, w.hidden)),
+                      "wu": (T_MOE_WU, (w.expert_ffn, w.hidden)),
+                      "wd": (T_MOE_WD, (w.hidden, w.expert_ffn))}[name]
+        return _normal(self._seed(e, tid), shape, w.weight_sigma)
