@@ -97,6 +97,8 @@ def parse():
                     help="timed calls of each partial-sum transmission kernel (0: skip)")
     ap.add_argument("--quant-steps", type=int, default=1000,
                     help="timed decode steps over INT8 and INT4 weight shards (0: skip)")
+    ap.add_argument("--moe-steps", type=int, default=1000,
+                    help="MoE FFN shard decode steps (0: skip)")
     ap.add_argument("--repack-reps", type=int, default=20,
                     help="timed shard packs of the re-partition section (0: skip)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -292,6 +294,8 @@ def main():
     if args.quant_steps > 0:
         out["quant"] = quant_section(spec, dims, info, wl, args.quant_steps,
                                      max(1, args.quant_steps // 10), layers[0][0], args.eager)
+    if args.moe_steps > 0:
+        out["moe"] = moe_section(args.moe_steps, max(1, args.moe_steps // 10), args.eager)
     if args.cpu_seconds > 0:
         out["cpu_baseline"] = cpu_baseline(wl, pos, args.cpu_seconds, step_bytes)
     print(json.dumps(out), flush=True)
@@ -461,6 +465,95 @@ def quant_section(spec, dims, info, wl, steps, warmup, fp16_weights, eager=False
     res["note"] = ("same shard and position as the headline; bytes = codes + fp16 block scales "
                    "+ K/V + vectors; the format is the library's own 32-column block format")
     return res
+
+
+def moe_bytes(wl, n_cols):
+    """Algorithmic HBM bytes of one token through an MoE FFN shard: the
+    router, the selected experts' gate/up rows and down columns of the
+    shard, the gain, h in, the partial and y out."""
+    H, E, k = wl.hidden, wl.n_experts, wl.top_k
+    return 2 * (E * H + k * 3 * n_cols * H + 4 * H)
+
+
+def moe_section(steps, warmup, eager=False):
+    """Batch-1 decode through the MoE FFN shard (device 0 of the MoE
+    workload) with vt_moe_ffn_decode: 16 distinct tokens (each selects its
+    own experts) over enough weight copies (>= 768 MB) to keep the Infinity
+    Cache from serving them."""
+    import torch
+
+    from paper_2607_07046_amd import pack
+    from paper_2607_07046_amd import voltron as vt
+    from synth.configs import MOE_WORKLOADS
+    from synth.gen import MoEInputs
+
+    wl = MOE_WORKLOADS["moe"]
+    mi = MoEInputs(wl)
+    dims = vt.vt_layer_dims(hidden=wl.hidden, n_heads=1, n_kv_heads=1, head_dim=64,
+                            ffn=wl.expert_ffn, rms_eps=wl.rms_eps, rope_base=1e4, window=0)
+    spec = vt.vt_shard_spec_create(dims, wl.fracs, wl.fracs, wl.device)
+    _, info = vt.vt_shard_spec_query(spec)
+    nc = info.n_cols
+    shard_bytes = 2 * wl.n_experts * 3 * nc * wl.hidden
+    copies = max(1, math.ceil(MALL_DEFEAT_BYTES / shard_bytes))
+    w0 = pack.pack_moe_shard(mi, info.col_begin, nc)
+    shards = [w0]
+    for _ in range(1, copies):
+        t = {k: v.clone() for k, v in w0.tensors.items()}
+        p = lambda x: x.data_ptr()
+        shards.append(pack.MoEShardDev(t, vt.vt_moe_weights(
+            g_ffn=p(t["g_ffn"]), wr=p(t["wr"]), ld_r=w0.struct.ld_r, wg=p(t["wg"]),
+            ld_g=w0.struct.ld_g, wu=p(t["wu"]), ld_u=w0.struct.ld_u, wd=p(t["wd"]),
+            ld_d=w0.struct.ld_d)))
+    ntok = 16
+    hs = torch.from_numpy(np.stack([mi.h(t) for t in range(ntok)])).cuda()
+    H, k = wl.hidden, wl.top_k
+    p_ffn, y = (torch.empty(H, dtype=torch.float16, device="cuda") for _ in range(2))
+    sel = torch.empty(k, dtype=torch.int32, device="cuda")
+    ws_bytes = vt.vt_moe_workspace_size(spec, wl.n_experts, k)
+    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device="cuda")
+
+    def enqueue(i, stream):
+        io = vt.vt_layer_io(x=None, peer_attn=None, peer_ffn=None, attn_partial=None,
+                            h=hs[i % ntok].data_ptr(), ffn_partial=p_ffn.data_ptr(),
+                            y=y.data_ptr())
+        vt.vt_moe_ffn_decode(spec, shards[i % copies].struct, wl.n_experts, k, io,
+                             sel.data_ptr(), None, ws.data_ptr(), ws_bytes, stream)
+
+    per_graph = ntok * copies
+    g = None
+    if not eager:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for i in range(per_graph):
+                enqueue(i, torch.cuda.current_stream().cuda_stream)
+
+    def run(n):
+        if g is None:
+            for i in range(n):
+                enqueue(i, torch.cuda.current_stream().cuda_stream)
+            return n
+        reps = max(1, n // per_graph)
+        for _ in range(reps):
+            g.replay()
+        return reps * per_graph
+
+    run(warmup)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    n = run(steps)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / n
+    if not torch.isfinite(p_ffn.float()).all():
+        raise SystemExit("non-finite output of the MoE decode steps")
+    b = moe_bytes(wl, nc)
+    gbps = b / (ms * 1e-3) / 1e9
+    return {"workload": wl.title, "us_per_token": round(ms * 1e3, 3),
+            "tokens_s": round(1e3 / ms, 1), "bytes_per_token": b, "hbm_GBps": round(gbps, 1),
+            "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4), "weight_copies": copies, "steps": n,
+            "launch": "one persistent kernel: router | route + gate/up | down"}
 
 
 def comm_section(steps):

@@ -303,6 +303,57 @@ vt_status vt_shard_pack(const vt_shard_spec* spec, const vt_layer_weights* full,
 vt_status vt_kv_copy_heads(const vt_kv_view* src, int32_t src_head0, const vt_kv_view* dst,
                            int32_t dst_head0, int32_t n_heads, int32_t n_pos, void* stream);
 
+/* ---- Mixture-of-experts FFN (paper Sec. 2.1 FFN variants; Table 3's
+ * MoE model) ----
+ * The FFN sub-layer of an MoE layer, batch-1 decode, on one device's share:
+ * w = RMSNorm(h) * g_ffn; router logits r = Wr w over the n_experts
+ * experts; the top_k experts with the largest logits (ties: the lower
+ * index) are selected; output = sum over them of p_e * Wd_e (silu(Wg_e w)
+ * * (Wu_e w)), p = softmax(r) over all n_experts (not renormalised over
+ * the selection). Tensor parallelism shards every expert by its FFN columns
+ * as for the dense FFN, and every device routes for itself (the router is
+ * small), so the devices' partial sums add up to the unsharded output. The
+ * routed experts only: a shared expert is a dense FFN (vt_layer_decode
+ * with VT_FFN). */
+
+/* An MoE shard's weights (device, fp16, ld in elements, multiples of 8):
+ * wr [n_experts][ld_r >= hidden] router rows; wg, wu
+ * [n_experts][n_cols][ld >= hidden]: expert e's gate / up rows of the
+ * shard's columns (spec's col_begin.. of the expert's FFN); wd
+ * [n_experts][hidden][ld_d >= n_cols]: expert e's down rows over those
+ * columns. Each matrix must span less than 2 GiB. With n_cols = 0 the
+ * expert matrices may be NULL (the partial sum is then zero). */
+typedef struct vt_moe_weights {
+  const void* g_ffn;  /* [hidden] */
+  const void* wr;
+  int64_t ld_r;
+  const void* wg;
+  int64_t ld_g;
+  const void* wu;
+  int64_t ld_u;
+  const void* wd;
+  int64_t ld_d;
+} vt_moe_weights;
+
+/* Workspace bytes of vt_moe_ffn_decode (zero-filled once before its first
+ * use; the synchronisation words are left zero after every call; not shared
+ * by calls that may run at the same time). 1 <= n_experts <= 256,
+ * 1 <= top_k <= min(n_experts, 8), spec's n_cols < 32768. */
+vt_status vt_moe_workspace_size(const vt_shard_spec* spec, int32_t n_experts, int32_t top_k,
+                                size_t* bytes);
+
+/* One token through the MoE FFN shard. ``spec``: the layer's shard spec
+ * with dims.ffn one expert's FFN width (its n_cols / col_begin are the
+ * shard's columns of every expert; the attention fields are not used).
+ * Reads io->h and io->peer_ffn (optional); writes io->ffn_partial and, if
+ * not NULL, io->y = h + ffn_partial + peer_ffn (fp32 sum, rounded once).
+ * sel_out / prob_out (device, optional): the selected experts in
+ * descending logit order and their probabilities [top_k]. hidden must be a
+ * multiple of 8 up to 16384. */
+vt_status vt_moe_ffn_decode(const vt_shard_spec* spec, const vt_moe_weights* w, int32_t n_experts,
+                            int32_t top_k, const vt_layer_io* io, int32_t* sel_out, float* prob_out,
+                            void* ws, size_t ws_bytes, void* stream);
+
 /* ---- Communication scaling of the partial sums (paper Sec. 4.3.2) ----
  * To cut the bytes a device sends for the aggregation, its partial sums go
  * out in blocks of 32 activations, each at one precision; precisions are

@@ -42,10 +42,22 @@ constexpr int REC = 4;           // attention partial record = head_dim + REC fl
 constexpr unsigned kSpinLimit = 1u << 20;  // about a second of polling
 
 enum { PH_QKV = 0, PH_ATTN = 1, PH_O = 2, PH_GATEUP = 3, PH_DOWN = 4 };
-// Synchronisation words, each hot word in its own 4 KiB-separated spot so
-// that the grid barrier's pollers do not share a memory channel with the
-// per-head counters of the attention phase.
-enum { SW_BAR = 0, SW_EXIT = 1024, SW_ERR = 2048, SW_GROUP = 3072, SW_GROUP_STRIDE = 32 };
+// Synchronisation words, each kind in its own 4 KiB-separated spot so that
+// the grid barrier's pollers do not share a memory channel with the
+// per-head counters of the attention phase. The grid barrier counts
+// arrivals on NBAR counters (workgroup b on counter b % NBAR, BAR_STRIDE
+// words apart): agent-scope atomics on one word are performed one after
+// another, and 256 of them on a single counter made a barrier cost about
+// three times as much as on sixteen (measured on MI355X).
+constexpr int NBAR = 16, BAR_STRIDE = 32;
+enum {
+  SW_BAR = 0,
+  SW_EXIT = 1024,                        // exit counters, same layout
+  SW_EXIT_TOP = SW_EXIT + NBAR * BAR_STRIDE,  // groups whose workgroups have all left
+  SW_ERR = 2048,
+  SW_GROUP = 3072,
+  SW_GROUP_STRIDE = 32
+};
 
 struct Params {
   int H, d, nq, nkv, G, ncols, pos, cap, nchunk, cl;
@@ -73,19 +85,30 @@ struct Params {
 // grid barrier (only between phases of one persistent launch)
 // ---------------------------------------------------------------------------
 // Data crossing the barrier moves through st_shared / ld_shared only, so
-// arrival is: every wave's stores complete, then one relaxed increment.
+// arrival is: every wave's stores complete, then one relaxed increment of
+// the workgroup's counter.
 __device__ __forceinline__ void grid_arrive(unsigned* sync) {
   mem_done();
   __syncthreads();
   if (threadIdx.x == 0)
-    __hip_atomic_fetch_add(sync + SW_BAR, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_fetch_add(sync + SW_BAR + BAR_STRIDE * (blockIdx.x % NBAR), 1u, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
 }
 
-__device__ __forceinline__ void grid_wait(unsigned* sync, unsigned target) {
-  if (threadIdx.x == 0) {
+// Workgroups counting on counter i of NBAR.
+__device__ __forceinline__ unsigned bar_group_size(unsigned i) {
+  return i < gridDim.x ? (gridDim.x - i + NBAR - 1) / NBAR : 0u;
+}
+
+// Wait until every workgroup has arrived ``k`` times: lane i < NBAR of wave
+// 0 polls counter i.
+__device__ __forceinline__ void grid_wait(unsigned* sync, unsigned k) {
+  if (threadIdx.x < NBAR) {
+    const unsigned target = k * bar_group_size(threadIdx.x);
     unsigned n = 0;
-    while (__hip_atomic_load(sync + SW_BAR, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
-      __builtin_amdgcn_s_sleep(4);
+    while (__hip_atomic_load(sync + SW_BAR + BAR_STRIDE * threadIdx.x, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT) < target) {
+      __builtin_amdgcn_s_sleep(2);
       if (++n > kSpinLimit) {  // never expected: report instead of hanging
         sync_or(sync + SW_ERR, 1u);
         break;
@@ -93,6 +116,30 @@ __device__ __forceinline__ void grid_wait(unsigned* sync, unsigned target) {
     }
   }
   __syncthreads();
+}
+
+// At the end of a launch with grid barriers: the last workgroup out (the
+// last of the last group to empty) zeroes the barrier and exit counters for
+// the next launch.
+__device__ __forceinline__ void grid_exit(unsigned* sync) {
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const unsigned g = blockIdx.x % NBAR;
+    const unsigned old = __hip_atomic_fetch_add(sync + SW_EXIT + BAR_STRIDE * g, 1u, __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT);
+    if (old == bar_group_size(g) - 1) {
+      const unsigned ngroups = min(gridDim.x, static_cast<unsigned>(NBAR));
+      const unsigned top =
+          __hip_atomic_fetch_add(sync + SW_EXIT_TOP, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (top == ngroups - 1) {
+        for (int i = 0; i < NBAR; ++i) {
+          sync_store(sync + SW_BAR + BAR_STRIDE * i, 0u);
+          sync_store(sync + SW_EXIT + BAR_STRIDE * i, 0u);
+        }
+        sync_store(sync + SW_EXIT_TOP, 0u);
+      }
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -123,21 +170,34 @@ __device__ __forceinline__ RowAt mat_row(const Mat& m, int r) {
   return RowAt{m.r, m.s, static_cast<uint32_t>(r) * m.ld, static_cast<uint32_t>(r) * m.lds};
 }
 
+// Every row source also gives the byte offset of a row's segment sg (a
+// piece of 1 KiB); only the MoE down projection maps segments elsewhere.
+// kSlotTail: the row is several inputs one after the other, each ending in
+// a partial segment whose weight columns past col_limit are masked (plain
+// rows mask only past K).
+__device__ __forceinline__ uint32_t plain_seg(int sg) { return static_cast<uint32_t>(sg) * 1024u; }
+
 struct RowsQKV {
+  static constexpr bool kSlotTail = false;
   Mat q, k, v;
   int nqd, nkd;
+  __device__ __forceinline__ uint32_t seg_off(int sg) const { return plain_seg(sg); }
   __device__ __forceinline__ RowAt at(int r) const {
     return r < nqd ? mat_row(q, r) : r < nqd + nkd ? mat_row(k, r - nqd) : mat_row(v, r - nqd - nkd);
   }
 };
 
 struct RowsOne {
+  static constexpr bool kSlotTail = false;
   Mat m;
+  __device__ __forceinline__ uint32_t seg_off(int sg) const { return plain_seg(sg); }
   __device__ __forceinline__ RowAt at(int r) const { return mat_row(m, r); }
 };
 
 struct RowsPair {  // row 2j -> a[j], row 2j+1 -> b[j]
+  static constexpr bool kSlotTail = false;
   Mat a, b;
+  __device__ __forceinline__ uint32_t seg_off(int sg) const { return plain_seg(sg); }
   __device__ __forceinline__ RowAt at(int r) const { return (r & 1) ? mat_row(b, r >> 1) : mat_row(a, r >> 1); }
 };
 
@@ -290,7 +350,7 @@ __device__ __forceinline__ void gemv_impl(const Rows& rows, int units, int K, co
     const int lr = div_rcp(p, rcp);
     const int sg = p - lr * nseg;
     const RowAt ra = rows.at(row0 + lr);
-    const uint32_t base = __builtin_amdgcn_readfirstlane(ra.off + static_cast<uint32_t>(sg) * 1024u);
+    const uint32_t base = __builtin_amdgcn_readfirstlane(ra.off + rows.seg_off(sg));
     const bool ok = (p < q1) && (sg != nseg - 1 || lane_in_tail);
     const uint32_t oob = static_cast<uint32_t>(!ok) << 31;
     return __builtin_amdgcn_raw_buffer_load_b128(ra.rs, (base + lane16) | oob, 0, 0);
@@ -378,7 +438,10 @@ __device__ __forceinline__ void gemv_impl(const Rows& rows, int units, int K, co
           const u32x4* xp = reinterpret_cast<const u32x4*>(xs16 + col);
           if constexpr (F == FMT_F16) {
             u32x4 w = buf[i];
-            if (cs == nseg - 1 && tail < SEGC) w = mask_tail(w, col, K);
+            if constexpr (Rows::kSlotTail)
+              w = mask_tail(w, col, rows.col_limit(cs));
+            else if (cs == nseg - 1 && tail < SEGC)
+              w = mask_tail(w, col, K);
             acc = dot8(w, xp[0], acc);
           } else {
             // codes past K are zero by the format, and so is the input
@@ -577,7 +640,7 @@ __host__ __device__ __forceinline__ int attn_lds_floats(int d, int nchunk) {
   return d + MAXPASS * ppp + ppp * d + 2 * d + 2 * nchunk + 4;
 }
 
-__device__ __forceinline__ void phase_attn(const Params& P, float* lds, bool wait, unsigned target) {
+__device__ __forceinline__ void phase_attn(const Params& P, float* lds, bool wait, unsigned nbar) {
   const int d = P.d, G = P.G, CL = P.cl;
   const int TPP = d / 8, PPP = NT / TPP, NPASS = CL / PPP;
   const int t = threadIdx.x, wave = t / kWave, lane = t % kWave;
@@ -624,7 +687,7 @@ __device__ __forceinline__ void phase_attn(const Params& P, float* lds, bool wai
     float c0 = 1.f, s0 = 0.f;
     if (t < half) rope_angle(P.pos, t, d, P.rope_base, c0, s0);
     if (!waited) {
-      if (wait) grid_wait(P.sync, target);
+      if (wait) grid_wait(P.sync, nbar);
       waited = true;
     }
     if (id >= ids) break;
@@ -807,10 +870,11 @@ __device__ __forceinline__ void phase_attn(const Params& P, float* lds, bool wai
 // ---------------------------------------------------------------------------
 // the kernel
 // ---------------------------------------------------------------------------
-// One phase; ``wait`` / ``target`` describe the grid barrier in front of it.
+// One phase; ``wait``: a grid barrier is in front of it, the ``nbar``-th of
+// the launch.
 template <int PH, int F>
 __device__ __forceinline__ void run_phase(const Params& P, float* lds, uint16_t* xs, float* slots,
-                                          float* red, bool wait, unsigned target) {
+                                          float* red, bool wait, unsigned nbar) {
   uint16_t* scl = reinterpret_cast<uint16_t*>(red + 16);  // block scales (quantised formats)
   if constexpr (PH == PH_QKV) {
     RowsQKV rows{make_mat(P.wq, P.ld_q, P.nq * P.d, P.sq, P.lds_q),
@@ -821,14 +885,14 @@ __device__ __forceinline__ void run_phase(const Params& P, float* lds, uint16_t*
         [&]() { stage_rmsnorm_h(P.x, P.g_attn, P.H, padded(P.H, F), P.eps, xs, red); },
         [&](int r, const float* v) { st_shared(P.qkv + r, v[0]); });
   } else if constexpr (PH == PH_ATTN) {
-    phase_attn(P, lds, wait, target);
+    phase_attn(P, lds, wait, nbar);
   } else if constexpr (PH == PH_O) {
     RowsOne rows{make_mat(P.wo, P.ld_o, P.H, P.so, P.lds_o)};
     const int K = P.nq * P.d;
     gemv_phase<1, F>(
         rows, P.H, K, xs, slots, scl,
         [&]() {
-          if (wait) grid_wait(P.sync, target);
+          if (wait) grid_wait(P.sync, nbar);
           stage_copy_f(P.o, K, padded(K, F), xs);
         },
         [&](int r, const float* v) {
@@ -844,7 +908,7 @@ __device__ __forceinline__ void run_phase(const Params& P, float* lds, uint16_t*
     gemv_phase<2, F>(
         rows, P.ncols, P.H, xs, slots, scl,
         [&]() {
-          if (wait) grid_wait(P.sync, target);
+          if (wait) grid_wait(P.sync, nbar);
           if (P.h_from_ws)
             stage_rmsnorm_f(P.hbuf, P.g_ffn, P.H, padded(P.H, F), P.eps, xs, red);
           else
@@ -860,7 +924,7 @@ __device__ __forceinline__ void run_phase(const Params& P, float* lds, uint16_t*
     gemv_phase<1, F>(
         rows, P.H, K, xs, slots, scl,
         [&]() {
-          if (wait) grid_wait(P.sync, target);
+          if (wait) grid_wait(P.sync, nbar);
           stage_copy_f(P.m, K, padded(K, F), xs);
         },
         [&](int r, const float* v) {
@@ -877,7 +941,7 @@ __device__ __forceinline__ void run_phase(const Params& P, float* lds, uint16_t*
 template <int PH, int PE, int PB, int F>
 __device__ __forceinline__ void run_phases(const Params& P, float* lds, uint16_t* xs, float* slots,
                                            float* red) {
-  run_phase<PH, F>(P, lds, xs, slots, red, PH > PB, static_cast<unsigned>(PH - PB) * gridDim.x);
+  run_phase<PH, F>(P, lds, xs, slots, red, PH > PB, static_cast<unsigned>(PH - PB));
   if constexpr (PH < PE) {
     grid_arrive(P.sync);
     run_phases<PH + 1, PE, PB, F>(P, lds, xs, slots, red);
@@ -897,17 +961,232 @@ __global__ void __launch_bounds__(NT) decode_kernel(Params P) {
   float* slots = lds + max(kmax / 2, attn);
   float* red = slots + MAX_SLOTS;
   run_phases<PB, PE, PB, F>(P, lds, xs, slots, red);
-  if constexpr (PE > PB) {  // the last workgroup out clears the barrier words
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      const unsigned old = __hip_atomic_fetch_add(P.sync + SW_EXIT, 1u, __ATOMIC_RELAXED,
-                                                  __HIP_MEMORY_SCOPE_AGENT);
-      if (old == gridDim.x - 1) {
-        sync_store(P.sync + SW_BAR, 0u);
-        sync_store(P.sync + SW_EXIT, 0u);
+  if constexpr (PE > PB) grid_exit(P.sync);
+}
+
+// ---------------------------------------------------------------------------
+// Mixture-of-experts FFN of a shard (paper Sec. 2.1 FFN variants; the MoE
+// model of Table 3): w = RMSNorm(h) * g_ffn; router logits Wr w over the E
+// experts; the top_k largest (ties: lower index) with their softmax
+// probabilities p (over all E); output sum over the selected experts of
+// p_e Wd_e (silu(Wg_e w) * (Wu_e w)), over this shard's columns of every
+// expert. One persistent launch: router GEMV | routing (every workgroup,
+// from the logits) + the selected experts' gate/up GEMV | down GEMV.
+// ---------------------------------------------------------------------------
+constexpr int MOE_MAX_E = 256, MOE_MAX_K = 8;
+
+struct MoeParams {
+  int H, E, topk, ncols, npe;  // npe: a slot's share of the down input, whole 512-column segments
+  uint64_t m_ncols;            // div_m40 multiplier of ncols
+  float eps;
+  const uint16_t *g_ffn, *h, *peer_f;
+  const uint8_t *wr, *wg, *wu, *wd;  // strides in bytes
+  int64_t ld_r, ld_g, ld_u, ld_d;
+  uint16_t *p_ffn, *y;
+  float *logits, *m;  // m: [topk][ncols]
+  int32_t* sel_out;
+  float* prob_out;
+  unsigned* sync;
+};
+
+// q / n for 0 <= q < 2^18 and n < 2^15 with m = floor(2^40 / n) + 1 (exact
+// while q * n < 2^40).
+__device__ __forceinline__ int div_m40(int q, uint64_t m) {
+  return static_cast<int>((static_cast<uint64_t>(static_cast<uint32_t>(q)) * m) >> 40);
+}
+
+// The selected experts (each < 256) packed a byte per slot into one
+// wave-uniform 64-bit word: a slot's expert is a shift and a mask in scalar
+// registers (a register array indexed by the slot would be placed in
+// scratch memory).
+__device__ __forceinline__ int slot_expert(uint64_t sel8, int sl) {
+  return static_cast<int>((sel8 >> (8 * sl)) & 0xFFu);
+}
+
+// Virtual row 2u (+1): the gate (up) row of column j of the expert in slot
+// s, u = s * ncols + j; expert e's column j is row e * ncols + j of wg / wu.
+struct RowsMoePair {
+  static constexpr bool kSlotTail = false;
+  Mat g, u;
+  int ncols, topk;
+  uint64_t m_ncols;  // div_m40 multiplier of ncols
+  uint64_t sel8;
+  // (rows past the phase's units are asked for by loads that read nothing;
+  // the slot is clamped all the same)
+  __device__ __forceinline__ RowAt at(int r) const {
+    const int un = r >> 1, sl = min(div_m40(un, m_ncols), topk - 1), j = un - sl * ncols;
+    const int row = slot_expert(sel8, sl) * ncols + j;
+    return (r & 1) ? mat_row(u, row) : mat_row(g, row);
+  }
+  __device__ __forceinline__ uint32_t seg_off(int sg) const { return plain_seg(sg); }
+};
+
+// Row r of the down projection over the selected experts: its input is the
+// slots' m vectors one after the other, each padded to spe segments;
+// segment sg of row r is in the matrix of the expert of slot sg / spe
+// (expert e's rows start at byte e * H * ld).
+struct RowsMoeDown {
+  static constexpr bool kSlotTail = true;
+  Mat d;
+  int H, spe, ncols;
+  uint32_t rcp_spe;  // div_rcp reciprocal of spe
+  uint64_t sel8;
+  __device__ __forceinline__ RowAt at(int r) const { return mat_row(d, r); }
+  __device__ __forceinline__ uint32_t seg_off(int sg) const {
+    const int sl = div_rcp(sg, rcp_spe), ls = sg - sl * spe;
+    return static_cast<uint32_t>(slot_expert(sel8, sl) * H) * d.ld + static_cast<uint32_t>(ls) * 1024u;
+  }
+  // columns of slot sl's input are [sl * spe * 512, that + ncols)
+  __device__ __forceinline__ int col_limit(int sg) const {
+    return div_rcp(sg, rcp_spe) * spe * Fmt<FMT_F16>::SEGC + ncols;
+  }
+};
+
+// Every workgroup: the top_k experts and their probabilities from the E
+// logits, into LDS (sel / prob). Thread t < E ranks expert t among all E
+// (larger logit first, ties to the lower index); the top_k ranks also take
+// the softmax denominator. The logits are read back from LDS 16 at a time
+// (four 16-byte reads in flight), padded with -inf to a multiple of 16. sel
+// entries start at 0, so they name an expert whatever the logits hold.
+// ``L`` is 16-byte aligned LDS scratch of MOE_MAX_E floats. Ends with a
+// workgroup barrier.
+__device__ __forceinline__ void moe_route(const MoeParams& P, float* L, int* sel, float* prob) {
+  const int t = threadIdx.x;
+  const int e16 = (P.E + 15) & ~15;
+  if (t < MOE_MAX_K) {
+    sel[t] = 0;
+    prob[t] = 0.f;
+  }
+  if (t < e16) {
+    const uint32_t off = static_cast<uint32_t>(t) * 4u | (static_cast<uint32_t>(t >= P.E) << 31);
+    const float l = buf_ld_shared(make_rsrc(P.logits, static_cast<uint32_t>(P.E) * 4u), off);
+    L[t] = t < P.E ? l : -INFINITY;
+  }
+  __syncthreads();
+  if (t < P.E) {
+    const float4* L4 = reinterpret_cast<const float4*>(L);
+    const float v = L[t];
+    float mx = -INFINITY;
+    int rank = 0;
+    for (int i0 = 0; i0 < e16; i0 += 16) {
+      float4 q[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) q[u] = L4[i0 / 4 + u];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float c[4] = {q[u].x, q[u].y, q[u].z, q[u].w};
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const int i = i0 + 4 * u + w;
+          mx = fmaxf(mx, c[w]);
+          rank += (c[w] > v || (c[w] == v && i < t)) ? 1 : 0;
+        }
       }
     }
+    if (rank < P.topk) {
+      float sum = 0.f;
+      for (int i0 = 0; i0 < e16; i0 += 16) {
+        float4 q[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) q[u] = L4[i0 / 4 + u];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          sum += (__expf(q[u].x - mx) + __expf(q[u].y - mx)) + (__expf(q[u].z - mx) + __expf(q[u].w - mx));
+      }
+      sel[rank] = t;
+      prob[rank] = __expf(v - mx) / sum;
+    }
   }
+  __syncthreads();
+}
+
+// xs[k] for k < topk * npe: slot k / npe's m value at column k % npe, zero
+// from ncols on. Coherent loads in batches; positions without a value read
+// nothing (offset past the buffer). Ends with a workgroup barrier.
+__device__ __forceinline__ void moe_stage_down(const MoeParams& P, uint16_t* xs, uint32_t rcp_spe) {
+  constexpr int B = 8;
+  const int n = P.topk * P.npe;
+  const rsrc_t rm = make_rsrc(P.m, static_cast<uint32_t>(P.topk * P.ncols) * 4u);
+  for (int c0 = 0; c0 < n; c0 += B * NT) {
+    float v[B];
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+      const int k = c0 + threadIdx.x + u * NT;
+      const int sl = div_rcp(k >> 9, rcp_spe), j = k - sl * P.npe;
+      const bool ok = k < n && j < P.ncols;
+      const uint32_t off = static_cast<uint32_t>(sl * P.ncols + j) * 4u;
+      v[u] = buf_ld_shared(rm, off | (static_cast<uint32_t>(!ok) << 31));
+    }
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+      const int k = c0 + threadIdx.x + u * NT;
+      if (k < n) xs[k] = f2h(v[u]);
+    }
+  }
+  __syncthreads();
+}
+
+__global__ void __launch_bounds__(NT) moe_kernel(MoeParams P) {
+  extern __shared__ float lds[];
+  // LDS: xs | slots[MAX_SLOTS] | red[16] | sel[MOE_MAX_K] | prob[MOE_MAX_K]
+  const int kmax = max(padded(P.H, FMT_F16), P.topk * P.npe);
+  uint16_t* xs = reinterpret_cast<uint16_t*>(lds);
+  float* slots = lds + kmax / 2;
+  float* red = slots + MAX_SLOTS;
+  int* sel = reinterpret_cast<int*>(red + 16);
+  float* prob = reinterpret_cast<float*>(sel + MOE_MAX_K);
+
+  // router logits (xs keeps w for the gate/up phase)
+  gemv_phase<1, FMT_F16>(
+      RowsOne{make_mat(P.wr, P.ld_r, P.E, nullptr, 0)}, P.E, P.H, xs, slots, nullptr,
+      [&]() { stage_rmsnorm_h(P.h, P.g_ffn, P.H, padded(P.H, FMT_F16), P.eps, xs, red); },
+      [&](int e, const float* v) { st_shared(P.logits + e, v[0]); });
+  grid_arrive(P.sync);
+  grid_wait(P.sync, 1);
+  moe_route(P, slots, sel, prob);  // slots are free between phases
+  if (blockIdx.x == 0 && threadIdx.x < P.topk) {
+    if (P.sel_out) P.sel_out[threadIdx.x] = sel[threadIdx.x];
+    if (P.prob_out) P.prob_out[threadIdx.x] = prob[threadIdx.x];
+  }
+  // the selected experts' gate/up rows; m = p_e * silu(gate) * up
+  uint64_t sel8 = 0;
+#pragma unroll
+  for (int i = 0; i < MOE_MAX_K; ++i)
+    sel8 |= static_cast<uint64_t>(__builtin_amdgcn_readfirstlane(sel[i]) & 0xFF) << (8 * i);
+  const RowsMoePair rp{make_mat(P.wg, P.ld_g, static_cast<int64_t>(P.E) * P.ncols, nullptr, 0),
+                       make_mat(P.wu, P.ld_u, static_cast<int64_t>(P.E) * P.ncols, nullptr, 0),
+                       P.ncols,
+                       P.topk,
+                       P.m_ncols,
+                       sel8};
+  const int spe = P.npe / Fmt<FMT_F16>::SEGC;
+  const RowsMoeDown rd{make_mat(P.wd, P.ld_d, static_cast<int64_t>(P.E) * P.H, nullptr, 0),
+                       P.H,
+                       spe,
+                       P.ncols,
+                       (1u << 24) / static_cast<uint32_t>(spe) + 1u,
+                       sel8};
+  gemv_phase<2, FMT_F16>(
+      rp, P.topk * P.ncols, P.H, xs, slots, nullptr, []() { __syncthreads(); },
+      [&](int un, const float* v) {
+        const int sl = un / P.ncols;
+        const float gt = v[0], up = v[1];
+        st_shared(P.m + un, prob[sl] * (gt / (1.0f + __expf(-gt)) * up));
+      });
+  grid_arrive(P.sync);
+  // down rows over the selected experts' columns
+  gemv_phase<1, FMT_F16>(
+      rd, P.H, P.topk * P.npe, xs, slots, nullptr,
+      [&]() {
+        grid_wait(P.sync, 2);
+        moe_stage_down(P, xs, rd.rcp_spe);
+      },
+      [&](int r, const float* v) {
+        const float pf = v[0];
+        P.p_ffn[r] = f2h(pf);
+        if (P.y) P.y[r] = f2h(h2f(P.h[r]) + pf + (P.peer_f ? h2f(P.peer_f[r]) : 0.f));
+      });
+  grid_exit(P.sync);
 }
 
 typedef void (*DecodeKernel)(Params);
@@ -1002,6 +1281,8 @@ vt_status device_info(DeviceInfo** out) {
         (void)hipFuncSetAttribute(reinterpret_cast<const void*>(dec::decode_kernel_for(r[0], r[1], fmt)),
                                   hipFuncAttributeMaxDynamicSharedMemorySize,
                                   static_cast<int>(di.max_lds));
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(dec::moe_kernel),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(di.max_lds));
     (void)hipGetLastError();
     di.lds_attr_set = true;
   }
@@ -1414,5 +1695,136 @@ extern "C" vt_status vt_workspace_size(const vt_shard_spec* spec, int32_t max_to
   if (max_tokens < 1 || max_ctx < 1) return fail(VT_ERR_ARG, "max_tokens and max_ctx must be >= 1");
   *bytes = std::max(decode_workspace_bytes(*spec, max_ctx),
                     prefill_workspace_bytes(*spec, max_tokens, max_ctx));
+  return VT_OK;
+}
+
+// ---------------------------------------------------------------------------
+// MoE FFN of a shard
+// ---------------------------------------------------------------------------
+namespace {
+
+struct MoeWs {
+  size_t sync, logits, m, total;
+  int npe;
+};
+
+MoeWs moe_ws_layout(const vt_shard_spec& s, int32_t top_k, int32_t n_experts) {
+  MoeWs w{};
+  w.npe = static_cast<int>(std::max<int64_t>(512, round_up(s.info.n_cols, 512)));
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = off;
+    off += static_cast<size_t>(round_up(static_cast<int64_t>(bytes), 256));
+    return at;
+  };
+  w.sync = take(sizeof(unsigned) * (dec::SW_GROUP + dec::SW_GROUP_STRIDE));
+  w.logits = take(sizeof(float) * n_experts);
+  w.m = take(sizeof(float) * static_cast<size_t>(top_k) * w.npe);
+  w.total = off;
+  return w;
+}
+
+vt_status check_moe_args(const vt_shard_spec* spec, int32_t n_experts, int32_t top_k) {
+  if (!spec) return fail(VT_ERR_ARG, "null spec");
+  if (n_experts < 1 || n_experts > dec::MOE_MAX_E)
+    return fail(VT_ERR_UNSUPPORTED, "n_experts %d outside [1, %d]", n_experts, dec::MOE_MAX_E);
+  if (top_k < 1 || top_k > std::min(n_experts, dec::MOE_MAX_K))
+    return fail(VT_ERR_ARG, "top_k %d outside [1, min(n_experts, %d)]", top_k, dec::MOE_MAX_K);
+  if (spec->info.n_cols >= 32768) return fail(VT_ERR_UNSUPPORTED, "n_cols %d >= 32768", spec->info.n_cols);
+  return VT_OK;
+}
+
+}  // namespace
+
+extern "C" vt_status vt_moe_workspace_size(const vt_shard_spec* spec, int32_t n_experts, int32_t top_k,
+                                           size_t* bytes) {
+  clear_error();
+  if (!bytes) return fail(VT_ERR_ARG, "null argument");
+  vt_status st = check_moe_args(spec, n_experts, top_k);
+  if (st != VT_OK) return st;
+  *bytes = moe_ws_layout(*spec, top_k, n_experts).total;
+  return VT_OK;
+}
+
+extern "C" vt_status vt_moe_ffn_decode(const vt_shard_spec* spec, const vt_moe_weights* w, int32_t n_experts,
+                                       int32_t top_k, const vt_layer_io* io, int32_t* sel_out, float* prob_out,
+                                       void* ws, size_t ws_bytes, void* stream) {
+  clear_error();
+  vt_status st = check_moe_args(spec, n_experts, top_k);
+  if (st != VT_OK) return st;
+  if (!w || !io) return fail(VT_ERR_ARG, "null argument");
+  const vt_layer_dims& D = spec->dims;
+  const int64_t H = D.hidden, E = n_experts, nc = spec->info.n_cols;
+  if (H % 8 || H > 16384) return fail(VT_ERR_UNSUPPORTED, "hidden %lld: a multiple of 8 up to 16384", (long long)H);
+  if (!w->g_ffn || !aligned16(w->g_ffn)) return fail(VT_ERR_ARG, "g_ffn NULL or not 16-byte aligned");
+  struct M {
+    const void* p;
+    int64_t ld, rowlen, rows;
+    const char* what;
+  };
+  const M mats[] = {{w->wr, w->ld_r, H, E, "wr"},
+                    {w->wg, w->ld_g, H, E * nc, "wg"},
+                    {w->wu, w->ld_u, H, E * nc, "wu"},
+                    {w->wd, w->ld_d, nc, E * H, "wd"}};
+  for (const M& m : mats) {
+    if (m.rows == 0 || m.rowlen == 0) continue;
+    if (!m.p) return fail(VT_ERR_ARG, "%s is NULL", m.what);
+    if (!aligned16(m.p)) return fail(VT_ERR_ALIGN, "%s is not 16-byte aligned", m.what);
+    if (m.ld < m.rowlen || m.ld % 8)
+      return fail(VT_ERR_ARG, "ld of %s (%lld) must be a multiple of 8 and >= %lld", m.what,
+                  static_cast<long long>(m.ld), static_cast<long long>(m.rowlen));
+    if (m.rows * m.ld * 2 >= (int64_t(1) << 31))
+      return fail(VT_ERR_UNSUPPORTED, "%s spans 2 GiB or more", m.what);
+  }
+  if ((st = check_io_vec(io->h, "h", true)) != VT_OK) return st;
+  if ((st = check_io_vec(io->peer_ffn, "peer_ffn", false)) != VT_OK) return st;
+  if ((st = check_io_vec(io->ffn_partial, "ffn_partial", true)) != VT_OK) return st;
+  if ((st = check_io_vec(io->y, "y", false)) != VT_OK) return st;
+  const MoeWs L = moe_ws_layout(*spec, top_k, n_experts);
+  if (!ws || ws_bytes < L.total) return fail(VT_ERR_WORKSPACE, "workspace %zu bytes, need %zu", ws_bytes, L.total);
+  if (!aligned16(ws)) return fail(VT_ERR_ALIGN, "workspace not 16-byte aligned");
+  DeviceInfo* di = nullptr;
+  if ((st = device_info(&di)) != VT_OK) return st;
+
+  dec::MoeParams P{};
+  P.H = static_cast<int>(H);
+  P.E = n_experts;
+  P.topk = top_k;
+  P.ncols = static_cast<int>(nc);
+  P.npe = L.npe;
+  P.m_ncols = nc > 0 ? (uint64_t(1) << 40) / static_cast<uint64_t>(nc) + 1 : 1;
+  P.eps = D.rms_eps;
+  P.g_ffn = static_cast<const uint16_t*>(w->g_ffn);
+  P.h = static_cast<const uint16_t*>(io->h);
+  P.peer_f = static_cast<const uint16_t*>(io->peer_ffn);
+  P.wr = static_cast<const uint8_t*>(w->wr);
+  P.wg = nc > 0 ? static_cast<const uint8_t*>(w->wg) : nullptr;
+  P.wu = nc > 0 ? static_cast<const uint8_t*>(w->wu) : nullptr;
+  P.wd = nc > 0 ? static_cast<const uint8_t*>(w->wd) : nullptr;
+  P.ld_r = w->ld_r * 2;
+  P.ld_g = nc > 0 ? w->ld_g * 2 : 0;
+  P.ld_u = nc > 0 ? w->ld_u * 2 : 0;
+  P.ld_d = nc > 0 ? w->ld_d * 2 : 0;
+  P.p_ffn = static_cast<uint16_t*>(io->ffn_partial);
+  P.y = static_cast<uint16_t*>(io->y);
+  char* base = static_cast<char*>(ws);
+  P.sync = reinterpret_cast<unsigned*>(base + L.sync);
+  P.logits = reinterpret_cast<float*>(base + L.logits);
+  P.m = reinterpret_cast<float*>(base + L.m);
+  P.sel_out = sel_out;
+  P.prob_out = prob_out;
+
+  const int kmax = std::max(dec::padded(P.H, dec::FMT_F16), top_k * L.npe);
+  const size_t lds = sizeof(float) * (kmax / 2 + dec::MAX_SLOTS + 16 + 2 * dec::MOE_MAX_K);
+  if (lds > di->max_lds)
+    return fail(VT_ERR_UNSUPPORTED, "shape needs %zu bytes of LDS, device has %zu", lds, di->max_lds);
+  // every workgroup resident (one per CU): grid barriers separate the phases
+  int per_cu = 0;
+  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, dec::moe_kernel, dec::NT, lds);
+  if (e != hipSuccess) return fail(VT_ERR_HIP, "occupancy query: %s", hipGetErrorString(e));
+  if (per_cu < 1) return fail(VT_ERR_UNSUPPORTED, "MoE kernel does not fit on a CU with %zu bytes of LDS", lds);
+  hipLaunchKernelGGL(dec::moe_kernel, dim3(di->cus), dim3(dec::NT), lds, static_cast<hipStream_t>(stream), P);
+  e = hipGetLastError();
+  if (e != hipSuccess) return fail(VT_ERR_HIP, "MoE launch: %s", hipGetErrorString(e));
   return VT_OK;
 }

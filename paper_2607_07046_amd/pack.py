@@ -143,3 +143,35 @@ def alloc_shard(dims: vt.vt_layer_dims, info: vt.vt_shard_info, device="cuda") -
     t = {"g_attn": e(H), "g_ffn": e(H), "wq": e(qd, H), "wk": e(kd, H), "wv": e(kd, H),
          "wo": e(H, qd), "wg": e(nc, H), "wu": e(nc, H), "wd": e(H, ld_d)}
     return ShardWeightsDev(t, struct_of(t, dims, info, ld_d))
+
+
+@dataclass
+class MoEShardDev:
+    tensors: dict
+    struct: vt.vt_moe_weights
+
+
+def pack_moe_shard(mi, c0, n_cols, device="cuda", ld_pad=0) -> MoEShardDev:
+    """One device's share of an MoE FFN (columns [c0, c0 + n_cols) of every
+    expert) laid out as vt_moe_ffn_decode takes it: wr [E][H], wg / wu
+    [E][n_cols][H + ld_pad], wd [E][H][round_up(n_cols, 8) + ld_pad]. ``mi``
+    is any object with ``g_ffn()``, ``router()`` and ``expert(name, e)``
+    returning fp16 host arrays (canonical out x in). Row padding is left as
+    zero; a caller may fill it to check that it is never used."""
+    wl = mi.wl
+    H, E = wl.hidden, wl.n_experts
+    ldg = H + ld_pad
+    ldd = max(8, round_up(n_cols, 8)) + ld_pad
+    wg = np.zeros((E, n_cols, ldg), np.float16)
+    wu = np.zeros((E, n_cols, ldg), np.float16)
+    wd = np.zeros((E, H, ldd), np.float16)
+    for e in range(E):
+        wg[e, :, :H] = mi.expert("wg", e)[c0:c0 + n_cols]
+        wu[e, :, :H] = mi.expert("wu", e)[c0:c0 + n_cols]
+        wd[e, :, :n_cols] = mi.expert("wd", e)[:, c0:c0 + n_cols]
+    t = {"g_ffn": _dev(mi.g_ffn(), device), "wr": _dev(mi.router(), device),
+         "wg": _dev(wg, device), "wu": _dev(wu, device), "wd": _dev(wd, device)}
+    p = lambda x: x.data_ptr() if x.numel() else None
+    st = vt.vt_moe_weights(g_ffn=p(t["g_ffn"]), wr=p(t["wr"]), ld_r=H, wg=p(t["wg"]), ld_g=ldg,
+                           wu=p(t["wu"]), ld_u=ldg, wd=p(t["wd"]), ld_d=ldd)
+    return MoEShardDev(t, st)

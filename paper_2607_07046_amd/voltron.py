@@ -33,7 +33,7 @@ EXPORTS = ("vt_shard_spec_create", "vt_shard_spec_query", "vt_shard_spec_destroy
            "vt_kv_append", "vt_workspace_size", "vt_layer_decode", "vt_layer_prefill_chunk",
            "vt_qplan", "vt_partial_encode", "vt_partial_decode_add",
            "vt_status_string", "vt_last_error", "vt_quantize_rows", "vt_layer_decode_q",
-           "vt_shard_pack", "vt_kv_copy_heads")
+           "vt_shard_pack", "vt_kv_copy_heads", "vt_moe_workspace_size", "vt_moe_ffn_decode")
 
 
 class VoltronError(RuntimeError):
@@ -78,6 +78,14 @@ class vt_layer_qweights(ctypes.Structure):
                 ("wq", vt_qmat), ("wk", vt_qmat), ("wv", vt_qmat), ("wo", vt_qmat),
                 ("g_ffn", ctypes.c_void_p),
                 ("wg", vt_qmat), ("wu", vt_qmat), ("wd", vt_qmat)]
+
+
+class vt_moe_weights(ctypes.Structure):
+    _fields_ = [("g_ffn", ctypes.c_void_p),
+                ("wr", ctypes.c_void_p), ("ld_r", ctypes.c_int64),
+                ("wg", ctypes.c_void_p), ("ld_g", ctypes.c_int64),
+                ("wu", ctypes.c_void_p), ("ld_u", ctypes.c_int64),
+                ("wd", ctypes.c_void_p), ("ld_d", ctypes.c_int64)]
 
 
 class vt_kv_view(ctypes.Structure):
@@ -134,10 +142,14 @@ def load_library(path=None):
                                   ctypes.POINTER(vt_layer_weights), P]
     lib.vt_kv_copy_heads.argtypes = [ctypes.POINTER(vt_kv_view), I32, ctypes.POINTER(vt_kv_view),
                                      I32, I32, I32, P]
+    lib.vt_moe_workspace_size.argtypes = [P, I32, I32, ctypes.POINTER(SZ)]
+    lib.vt_moe_ffn_decode.argtypes = [P, ctypes.POINTER(vt_moe_weights), I32, I32,
+                                      ctypes.POINTER(vt_layer_io), P, P, P, SZ, P]
     for name in ("vt_shard_spec_create", "vt_shard_spec_query", "vt_kv_append",
                  "vt_workspace_size", "vt_layer_decode", "vt_layer_prefill_chunk",
                  "vt_qplan", "vt_partial_encode", "vt_partial_decode_add",
-                 "vt_quantize_rows", "vt_layer_decode_q", "vt_shard_pack", "vt_kv_copy_heads"):
+                 "vt_quantize_rows", "vt_layer_decode_q", "vt_shard_pack", "vt_kv_copy_heads",
+                 "vt_moe_workspace_size", "vt_moe_ffn_decode"):
         getattr(lib, name).restype = ctypes.c_int
     lib.vt_status_string.argtypes = [ctypes.c_int]
     lib.vt_status_string.restype = ctypes.c_char_p
@@ -257,3 +269,16 @@ def vt_kv_copy_heads(src: vt_kv_view, src_head0, dst: vt_kv_view, dst_head0, n_h
                      stream=None):
     _check(load_library().vt_kv_copy_heads(ctypes.byref(src), src_head0, ctypes.byref(dst),
                                            dst_head0, n_heads, n_pos, stream))
+
+
+def vt_moe_workspace_size(spec: ShardSpec, n_experts, top_k) -> int:
+    n = ctypes.c_size_t(0)
+    _check(load_library().vt_moe_workspace_size(spec.handle, n_experts, top_k, ctypes.byref(n)))
+    return n.value
+
+
+def vt_moe_ffn_decode(spec: ShardSpec, w: vt_moe_weights, n_experts, top_k, io: vt_layer_io,
+                      sel_out, prob_out, ws, ws_bytes, stream=None):
+    _check(load_library().vt_moe_ffn_decode(spec.handle, ctypes.byref(w), n_experts, top_k,
+                                            ctypes.byref(io), sel_out, prob_out, ws, ws_bytes,
+                                            stream))

@@ -307,3 +307,49 @@ def test_window_validation(lib):
     assert e.value.status == vt.VT_ERR_ARG
     spec = vt.vt_shard_spec_create(vt.vt_layer_dims(window=64, **base), (1.0,), (1.0,), 0)
     assert vt.vt_shard_spec_query(spec)[0].window == 64
+
+
+def test_moe_validation_errors(lib):
+    dims = vt.vt_layer_dims(hidden=2048, n_heads=1, n_kv_heads=1, head_dim=64, ffn=1408,
+                            rms_eps=1e-5, rope_base=1e4, window=0)
+    spec = vt.vt_shard_spec_create(dims, (0.25,) * 4, (0.25,) * 4, 0)   # 352 columns
+    A = 1 << 20
+
+    def w(**over):
+        m = vt.vt_moe_weights(g_ffn=A, wr=A, ld_r=2048, wg=A, ld_g=2048, wu=A, ld_u=2048, wd=A,
+                              ld_d=352)
+        for k, v in over.items():
+            setattr(m, k, v)
+        return m
+
+    def call(m, E=60, k=4, ws_bytes=1 << 20, io=None):
+        with pytest.raises(vt.VoltronError) as e:
+            vt.vt_moe_ffn_decode(spec, m, E, k, io or _fake_io(), None, None, A, ws_bytes)
+        return e.value.status
+
+    need = vt.vt_moe_workspace_size(spec, 60, 4)
+    assert need >= 4 * (60 + 4 * 512)
+    for E, k in ((0, 1), (257, 4)):
+        with pytest.raises(vt.VoltronError) as e:
+            vt.vt_moe_workspace_size(spec, E, k)
+        assert e.value.status == vt.VT_ERR_UNSUPPORTED
+    for E, k in ((60, 0), (60, 9), (3, 4)):
+        with pytest.raises(vt.VoltronError) as e:
+            vt.vt_moe_workspace_size(spec, E, k)
+        assert e.value.status == vt.VT_ERR_ARG
+    assert call(w(), k=9) == vt.VT_ERR_ARG
+    assert call(w(wr=None)) == vt.VT_ERR_ARG
+    assert call(w(wg=A + 2)) == vt.VT_ERR_ALIGN
+    assert call(w(ld_d=344)) == vt.VT_ERR_ARG              # rows shorter than 352 columns
+    assert call(w(ld_u=2052)) == vt.VT_ERR_ARG             # not a multiple of 8
+    assert call(w(ld_g=1 << 18), E=256) == vt.VT_ERR_UNSUPPORTED   # 2 GiB or more
+    assert call(w(), ws_bytes=need - 1) == vt.VT_ERR_WORKSPACE
+    io = _fake_io()
+    io.h = None
+    assert call(w(), io=io) == vt.VT_ERR_ARG
+    big = vt.vt_shard_spec_create(vt.vt_layer_dims(hidden=512, n_heads=1, n_kv_heads=1,
+                                                   head_dim=64, ffn=40000, rms_eps=1e-5,
+                                                   rope_base=1e4, window=0), (1.0,), (1.0,), 0)
+    with pytest.raises(vt.VoltronError) as e:
+        vt.vt_moe_workspace_size(big, 8, 2)
+    assert e.value.status == vt.VT_ERR_UNSUPPORTED
