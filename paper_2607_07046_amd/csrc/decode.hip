@@ -1043,58 +1043,71 @@ struct RowsMoeDown {
 };
 
 // Every workgroup: the top_k experts and their probabilities from the E
-// logits, into LDS (sel / prob). Thread t < E ranks expert t among all E
-// (larger logit first, ties to the lower index); the top_k ranks also take
-// the softmax denominator. The logits are read back from LDS 16 at a time
-// (four 16-byte reads in flight), padded with -inf to a multiple of 16. sel
-// entries start at 0, so they name an expert whatever the logits hold.
-// ``L`` is 16-byte aligned LDS scratch of MOE_MAX_E floats. Ends with a
-// workgroup barrier.
-__device__ __forceinline__ void moe_route(const MoeParams& P, float* L, int* sel, float* prob) {
+// logits, into LDS (sel / prob). Expert t's rank is the number of experts
+// ordered before it: a larger logit, or an equal one at a lower index. With
+// key(t) = (order-preserving bits of the logit, +0 for -0) << 8 | (255 - t)
+// that is the number of larger keys, one 64-bit compare per pair. The E x E
+// compares are split over all waves (expert t % E64 on every thread, the
+// keys in E64 / (NT / E64) long runs, wave-uniform so every key read is an
+// LDS broadcast); wave 0 meanwhile takes the softmax maximum and
+// denominator. sel entries start at 0, so they name an expert whatever the
+// logits hold. ``scr`` is LDS scratch of 1536 floats, 16-byte aligned. Ends
+// with a workgroup barrier.
+__device__ __forceinline__ uint64_t route_key(float l, int t) {
+  const uint32_t b = __float_as_uint(l + 0.0f);  // -0 -> +0: equal logits, equal keys
+  const uint32_t o = (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+  return (static_cast<uint64_t>(o) << 8) | static_cast<uint64_t>(255 - t);
+}
+
+__device__ __forceinline__ void moe_route(const MoeParams& P, float* scr, int* sel, float* prob) {
+  uint64_t* key = reinterpret_cast<uint64_t*>(scr);  // [MOE_MAX_E]
+  float* lg = scr + 2 * MOE_MAX_E;                    // [MOE_MAX_E] logits, -inf past E
+  int* part = reinterpret_cast<int*>(scr + 3 * MOE_MAX_E);  // [NT] partial ranks
+  float* stat = scr + 3 * MOE_MAX_E + NT;             // max, denominator
   const int t = threadIdx.x;
-  const int e16 = (P.E + 15) & ~15;
   if (t < MOE_MAX_K) {
     sel[t] = 0;
     prob[t] = 0.f;
   }
-  if (t < e16) {
+  if (t < MOE_MAX_E) {
     const uint32_t off = static_cast<uint32_t>(t) * 4u | (static_cast<uint32_t>(t >= P.E) << 31);
     const float l = buf_ld_shared(make_rsrc(P.logits, static_cast<uint32_t>(P.E) * 4u), off);
-    L[t] = t < P.E ? l : -INFINITY;
+    lg[t] = t < P.E ? l : -INFINITY;
+    key[t] = t < P.E ? route_key(l, t) : 0ull;  // below every expert's key
+  }
+  __syncthreads();
+  const int e64 = (P.E + 63) & ~63;
+  const int np = NT / e64, run = e64 / np;
+  const int pr = t / e64, te = t - pr * e64;
+  if (pr < np) {
+    const uint64_t mine = key[te];
+    int cnt = 0;
+    const int i0 = pr * run;
+#pragma unroll 8
+    for (int i = 0; i < run; ++i) cnt += key[i0 + i] > mine ? 1 : 0;
+    part[pr * e64 + te] = cnt;
+  }
+  if (t < kWave) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < MOE_MAX_E / kWave; ++j) mx = fmaxf(mx, lg[t + kWave * j]);
+    mx = wave_max(mx);
+    float sm = 0.f;
+#pragma unroll
+    for (int j = 0; j < MOE_MAX_E / kWave; ++j) sm += __expf(lg[t + kWave * j] - mx);
+    sm = wave_sum(sm);
+    if (t == 0) {
+      stat[0] = mx;
+      stat[1] = sm;
+    }
   }
   __syncthreads();
   if (t < P.E) {
-    const float4* L4 = reinterpret_cast<const float4*>(L);
-    const float v = L[t];
-    float mx = -INFINITY;
     int rank = 0;
-    for (int i0 = 0; i0 < e16; i0 += 16) {
-      float4 q[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) q[u] = L4[i0 / 4 + u];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const float c[4] = {q[u].x, q[u].y, q[u].z, q[u].w};
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          const int i = i0 + 4 * u + w;
-          mx = fmaxf(mx, c[w]);
-          rank += (c[w] > v || (c[w] == v && i < t)) ? 1 : 0;
-        }
-      }
-    }
+    for (int q = 0; q < np; ++q) rank += part[q * e64 + t];
     if (rank < P.topk) {
-      float sum = 0.f;
-      for (int i0 = 0; i0 < e16; i0 += 16) {
-        float4 q[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) q[u] = L4[i0 / 4 + u];
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-          sum += (__expf(q[u].x - mx) + __expf(q[u].y - mx)) + (__expf(q[u].z - mx) + __expf(q[u].w - mx));
-      }
       sel[rank] = t;
-      prob[rank] = __expf(v - mx) / sum;
+      prob[rank] = __expf(lg[t] - stat[0]) / stat[1];
     }
   }
   __syncthreads();

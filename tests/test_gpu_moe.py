@@ -223,3 +223,47 @@ def test_moe_shard_without_columns():
     wg, wu, wd = oracle_shard(mi, 0, 0)
     ref = moe_ffn(mi.g_ffn(), mi.router(), wg, wu, wd, wl.rms_eps, h, wl.top_k)
     check_selection(out["sel"], ref, wl.top_k)
+
+
+class RouterOverride(CachedInputs):
+    """A small workload whose router rows are set by the test."""
+
+    def __init__(self, wl, router):
+        super().__init__(wl)
+        self._router = np.asarray(router, np.float16)
+
+    def router(self):
+        return self._router
+
+
+@pytest.mark.parametrize("k", [1, 2, 3])
+def test_moe_ties_go_to_the_lower_index(k):
+    """Equal logits (identical router rows: the same fp32 sums on the device,
+    the same fp64 sums in the oracle) are ordered by expert index."""
+    wl = small(961, 256, 8, 64, k, (1.0,))
+    base = CachedInputs(wl)
+    r = base.router().copy()
+    r[5] = r[2] = np.abs(r[2]) * np.sign(base.h(0) * base.g_ffn()).astype(np.float16)  # largest
+    mi = RouterOverride(wl, r)
+    g = GpuMoE(mi, 0)
+    out, ref = check_token(g, mi, mi.h(0))
+    assert out["sel"][0] == 2 and ref["sel"][0] == 2
+    if k >= 2:
+        assert out["sel"][1] == 5 and ref["sel"][1] == 5
+        assert out["probs"][0] == out["probs"][1]
+
+
+def test_moe_zero_logits_tie():
+    """Zero router rows give logits of exactly zero (whatever their sign
+    bit); every other expert's logit is negative, so the zero-logit experts
+    are selected lowest index first."""
+    wl = small(963, 256, 6, 64, 2, (1.0,))
+    base = CachedInputs(wl)
+    sgn = np.sign(base.h(0).astype(np.float32) * base.g_ffn().astype(np.float32))
+    r = np.tile(-0.05 * sgn, (6, 1)).astype(np.float16)
+    r[1] = 0
+    r[3] = 0
+    mi = RouterOverride(wl, r)
+    g = GpuMoE(mi, 0)
+    out, ref = check_token(g, mi, mi.h(0))
+    assert list(out["sel"]) == [1, 3] and list(ref["sel"]) == [1, 3]
