@@ -55,10 +55,14 @@ def algorithmic_bytes(dims, info, pos):
 PROFILE = os.path.join(ROOT, "profiles", "decode_kernel_7b_shard30.md")
 
 
-def kernel_source_hash():
+DECODE_SOURCES = ("decode.hip", "gemv.hpp", "device.hpp")
+MOE_SOURCES = ("moe.hip", "gemv.hpp", "device.hpp")
+
+
+def kernel_source_hash(files=DECODE_SOURCES):
     import hashlib
     h = hashlib.sha256()
-    for f in ("decode.hip", "device.hpp"):
+    for f in files:
         with open(os.path.join(ROOT, "paper_2607_07046_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

@@ -13,7 +13,7 @@ CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libvoltron.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["spec.cpp", "decode.hip", "prefill.hip", "comm.hip", "wquant.hip", "repack.hip"]
+SOURCES = ["spec.cpp", "decode.hip", "moe.hip", "prefill.hip", "comm.hip", "wquant.hip", "repack.hip"]
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-Wno-unused-command-line-argument"]
