@@ -552,6 +552,8 @@ def moe_section(steps, warmup, eager=False):
     ms = e0.elapsed_time(e1) / n
     if not torch.isfinite(p_ffn.float()).all():
         raise SystemExit("non-finite output of the MoE decode steps")
+    if ws[8192:8196].view(torch.int32).item() != 0:
+        raise SystemExit("a grid barrier's bounded wait expired during the MoE steps")
     b = moe_bytes(wl, nc)
     gbps = b / (ms * 1e-3) / 1e9
     return {"workload": wl.title, "us_per_token": round(ms * 1e3, 3),

@@ -186,7 +186,16 @@ vt_status vt_kv_append(vt_kv_view* kv, const void* k, const void* v, int32_t n_t
  * decode only) and ``max_ctx`` cached-plus-new positions. The workspace must
  * be zero-filled once before its first use; the library leaves its
  * synchronisation words zero after every call. One workspace must not be
- * used by two calls that may run at the same time. */
+ * used by two calls that may run at the same time.
+ *
+ * A persistent decode (or MoE) launch needs every one of its workgroups
+ * (one per CU) resident at once; its grid barriers wait a bounded time (about
+ * a second) and, should that ever expire (other work holding CUs), set the
+ * 32-bit error word at byte offset VT_WS_ERROR_WORD of the workspace to
+ * nonzero instead of hanging; the call's outputs are then undefined. The
+ * library never clears that word: a caller that checks it reads it after
+ * synchronising and zeroes it itself. */
+#define VT_WS_ERROR_WORD 8192
 vt_status vt_workspace_size(const vt_shard_spec* spec, int32_t max_tokens,
                             int32_t max_ctx, size_t* bytes);
 
@@ -337,7 +346,8 @@ typedef struct vt_moe_weights {
 
 /* Workspace bytes of vt_moe_ffn_decode (zero-filled once before its first
  * use; the synchronisation words are left zero after every call; not shared
- * by calls that may run at the same time). 1 <= n_experts <= 256,
+ * by calls that may run at the same time; the barrier error word at
+ * VT_WS_ERROR_WORD as for decode). 1 <= n_experts <= 256,
  * 1 <= top_k <= min(n_experts, 8), spec's n_cols < 32768. */
 vt_status vt_moe_workspace_size(const vt_shard_spec* spec, int32_t n_experts, int32_t top_k,
                                 size_t* bytes);

@@ -35,6 +35,7 @@ namespace vt {
 namespace dec {
 
 constexpr int REC = 4;           // attention partial record = head_dim + REC floats
+static_assert(SW_ERR * 4 == VT_WS_ERROR_WORD, "the error word's documented offset");
 
 enum { PH_QKV = 0, PH_ATTN = 1, PH_O = 2, PH_GATEUP = 3, PH_DOWN = 4 };
 

@@ -196,19 +196,6 @@ __device__ __forceinline__ float dot8(const u32x4 w, const u32x4 x, float acc) {
   return acc;
 }
 
-// One GEMV phase over ``units`` output units of U virtual rows of K columns.
-// A row is split into segments of 512 columns; a piece is one segment of
-// one row (64 lanes x 16 B). Wave 0 is the control wave: it holds no weight
-// loads, so it can wait at the grid barrier and stage the phase's input
-// while the other (streaming) waves' first PF loads are in flight; memory
-// ordering is in-order per wave, so a wave holding loads could not see the
-// barrier flip before they land. The workgroup's rows form a contiguous run
-// of pieces that the streaming waves split into contiguous sub-runs; each
-// streams its sub-run through a ring of PF loads, accumulates a row's
-// segments in each lane and reduces across the wave at the row's end (or
-// where its sub-run ends), writing the sum to slots[piece]. ``stage`` (run
-// by wave 0 alone) writes the input as fp16 to xs16[0, nseg*512), zero past
-// K. ``epi(unit, sums)`` gets each unit's U row sums, added in piece order.
 // q / n for 0 <= q < 2^24 / n, with rcp = floor(2^24 / n) + 1: a scalar
 // multiply and shift (exact in that range; pieces per round stay < 2^13).
 __device__ __forceinline__ int div_rcp(int q, uint32_t rcp) {
@@ -275,6 +262,19 @@ constexpr int SC_LDS_HALFS = SC_ROWS * SC_ROW_WORDS * 2 * kWave;  // 32 rows x 5
 // past its buffer, costs the memory pipeline an instruction)
 constexpr int SC_PER_WAVE = (SC_ROWS + NW - 1) / NW;
 
+// One GEMV phase over ``units`` output units of U virtual rows of K columns.
+// A row is split into segments (512 fp16, 1024 INT8 or 2048 INT4 columns);
+// a piece is one segment of one row (64 lanes x 16 B). The units are split
+// evenly over the workgroups; a workgroup's rows (in rounds of at most
+// MAX_SLOTS pieces) form one contiguous run of pieces that its eight waves
+// split into contiguous sub-runs. Each wave issues its first PRE pieces,
+// then ``stage`` runs (all threads: it waits at the grid barrier in front of
+// the phase, if any, writes the input as fp16 to xs16[0, nseg * SEGC), zero
+// past K, and ends with a workgroup barrier), then the wave streams the rest
+// of its sub-run through a ring of PF loads, accumulating a row's segments
+// in each lane and reducing across the wave at the row's end (or where its
+// sub-run ends) into slots[piece]. ``epi(unit, sums)`` gets each unit's U
+// row sums, added in piece order (a fixed order: bitwise reproducible).
 template <int U, int F, int SCW, class Rows, class Stage, class Epi>
 __device__ __forceinline__ void gemv_impl(const Rows& rows, int units, int K, const uint16_t* xs16,
                                           float* slots, uint16_t* scl, Stage stage, Epi epi) {

@@ -27,6 +27,8 @@ namespace dec {
 // from the logits) + the selected experts' gate/up GEMV | down GEMV.
 // ---------------------------------------------------------------------------
 constexpr int MOE_MAX_E = 256, MOE_MAX_K = 8;
+// (the sync words sit at the start of the workspace, as for decode)
+static_assert(SW_ERR * 4 == VT_WS_ERROR_WORD, "the error word's documented offset");
 
 struct MoeParams {
   int H, E, topk, ncols, npe;  // npe: a slot's share of the down input, whole 512-column segments

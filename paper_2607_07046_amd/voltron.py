@@ -27,6 +27,7 @@ VT_STAGED = 0x100
 
 VT_PREC_FP16, VT_PREC_INT8, VT_PREC_INT4, VT_PREC_PRUNED = 0, 1, 2, 3
 VT_W_INT8, VT_W_INT4 = 1, 2
+VT_WS_ERROR_WORD = 8192  # byte offset of the workspace's barrier error word
 
 # every symbol include/voltron.h declares
 EXPORTS = ("vt_shard_spec_create", "vt_shard_spec_query", "vt_shard_spec_destroy",

@@ -34,6 +34,14 @@ def test_exports_every_declared_symbol(lib):
         assert hasattr(lib, name), name
 
 
+def test_binding_constants_match_header():
+    with open(os.path.join(ROOT, "include", "voltron.h")) as f:
+        hdr = f.read()
+    defines = dict(re.findall(r"^#define\s+(VT_\w+)\s+(\w+)", hdr, re.M))
+    for name in ("VT_ATTN", "VT_FFN", "VT_STAGED", "VT_WS_ERROR_WORD"):
+        assert int(defines[name].rstrip("u"), 0) == getattr(vt, name), name
+
+
 def _dims(wd):
     return vt.vt_layer_dims(hidden=wd.hidden, n_heads=wd.n_heads, n_kv_heads=wd.n_kv_heads,
                             head_dim=wd.head_dim, ffn=wd.ffn, rms_eps=wd.rms_eps,
