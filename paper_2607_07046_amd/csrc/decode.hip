@@ -231,10 +231,23 @@ __device__ __forceinline__ void phase_attn(const Params& P, float* lds, bool wai
 #pragma unroll
     for (int x = 0; x < 8; ++x) R[pl * d + dc + x] = acc[x];
     __syncthreads();
-    for (int dd = t; dd < d; dd += NT) {
+    // sum of R's PPP rows in two levels over all threads: group gi of the
+    // NT / d groups adds rows gi, gi + NT / d, ... (PPP * d = 8 * NT, so 8
+    // rows each, loads independent), then d threads add the group sums (a
+    // one-thread-per-column loop over PPP rows was a chain of LDS round trips)
+    {
+      const int ng = NT / d, gi = t / d, dd = t % d;
       float a = 0.f;
-      for (int q = 0; q < PPP; ++q) a += R[q * d + dd];
-      st_shared(rec + dd, a);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) a += R[(gi + ng * i) * d + dd];
+      __syncthreads();
+      R[gi * d + dd] = a;
+      __syncthreads();
+      if (t < d) {
+        float s = 0.f;
+        for (int q = 0; q < ng; ++q) s += R[q * d + t];
+        st_shared(rec + t, s);
+      }
     }
 
     // the last chunk of head j to finish merges the head's chunks
