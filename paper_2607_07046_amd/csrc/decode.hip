@@ -332,10 +332,26 @@ template <int PH, int F>
 __device__ __forceinline__ void run_phase(const Params& P, float* lds, uint16_t* xs, float* slots,
                                           float* red, bool wait, unsigned nbar) {
   uint16_t* scl = reinterpret_cast<uint16_t*>(red + 16);  // block scales (quantised formats)
+  // The fields that describe the weight matrices are read again in each
+  // phase from the kernel-argument segment, through a pointer the compiler
+  // cannot follow from one phase to the next (scalar loads): the buffer
+  // descriptors built from them then live in scalar registers during their
+  // own phase only. Kept live across the whole launch, they overflow the
+  // scalar register file, and the spill reloads land in the weight-streaming
+  // loops.
+  typedef const __attribute__((address_space(4))) uint32_t* KernargWords;
+  KernargWords pk = (KernargWords)__builtin_amdgcn_kernarg_segment_ptr();
+  asm volatile("" : "+s"(pk));
+  static_assert(sizeof(Params) % 4 == 0, "Params is read as 32-bit words");
+  uint32_t words[sizeof(Params) / 4];
+#pragma unroll
+  for (int i = 0; i < static_cast<int>(sizeof(Params) / 4); ++i) words[i] = pk[i];
+  Params PW;
+  __builtin_memcpy(&PW, words, sizeof(Params));
   if constexpr (PH == PH_QKV) {
-    RowsQKV rows{make_mat(P.wq, P.ld_q, P.nq * P.d, P.sq, P.lds_q),
-                 make_mat(P.wk, P.ld_k, P.nkv * P.d, P.sk, P.lds_k),
-                 make_mat(P.wv, P.ld_v, P.nkv * P.d, P.sv, P.lds_v), P.nq * P.d, P.nkv * P.d};
+    RowsQKV rows{make_mat(PW.wq, PW.ld_q, PW.nq * PW.d, PW.sq, PW.lds_q),
+                 make_mat(PW.wk, PW.ld_k, PW.nkv * PW.d, PW.sk, PW.lds_k),
+                 make_mat(PW.wv, PW.ld_v, PW.nkv * PW.d, PW.sv, PW.lds_v), PW.nq * PW.d, PW.nkv * PW.d};
     gemv_phase<1, F>(
         rows, (P.nq + 2 * P.nkv) * P.d, P.H, xs, slots, scl,
         [&]() { stage_rmsnorm_h(P.x, P.g_attn, P.H, padded(P.H, F), P.eps, xs, red); },
@@ -343,7 +359,7 @@ __device__ __forceinline__ void run_phase(const Params& P, float* lds, uint16_t*
   } else if constexpr (PH == PH_ATTN) {
     phase_attn(P, lds, wait, nbar);
   } else if constexpr (PH == PH_O) {
-    RowsOne rows{make_mat(P.wo, P.ld_o, P.H, P.so, P.lds_o)};
+    RowsOne rows{make_mat(PW.wo, PW.ld_o, PW.H, PW.so, PW.lds_o)};
     const int K = P.nq * P.d;
     gemv_phase<1, F>(
         rows, P.H, K, xs, slots, scl,
@@ -359,8 +375,8 @@ __device__ __forceinline__ void run_phase(const Params& P, float* lds, uint16_t*
           st_shared(P.hbuf + r, hv);
         });
   } else if constexpr (PH == PH_GATEUP) {
-    RowsPair rows{make_mat(P.wg, P.ld_g, P.ncols, P.sg, P.lds_g),
-                  make_mat(P.wu, P.ld_u, P.ncols, P.su, P.lds_u)};
+    RowsPair rows{make_mat(PW.wg, PW.ld_g, PW.ncols, PW.sg, PW.lds_g),
+                  make_mat(PW.wu, PW.ld_u, PW.ncols, PW.su, PW.lds_u)};
     gemv_phase<2, F>(
         rows, P.ncols, P.H, xs, slots, scl,
         [&]() {
@@ -375,7 +391,7 @@ __device__ __forceinline__ void run_phase(const Params& P, float* lds, uint16_t*
           st_shared(P.m + j, gt / (1.0f + __expf(-gt)) * up);
         });
   } else {
-    RowsOne rows{make_mat(P.wd, P.ld_d, P.H, P.sd, P.lds_d)};
+    RowsOne rows{make_mat(PW.wd, PW.ld_d, PW.H, PW.sd, PW.lds_d)};
     const int K = P.ncols;
     gemv_phase<1, F>(
         rows, P.H, K, xs, slots, scl,
