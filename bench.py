@@ -16,7 +16,8 @@ reports the decode kernel against the 8 TB/s HBM peak. The ``prefill``
 section times the 256-token prefill chunk (MFMA utilisation) and the
 ``comm`` section the partial-sum transmission kernels, the ``quant`` section
 the same decode over INT8 and INT4 block-quantised weights, the ``repack``
-section the shard re-pack of an elastic re-partition. ``cpu_baseline`` is
+section the shard re-pack of an elastic re-partition, the ``stack`` section
+consecutive tokens through the 40-layer 13B-shaped stack. ``cpu_baseline`` is
 the fp64 oracle timed on the host cores on a bounded sample of the same
 workload (a reference, not the target).
 """
@@ -103,6 +104,8 @@ def parse():
                     help="timed decode steps over INT8 and INT4 weight shards (0: skip)")
     ap.add_argument("--moe-steps", type=int, default=1000,
                     help="MoE FFN shard decode steps (0: skip)")
+    ap.add_argument("--stack-tokens", type=int, default=16,
+                    help="timed tokens of the 40-layer 13B-shaped stack section (0: skip)")
     ap.add_argument("--repack-reps", type=int, default=20,
                     help="timed shard packs of the re-partition section (0: skip)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -300,6 +303,8 @@ def main():
                                      max(1, args.quant_steps // 10), layers[0][0], args.eager)
     if args.moe_steps > 0:
         out["moe"] = moe_section(args.moe_steps, max(1, args.moe_steps // 10), args.eager)
+    if args.stack_tokens > 0:
+        out["stack"] = stack_section(args.stack_tokens, 4)
     if args.cpu_seconds > 0:
         out["cpu_baseline"] = cpu_baseline(wl, pos, args.cpu_seconds, step_bytes)
     print(json.dumps(out), flush=True)
@@ -477,6 +482,112 @@ def moe_bytes(wl, n_cols):
     shard, the gain, h in, the partial and y out."""
     H, E, k = wl.hidden, wl.n_experts, wl.top_k
     return 2 * (E * H + k * 3 * n_cols * H + 4 * H)
+
+
+def stack_section(tokens, warmup):
+    """The 13B-shaped 40-layer stack, 40% shard (16 of 40 heads, 5530 of
+    13824 FFN columns): consecutive tokens from position 2048, each token
+    one fused decode launch per layer, layer l's y the input x of layer l+1
+    (the other devices' partials taken as zero), every layer appending to
+    its own KV cache. The 40 layers' shard weights (10.2 GB) are drawn on
+    the device from a seeded generator with the workload's distributions
+    (weights N(0, 0.02), gains 1 + N(0, 0.1), cached K/V and token inputs
+    N(0, 1)); the stack's parity against the oracle chain is a test, this
+    section only times it. Tokens are enqueued eagerly (40 launches each)."""
+    import torch
+
+    from paper_2607_07046_amd import pack
+    from paper_2607_07046_amd import voltron as vt
+    from synth import get
+
+    wl = get("13b_stack")
+    wd = wl.dims
+    dims = vt.vt_layer_dims(hidden=wd.hidden, n_heads=wd.n_heads, n_kv_heads=wd.n_kv_heads,
+                            head_dim=wd.head_dim, ffn=wd.ffn, rms_eps=wd.rms_eps,
+                            rope_base=wd.rope_base, window=wd.window)
+    spec = vt.vt_shard_spec_create(dims, wl.fracs, wl.fracs, wl.device)
+    dims, info = vt.vt_shard_spec_query(spec)
+    H, d, nkv, nq, F = dims.hidden, dims.head_dim, info.n_kv_heads, info.n_q_heads, info.n_cols
+    ntok = warmup + tokens
+    cap = wl.ctx + ntok
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(7046 * 1000 + wl.seed_id)
+
+    def normal(shape, sigma, mean=0.0):
+        t = torch.empty(shape, dtype=torch.float32, device="cuda")
+        t.normal_(mean, sigma, generator=gen)
+        return t.half()
+
+    ld_d = max(8, pack.round_up(F, 8))
+    layers = []
+    t0 = time.time()
+    for _ in range(wl.n_layers):
+        t = {"g_attn": normal((H,), 0.1, 1.0), "g_ffn": normal((H,), 0.1, 1.0),
+             "wq": normal((nq * d, H), wl.weight_sigma), "wk": normal((nkv * d, H), wl.weight_sigma),
+             "wv": normal((nkv * d, H), wl.weight_sigma), "wo": normal((H, nq * d), wl.weight_sigma),
+             "wg": normal((F, H), wl.weight_sigma), "wu": normal((F, H), wl.weight_sigma)}
+        wdn = torch.zeros((H, ld_d), dtype=torch.float16, device="cuda")
+        wdn[:, :F] = normal((H, F), wl.weight_sigma)
+        t["wd"] = wdn
+        kc = torch.zeros((nkv, cap, d), dtype=torch.float16, device="cuda")
+        vc = torch.zeros_like(kc)
+        kc[:, :wl.ctx] = normal((nkv, wl.ctx, d), 1.0)
+        vc[:, :wl.ctx] = normal((nkv, wl.ctx, d), 1.0)
+        kv = vt.vt_kv_view(k=kc.data_ptr(), v=vc.data_ptr(), capacity=cap, n_kv_heads=nkv,
+                           head_dim=d, len=wl.ctx)
+        layers.append((t, pack.struct_of(t, dims, info, ld_d), kc, vc, kv))
+    xs = normal((ntok, H), 1.0)
+    ws_bytes = vt.vt_workspace_size(spec, 1, cap)
+    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device="cuda")
+    bufs = [torch.empty(H, dtype=torch.float16, device="cuda") for _ in range(2)]
+    p_attn, h, p_ffn = (torch.empty(H, dtype=torch.float16, device="cuda") for _ in range(3))
+    torch.cuda.synchronize()
+    setup_s = time.time() - t0
+    both = vt.VT_ATTN | vt.VT_FFN
+    s = torch.cuda.current_stream().cuda_stream
+
+    def token(tk):
+        pos = wl.ctx + tk
+        for li, (_, st, _, _, kv) in enumerate(layers):
+            x = xs[tk] if li == 0 else bufs[li % 2]
+            io = vt.vt_layer_io(x=x.data_ptr(), peer_attn=None, peer_ffn=None,
+                                attn_partial=p_attn.data_ptr(), h=h.data_ptr(),
+                                ffn_partial=p_ffn.data_ptr(), y=bufs[(li + 1) % 2].data_ptr())
+            vt.vt_layer_decode(spec, st, kv, io, pos, both, ws.data_ptr(), ws_bytes, s)
+
+    for tk in range(warmup):
+        token(tk)
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for tk in range(warmup, ntok):
+        token(tk)
+    end.record()
+    torch.cuda.synchronize()
+    ms_tok = start.elapsed_time(end) / tokens
+    err = int(ws[vt.VT_WS_ERROR_WORD:vt.VT_WS_ERROR_WORD + 4].view(torch.int32).item())
+    if err:
+        raise SystemExit("stack section: a decode wait expired (error word set)")
+    if not torch.isfinite(bufs[wl.n_layers % 2].float()).all():
+        raise SystemExit("stack section: non-finite output")
+    if any(kv.len != cap for (_, _, _, _, kv) in layers):
+        raise SystemExit("stack section: a layer's KV length did not advance once per token")
+    tok_bytes = sum(algorithmic_bytes(dims, info, wl.ctx + tk) for tk in range(warmup, ntok)) \
+        * wl.n_layers / tokens
+    gbps = tok_bytes / (ms_tok * 1e-3) / 1e9
+    return {
+        "workload": "13b_stack",
+        "shape": f"40 layers, hidden {H}, {nq} q / {nkv} kv heads, {F} FFN cols (40% shard)",
+        "positions": f"{wl.ctx + warmup}..{wl.ctx + ntok - 1} timed ({warmup} warm-up tokens before)",
+        "ms_per_token": round(ms_tok, 4),
+        "tokens_s": round(1e3 / ms_tok, 1),
+        "us_per_layer": round(ms_tok * 1e3 / wl.n_layers, 2),
+        "bytes_per_token": int(tok_bytes),
+        "hbm_GBps": round(gbps, 1),
+        "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
+        "launch": "one persistent launch per layer, eager",
+        "setup_s": round(setup_s, 1),
+    }
 
 
 def moe_section(steps, warmup, eager=False):
