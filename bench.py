@@ -104,6 +104,9 @@ def parse():
                     help="timed decode steps over INT8 and INT4 weight shards (0: skip)")
     ap.add_argument("--moe-steps", type=int, default=1000,
                     help="MoE FFN shard decode steps (0: skip)")
+    ap.add_argument("--fraction-sweep", action="store_true",
+                    help="also time the decode step of 7B- and 70B-shaped shards from 10%% to 100%% "
+                         "of the layer and fit time = fixed + bytes / bandwidth (about a minute)")
     ap.add_argument("--stack-tokens", type=int, default=16,
                     help="timed tokens of the 40-layer 13B-shaped stack section (0: skip)")
     ap.add_argument("--repack-reps", type=int, default=20,
@@ -305,6 +308,8 @@ def main():
         out["moe"] = moe_section(args.moe_steps, max(1, args.moe_steps // 10), args.eager)
     if args.stack_tokens > 0:
         out["stack"] = stack_section(args.stack_tokens, 4)
+    if args.fraction_sweep:
+        out["fraction_sweep"] = fraction_sweep_section()
     if args.cpu_seconds > 0:
         out["cpu_baseline"] = cpu_baseline(wl, pos, args.cpu_seconds, step_bytes)
     print(json.dumps(out), flush=True)
@@ -482,6 +487,112 @@ def moe_bytes(wl, n_cols):
     shard, the gain, h in, the partial and y out."""
     H, E, k = wl.hidden, wl.n_experts, wl.top_k
     return 2 * (E * H + k * 3 * n_cols * H + 4 * H)
+
+
+def _shard_step_us(H, nh, nkv, d, F, frac, pos, sigma):
+    """Time of one fused decode step of device 0's share (fraction ``frac``
+    of heads and FFN columns; the whole layer at 1.0) of a Llama-shaped
+    layer at position ``pos``: weights drawn on the device (seeded), enough
+    copies for 768 MB rotated, HIP-graph replays. Returns (info, bytes, us)."""
+    import torch
+
+    from paper_2607_07046_amd import pack
+    from paper_2607_07046_amd import voltron as vt
+
+    dims = vt.vt_layer_dims(hidden=H, n_heads=nh, n_kv_heads=nkv, head_dim=d, ffn=F, rms_eps=1e-5,
+                            rope_base=10000.0, window=0)
+    fr = [1.0] if frac >= 1.0 else [frac, 1.0 - frac]
+    spec = vt.vt_shard_spec_create(dims, fr, fr, 0)
+    dims, info = vt.vt_shard_spec_query(spec)
+    nq, nk, nc = info.n_q_heads, info.n_kv_heads, info.n_cols
+    step = algorithmic_bytes(dims, info, pos)
+    copies = max(2, math.ceil(MALL_DEFEAT_BYTES / step))
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(7046)
+
+    def normal(shape, sd, mean=0.0):
+        t = torch.empty(shape, dtype=torch.float32, device="cuda")
+        t.normal_(mean, sd, generator=gen)
+        return t.half()
+
+    ld_d = max(8, pack.round_up(nc, 8))
+    cap = pos + 1
+    layers = []
+    for _ in range(copies):
+        t = {"g_attn": normal((H,), 0.1, 1.0), "g_ffn": normal((H,), 0.1, 1.0),
+             "wq": normal((nq * d, H), sigma), "wk": normal((nk * d, H), sigma),
+             "wv": normal((nk * d, H), sigma), "wo": normal((H, nq * d), sigma),
+             "wg": normal((nc, H), sigma), "wu": normal((nc, H), sigma)}
+        wdn = torch.zeros((H, ld_d), dtype=torch.float16, device="cuda")
+        wdn[:, :nc] = normal((H, nc), sigma)
+        t["wd"] = wdn
+        kc, vc = normal((nk, cap, d), 1.0), normal((nk, cap, d), 1.0)
+        kv = vt.vt_kv_view(k=kc.data_ptr(), v=vc.data_ptr(), capacity=cap, n_kv_heads=nk,
+                           head_dim=d, len=pos)
+        layers.append((t, pack.struct_of(t, dims, info, ld_d), kc, vc, kv))
+    ws_bytes = vt.vt_workspace_size(spec, 1, cap)
+    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device="cuda")
+    bufs = [normal((H,), 1.0), torch.empty(H, dtype=torch.float16, device="cuda")]
+    pa, h, pf = (torch.empty(H, dtype=torch.float16, device="cuda") for _ in range(3))
+
+    def enqueue(i, stream):
+        _, st, _, _, kv = layers[i % copies]
+        kv.len = pos
+        io = vt.vt_layer_io(x=bufs[i % 2].data_ptr(), peer_attn=None, peer_ffn=None,
+                            attn_partial=pa.data_ptr(), h=h.data_ptr(), ffn_partial=pf.data_ptr(),
+                            y=bufs[(i + 1) % 2].data_ptr())
+        vt.vt_layer_decode(spec, st, kv, io, pos, vt.VT_ATTN | vt.VT_FFN, ws.data_ptr(), ws_bytes,
+                           stream)
+
+    n = copies * 2 * max(1, 64 // (copies * 2))
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        s = torch.cuda.current_stream().cuda_stream
+        for i in range(n):
+            enqueue(i, s)
+    for _ in range(3):
+        graph.replay()
+    torch.cuda.synchronize()
+    reps = max(3, 400 // n)
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(reps):
+        graph.replay()
+    end.record()
+    torch.cuda.synchronize()
+    us = start.elapsed_time(end) * 1e3 / (reps * n)
+    if not torch.isfinite(bufs[0].float()).all():
+        raise SystemExit("fraction sweep: non-finite output")
+    del layers, graph
+    torch.cuda.empty_cache()
+    return info, step, us
+
+
+def fraction_sweep_section():
+    """The fused decode step of the 7B-shaped layer (position 1024) and the
+    70B-shaped GQA layer (position 4096) at shard fractions from 10% to the
+    whole layer, and a least-squares line time = fixed + bytes / bandwidth
+    per layer shape: the bandwidth is what the weight streaming reaches, the
+    fixed part is the step's dependency chain (barriers, staging,
+    attention), which does not grow with the shard."""
+    out = {}
+    for name, shape, fracs in (("7b", (4096, 32, 32, 128, 11008, 1024, 0.02), (0.1, 0.2, 0.3, 0.5, 0.75, 1.0)),
+                               ("70b_gqa", (8192, 64, 8, 128, 28672, 4096, 0.015), (0.125, 0.25, 0.5, 1.0))):
+        H, nh, nkv, d, F, pos, sigma = shape
+        rows = []
+        for f in fracs:
+            info, step, us = _shard_step_us(H, nh, nkv, d, F, f, pos, sigma)
+            rows.append({"fraction": f, "q_heads": info.n_q_heads, "kv_heads": info.n_kv_heads,
+                         "cols": info.n_cols, "bytes": int(step), "us_per_step": round(us, 2),
+                         "GBps": round(step / us / 1e3, 1),
+                         "hbm_frac": round(step / us / 1e3 / HBM_PEAK_GBPS, 4)})
+        xb = np.array([r["bytes"] for r in rows], np.float64)
+        yt = np.array([r["us_per_step"] for r in rows], np.float64)
+        slope, icept = np.polyfit(xb, yt, 1)
+        out[name] = {"rows": rows, "fit_fixed_us": round(float(icept), 2),
+                     "fit_stream_GBps": round(float(1e-3 / slope), 1),
+                     "fit_stream_frac": round(float(1e-3 / slope) / HBM_PEAK_GBPS, 4)}
+    return out
 
 
 def stack_section(tokens, warmup):
