@@ -232,16 +232,26 @@ def main():
             use_graph = False
             torch.cuda.synchronize()
 
+    # The timed steps run as up to 20 back-to-back windows, each bracketed by
+    # events (no synchronisation between them), for a distribution of the
+    # per-step time besides the mean; every window size is run once in the
+    # warm-up so that no graph is captured inside the timed region.
+    nwin = max(1, min(20, args.steps))
+    wins = [args.steps // nwin + (1 if w < args.steps % nwin else 0) for w in range(nwin)]
     run(args.warmup)
+    for n in sorted(set(wins)):
+        run(n)
     torch.cuda.synchronize()
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(nwin + 1)]
     torch.cuda.synchronize()
-    start.record()
-    run(args.steps)
-    end.record()
+    evs[0].record()
+    for w, n in enumerate(wins):
+        run(n)
+        evs[w + 1].record()
     torch.cuda.synchronize()
-    ms = start.elapsed_time(end)
+    ms = evs[0].elapsed_time(evs[-1])
     ms_step = ms / args.steps
+    win_ms = np.array([evs[w].elapsed_time(evs[w + 1]) / wins[w] for w in range(nwin)])
     err_words = ws[:4 * (3072 + 32 * (info.n_q_heads + 1))].view(torch.int32).cpu().numpy()
     if np.any(err_words):
         raise SystemExit(f"decode kernel left synchronisation words set: {err_words[:4]}")
@@ -259,6 +269,9 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 6),
+        "ms_per_step_windows": {"windows": nwin, "p10": round(float(np.percentile(win_ms, 10)), 6),
+                                "median": round(float(np.median(win_ms)), 6),
+                                "p90": round(float(np.percentile(win_ms, 90)), 6)},
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
