@@ -338,7 +338,8 @@ __device__ __forceinline__ void run_phase(const Params& P, float* lds, uint16_t*
   // descriptors built from them then live in scalar registers during their
   // own phase only. Kept live across the whole launch, they overflow the
   // scalar register file, and the spill reloads land in the weight-streaming
-  // loops.
+  // loops. The parameters are the kernel's only argument, so they start at
+  // byte 0 of the segment.
   typedef const __attribute__((address_space(4))) uint32_t* KernargWords;
   KernargWords pk = (KernargWords)__builtin_amdgcn_kernarg_segment_ptr();
   asm volatile("" : "+s"(pk));
@@ -421,7 +422,9 @@ __device__ __forceinline__ void run_phases(const Params& P, float* lds, uint16_t
 }
 
 // Phases PB..PE of one decode step. PB < PE needs every workgroup resident
-// (one per CU): grid barriers separate the phases.
+// (one per CU): grid barriers separate the phases. Params must stay the only
+// kernel argument (run_phase reads it from the start of the argument
+// segment).
 template <int PB, int PE, int F>
 __global__ void __launch_bounds__(NT) decode_kernel(Params P) {
   extern __shared__ float lds[];
