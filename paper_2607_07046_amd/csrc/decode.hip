@@ -108,8 +108,18 @@ __device__ __forceinline__ void phase_attn(const Params& P, float* lds, bool wai
   int* flag = reinterpret_cast<int*>(W + 2 * P.nchunk);
   const rsrc_t rk = make_rsrc(P.kc, P.kv_bytes), rv = make_rsrc(P.vc, P.kv_bytes);
 
+  // rotation of pair t at the new position (independent of phase 0; the
+  // same for every item)
+  const int half = d / 2;
+  float c0 = 1.f, s0 = 0.f;
+  if (t < half) rope_angle(P.pos, t, d, P.rope_base, c0, s0);
+
   bool waited = false;
   for (int id = blockIdx.x;; id += gridDim.x) {
+    // past the first item, leave as soon as none is left (the next item's
+    // prologue would only delay this workgroup's arrival at the barrier,
+    // and the last merges are on the step's critical path)
+    if (waited && id >= ids) break;
     const int r8 = id % 8;
     const int jj = (id / 8) % G;
     const int u = (id / (8 * G)) * 8 + r8;
@@ -130,10 +140,6 @@ __device__ __forceinline__ void phase_attn(const Params& P, float* lds, bool wai
         vr[ps] = buf_load16(rv, off);
       }
     }
-    // rotation of pair t at the new position (independent of phase 0)
-    const int half = d / 2;
-    float c0 = 1.f, s0 = 0.f;
-    if (t < half) rope_angle(P.pos, t, d, P.rope_base, c0, s0);
     if (!waited) {
       if (wait) grid_wait(P.sync, nbar);
       waited = true;
