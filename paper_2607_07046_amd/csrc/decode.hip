@@ -366,9 +366,22 @@ __device__ __forceinline__ void run_phase(const Params& P, float* lds, uint16_t*
     RowsQKV rows{make_mat(PW.wq, PW.ld_q, PW.nq * PW.d, PW.sq, PW.lds_q),
                  make_mat(PW.wk, PW.ld_k, PW.nkv * PW.d, PW.sk, PW.lds_k),
                  make_mat(PW.wv, PW.ld_v, PW.nkv * PW.d, PW.sv, PW.lds_v), PW.nq * PW.d, PW.nkv * PW.d};
+    // x and the gains depend on nothing in this launch: their loads go out
+    // ahead of the first weight pieces instead of queueing behind them
+    // (fp16 7B shard 47.6 -> 47.4 us, 70B 108.1 -> 106.4, INT4 40.9 -> 39.7;
+    // INT8, whose scale rows also load up front, measured 43.7 -> 44.1 and
+    // keeps them behind)
+    constexpr bool kEarlyX = F != FMT_Q8;
+    RmsInH<4> xin;
     gemv_phase<1, F>(
         rows, (P.nq + 2 * P.nkv) * P.d, P.H, xs, slots, scl,
-        [&]() { stage_rmsnorm_h(P.x, P.g_attn, P.H, padded(P.H, F), P.eps, xs, red); },
+        [&]() {
+          if constexpr (kEarlyX) xin.load(P.x, P.g_attn, P.H);
+        },
+        [&]() {
+          if constexpr (!kEarlyX) xin.load(P.x, P.g_attn, P.H);
+          xin.finish(P.H, padded(P.H, F), P.eps, xs, red);
+        },
         [&](int r, const float* v) { st_shared(P.qkv + r, v[0]); });
   } else if constexpr (PH == PH_ATTN) {
     phase_attn(P, lds, wait, nbar);

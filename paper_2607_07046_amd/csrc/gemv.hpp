@@ -267,17 +267,18 @@ constexpr int SC_PER_WAVE = (SC_ROWS + NW - 1) / NW;
 // a piece is one segment of one row (64 lanes x 16 B). The units are split
 // evenly over the workgroups; a workgroup's rows (in rounds of at most
 // MAX_SLOTS pieces) form one contiguous run of pieces that its eight waves
-// split into contiguous sub-runs. Each wave issues its first PRE pieces,
-// then ``stage`` runs (all threads: it waits at the grid barrier in front of
+// split into contiguous sub-runs. ``pre`` runs first (all threads; loads
+// issued there leave ahead of every weight piece), each wave issues its
+// first PRE pieces, then ``stage`` runs (all threads: it waits at the grid barrier in front of
 // the phase, if any, writes the input as fp16 to xs16[0, nseg * SEGC), zero
 // past K, and ends with a workgroup barrier), then the wave streams the rest
 // of its sub-run through a ring of PF loads, accumulating a row's segments
 // in each lane and reducing across the wave at the row's end (or where its
 // sub-run ends) into slots[piece]. ``epi(unit, sums)`` gets each unit's U
 // row sums, added in piece order (a fixed order: bitwise reproducible).
-template <int U, int F, int SCW, class Rows, class Stage, class Epi>
+template <int U, int F, int SCW, class Rows, class Pre, class Stage, class Epi>
 __device__ __forceinline__ void gemv_impl(const Rows& rows, int units, int K, const uint16_t* xs16,
-                                          float* slots, uint16_t* scl, Stage stage, Epi epi) {
+                                          float* slots, uint16_t* scl, Pre pre, Stage stage, Epi epi) {
   constexpr int EPL = Fmt<F>::EPL, SEGC = Fmt<F>::SEGC;
   constexpr bool QUANT = F != FMT_F16;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
@@ -311,6 +312,7 @@ __device__ __forceinline__ void gemv_impl(const Rows& rows, int units, int K, co
     const uint32_t oob = static_cast<uint32_t>(!ok) << 31;
     return __builtin_amdgcn_raw_buffer_load_b128(ra.rs, (base + lane16) | oob, 0, 0);
   };
+  pre();
   bool staged = false;
   int ua = u0;
   do {
@@ -439,20 +441,26 @@ __device__ __forceinline__ void gemv_impl(const Rows& rows, int units, int K, co
   } while (ua < u1);
 }
 
-template <int U, int F, class Rows, class Stage, class Epi>
+template <int U, int F, class Rows, class Pre, class Stage, class Epi>
 __device__ __forceinline__ void gemv_phase(const Rows& rows, int units, int K, const uint16_t* xs16,
-                                           float* slots, uint16_t* scl, Stage stage, Epi epi) {
+                                           float* slots, uint16_t* scl, Pre pre, Stage stage, Epi epi) {
   if constexpr (F == FMT_F16) {
-    gemv_impl<U, F, 1>(rows, units, K, xs16, slots, scl, stage, epi);
+    gemv_impl<U, F, 1>(rows, units, K, xs16, slots, scl, pre, stage, epi);
   } else {
     const int words = ((K + 31) / 32 + 2 * kWave - 1) / (2 * kWave);  // per lane and scale row
     if (words <= 1)
-      gemv_impl<U, F, 1>(rows, units, K, xs16, slots, scl, stage, epi);
+      gemv_impl<U, F, 1>(rows, units, K, xs16, slots, scl, pre, stage, epi);
     else if (words <= 2)
-      gemv_impl<U, F, 2>(rows, units, K, xs16, slots, scl, stage, epi);
+      gemv_impl<U, F, 2>(rows, units, K, xs16, slots, scl, pre, stage, epi);
     else
-      gemv_impl<U, F, SC_ROW_WORDS>(rows, units, K, xs16, slots, scl, stage, epi);
+      gemv_impl<U, F, SC_ROW_WORDS>(rows, units, K, xs16, slots, scl, pre, stage, epi);
   }
+}
+
+template <int U, int F, class Rows, class Stage, class Epi>
+__device__ __forceinline__ void gemv_phase(const Rows& rows, int units, int K, const uint16_t* xs16,
+                                           float* slots, uint16_t* scl, Stage stage, Epi epi) {
+  gemv_phase<U, F>(rows, units, K, xs16, slots, scl, []() {}, stage, epi);
 }
 
 // ---------------------------------------------------------------------------
@@ -463,41 +471,54 @@ __device__ __forceinline__ void gemv_phase(const Rows& rows, int units, int K, c
 // caller-provided fp16 vector v (n a multiple of 8, n <= 8 * 4 * NT); zero
 // for n <= k < npad.
 template <int MAXC>
-__device__ __forceinline__ void stage_rmsnorm_h_impl(const uint16_t* v, const uint16_t* g, int n, int npad,
-                                                     float eps, uint16_t* xs, float* red) {
-  const int nch = n / 8;
-  const rsrc_t rv = make_rsrc(v, static_cast<uint32_t>(n) * 2u);
-  const rsrc_t rg = make_rsrc(g, static_cast<uint32_t>(n) * 2u);
+struct RmsInH {
   u32x4 xv[MAXC], gv[MAXC];
+  // the loads (chunks past n read as zero)
+  __device__ __forceinline__ void load(const uint16_t* v, const uint16_t* g, int n) {
+    const rsrc_t rv = make_rsrc(v, static_cast<uint32_t>(n) * 2u);
+    const rsrc_t rg = make_rsrc(g, static_cast<uint32_t>(n) * 2u);
 #pragma unroll
-  for (int c = 0; c < MAXC; ++c) {  // chunks past n read as zero
-    const uint32_t off = static_cast<uint32_t>(threadIdx.x + c * NT) * 16u;
-    xv[c] = buf_load16(rv, off);
-    gv[c] = buf_load16(rg, off);
-  }
-  float ss = 0.f;
-#pragma unroll
-  for (int c = 0; c < MAXC; ++c) {
-    float f[8];
-    unpack8(xv[c], f);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) ss = fmaf(f[e], f[e], ss);
-  }
-  ss = block_sum<NT>(ss, red);
-  const float rstd = 1.0f / sqrtf(ss / static_cast<float>(n) + eps);
-#pragma unroll
-  for (int c = 0; c < MAXC; ++c) {
-    const int k8 = threadIdx.x + c * NT;
-    if (k8 < nch) {
-      float f[8], gf[8];
-      unpack8(xv[c], f);
-      unpack8(gv[c], gf);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) xs[k8 * 8 + e] = f2h(f[e] * rstd * gf[e]);
+    for (int c = 0; c < MAXC; ++c) {
+      const uint32_t off = static_cast<uint32_t>(threadIdx.x + c * NT) * 16u;
+      xv[c] = buf_load16(rv, off);
+      gv[c] = buf_load16(rg, off);
     }
   }
-  for (int k = n + threadIdx.x; k < npad; k += NT) xs[k] = 0;
-  __syncthreads();
+  // the norm and the fp16 writes to LDS
+  __device__ __forceinline__ void finish(int n, int npad, float eps, uint16_t* xs, float* red) const {
+    const int nch = n / 8;
+    float ss = 0.f;
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c) {
+      float f[8];
+      unpack8(xv[c], f);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ss = fmaf(f[e], f[e], ss);
+    }
+    ss = block_sum<NT>(ss, red);
+    const float rstd = 1.0f / sqrtf(ss / static_cast<float>(n) + eps);
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c) {
+      const int k8 = threadIdx.x + c * NT;
+      if (k8 < nch) {
+        float f[8], gf[8];
+        unpack8(xv[c], f);
+        unpack8(gv[c], gf);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) xs[k8 * 8 + e] = f2h(f[e] * rstd * gf[e]);
+      }
+    }
+    for (int k = n + threadIdx.x; k < npad; k += NT) xs[k] = 0;
+    __syncthreads();
+  }
+};
+
+template <int MAXC>
+__device__ __forceinline__ void stage_rmsnorm_h_impl(const uint16_t* v, const uint16_t* g, int n, int npad,
+                                                     float eps, uint16_t* xs, float* red) {
+  RmsInH<MAXC> r;
+  r.load(v, g, n);
+  r.finish(n, npad, eps, xs, red);
 }
 
 // The same for an fp32 vector written by other workgroups of this launch
