@@ -204,10 +204,13 @@ __global__ void __launch_bounds__(NT) moe_kernel(MoeParams P) {
   int* sel = reinterpret_cast<int*>(red + 16);
   float* prob = reinterpret_cast<float*>(sel + MOE_MAX_K);
 
-  // router logits (xs keeps w for the gate/up phase)
+  // router logits (xs keeps w for the gate/up phase); h and the gains
+  // depend on nothing in this launch, so their loads leave first
+  RmsInH<4> hin;
   gemv_phase<1, FMT_F16>(
       RowsOne{make_mat(P.wr, P.ld_r, P.E, nullptr, 0)}, P.E, P.H, xs, slots, nullptr,
-      [&]() { stage_rmsnorm_h(P.h, P.g_ffn, P.H, padded(P.H, FMT_F16), P.eps, xs, red); },
+      [&]() { hin.load(P.h, P.g_ffn, P.H); },
+      [&]() { hin.finish(P.H, padded(P.H, FMT_F16), P.eps, xs, red); },
       [&](int e, const float* v) { st_shared(P.logits + e, v[0]); });
   grid_arrive(P.sync);
   grid_wait(P.sync, 1);
