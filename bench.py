@@ -1,25 +1,28 @@
 """Decode-layer-shard throughput on one MI355X.
 
-A step is one batch-1 decode of the shard through the whole hot path
-(RMSNorm, QKV, RoPE, KV append, attention, O, residual, RMSNorm, gate/up,
-SiLU-gate, down, residual) via vt_layer_decode. The workload is the 30%
-shard (10 of 32 heads, 3302 of 11008 FFN columns) of the 7B-shaped layer
-decoding at position 1024. To keep the 256 MB Infinity Cache from serving
-the weights, the bench holds R distinct weight/KV copies (>= 768 MB in all)
-and step i runs copy i mod R; step i+1 takes step i's output y as its input,
-so steps form a dependent chain like a stack of layers. Each step re-decodes
-position 1024 of its copy. Inputs are resident in HBM before timing starts.
+A step is one batch-1 decode token through the whole hot path (RMSNorm,
+QKV, RoPE, KV append, attention, O, residual, RMSNorm, gate/up, SiLU-gate,
+down, residual). The headline workload is the largest single-GPU one: the
+13B-shaped 40-layer stack, 40% shard (16 of 40 heads, 5530 of 13824 FFN
+columns), consecutive tokens from position 2048, each token through all 40
+layers in one vt_stack_decode launch (layer l's y is layer l+1's x), every
+layer appending to its own KV cache. Its 10.8 GB of weights per token
+stream from HBM (far past the 256 MB Infinity Cache). Inputs are resident
+in HBM before timing starts.
 
-Prints one JSON line. ``value`` is tokens/s (steps per second), the HBM
-figure is algorithmic bytes per step / time per step, and ``roofline``
-reports the decode kernel against the 8 TB/s HBM peak. The ``prefill``
-section times the 256-token prefill chunk (MFMA utilisation) and the
-``comm`` section the partial-sum transmission kernels, the ``quant`` section
-the same decode over INT8 and INT4 block-quantised weights, the ``repack``
-section the shard re-pack of an elastic re-partition, the ``stack`` section
-consecutive tokens through the 40-layer 13B-shaped stack. ``cpu_baseline`` is
-the fp64 oracle timed on the host cores on a bounded sample of the same
-workload (a reference, not the target).
+Prints one JSON line. ``value`` is tokens/s; the HBM figure is algorithmic
+bytes per token / time per token; ``roofline`` reports the stack launch (one
+per token) against the 8 TB/s HBM peak. Sections: ``decode_7b`` and
+``decode_70b_gqa`` time single-layer shards (the 7B-shaped 30% shard at
+position 1024 and the 70B-shaped GQA 25% shard at position 4096) with
+rotated weight/KV copies (>= 768 MB) and the y -> x chain, each with its own
+roofline block; ``per_layer_launches`` the same stack with one launch per
+layer; ``prefill`` the 256-token prefill chunk (MFMA utilisation); ``comm``
+the partial-sum transmission kernels; ``quant`` the 7B decode over INT8 and
+INT4 block-quantised weights; ``repack`` the shard re-pack of an elastic
+re-partition; ``moe`` the MoE FFN shard. ``cpu_baseline`` is the fp64
+oracle timed on the host cores on a bounded sample of the headline workload
+(a reference, not the target).
 """
 import argparse
 import json
@@ -53,11 +56,10 @@ def algorithmic_bytes(dims, info, pos):
     return weights + kv + vectors
 
 
-PROFILE = os.path.join(ROOT, "profiles", "decode_kernel_7b_shard30.md")
-
-
 DECODE_SOURCES = ("decode.hip", "gemv.hpp", "device.hpp")
 MOE_SOURCES = ("moe.hip", "gemv.hpp", "device.hpp")
+PROFILES = {"13b_stack": "decode_kernel_13b_stack40.md", "7b": "decode_kernel_7b_shard30.md",
+            "70b_gqa": "decode_kernel_70b_gqa_shard25.md"}
 
 
 def kernel_source_hash(files=DECODE_SOURCES):
@@ -69,14 +71,15 @@ def kernel_source_hash(files=DECODE_SOURCES):
     return h.hexdigest()[:16]
 
 
-def measured_traffic():
-    """HBM bytes per launch from the committed rocprofv3 counter summary, or
-    None if the kernel sources changed since the counters were taken."""
+def measured_traffic(workload):
+    """HBM bytes per launch from the committed rocprofv3 counter summary of
+    the workload, or None if there is none or the kernel sources changed
+    since the counters were taken."""
     import re
     try:
-        with open(PROFILE) as f:
+        with open(os.path.join(ROOT, "profiles", PROFILES[workload])) as f:
             txt = f.read()
-    except OSError:
+    except (OSError, KeyError):
         return None
     m_hash = re.search(r"first 16 hex\): `([0-9a-f]{16})`", txt)
     m_traffic = re.search(r"\*\*([0-9,]+) B\*\*", txt)
@@ -88,12 +91,15 @@ def measured_traffic():
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=2000)
-    ap.add_argument("--warmup", type=int, default=200)
-    ap.add_argument("--config", default="7b", help="decode workload key (synth.configs)")
-    ap.add_argument("--copies", type=int, default=0, help="weight copies (0: enough for 768 MB)")
-    ap.add_argument("--staged", action="store_true", help="one launch per stage")
-    ap.add_argument("--eager", action="store_true", help="no HIP graph")
+    ap.add_argument("--steps", type=int, default=60, help="timed tokens of the headline")
+    ap.add_argument("--warmup", type=int, default=6)
+    ap.add_argument("--config", default="13b_stack",
+                    help="headline workload (synth.configs): a stack, or a single-layer decode "
+                         "workload timed as the decode sections are")
+    ap.add_argument("--decode-steps", type=int, default=2000,
+                    help="timed steps of each single-layer decode section (0: skip)")
+    ap.add_argument("--per-layer-tokens", type=int, default=8,
+                    help="tokens of the stack run with one launch per layer (0: skip)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="host time budget of the oracle baseline (0: skip)")
     ap.add_argument("--prefill-steps", type=int, default=200,
@@ -104,13 +110,11 @@ def parse():
                     help="timed decode steps over INT8 and INT4 weight shards (0: skip)")
     ap.add_argument("--moe-steps", type=int, default=1000,
                     help="MoE FFN shard decode steps (0: skip)")
+    ap.add_argument("--repack-reps", type=int, default=20,
+                    help="timed shard packs of the re-partition section (0: skip)")
     ap.add_argument("--fraction-sweep", action="store_true",
                     help="also time the decode step of 7B- and 70B-shaped shards from 10%% to 100%% "
                          "of the layer and fit time = fixed + bytes / bandwidth (about a minute)")
-    ap.add_argument("--stack-tokens", type=int, default=16,
-                    help="timed tokens of the 40-layer 13B-shaped stack section (0: skip)")
-    ap.add_argument("--repack-reps", type=int, default=20,
-                    help="timed shard packs of the re-partition section (0: skip)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="instead of the bench: copy MIB MiB device-to-device 10 times "
                          "(the known-size kernel that scales the HBM byte counters)")
@@ -130,6 +134,268 @@ def copy_calibration(mib):
                       "bytes_written_per_launch": n * 2, "launches": 10}))
 
 
+def lib_dims(wd):
+    from paper_2607_07046_amd import voltron as vt
+    return vt.vt_layer_dims(hidden=wd.hidden, n_heads=wd.n_heads, n_kv_heads=wd.n_kv_heads,
+                            head_dim=wd.head_dim, ffn=wd.ffn, rms_eps=wd.rms_eps,
+                            rope_base=wd.rope_base, window=wd.window)
+
+
+def device_normal(seed):
+    """Seeded fp16 N(mean, sigma) tensors drawn on the device (for weights
+    too large to draw on the host quickly)."""
+    import torch
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(seed)
+
+    def normal(shape, sigma, mean=0.0):
+        t = torch.empty(shape, dtype=torch.float32, device="cuda")
+        t.normal_(mean, sigma, generator=gen)
+        return t.half()
+    return normal
+
+
+def roofline(step_bytes, ms, kernel, workload, launches_per_step=1):
+    gbps = step_bytes / (ms * 1e-3) / 1e9
+    return {"bound": "hbm", "kernel": kernel, "achieved": round(gbps, 1), "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s", "frac": round(gbps / HBM_PEAK_GBPS, 4),
+            "traffic": measured_traffic(workload),
+            "traffic_unit": "B per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-scaled)",
+            "launches_per_step": launches_per_step}
+
+
+def windows(steps, nwin=20):
+    nwin = max(1, min(nwin, steps))
+    return [steps // nwin + (1 if w < steps % nwin else 0) for w in range(nwin)]
+
+
+def stack_headline(wl, steps, warmup, per_layer_tokens):
+    """The 40-layer stack, one vt_stack_decode launch per token, consecutive
+    positions from the cached context. Weights drawn on the device with the
+    workload's distributions (weights N(0, sigma), gains 1 + N(0, 0.1),
+    cached K/V and token inputs N(0, 1)); the stack's parity against the
+    oracle is the tests' (teacher-forced on every layer, and bit for bit
+    against one launch per layer)."""
+    import torch
+
+    from paper_2607_07046_amd import pack
+    from paper_2607_07046_amd import voltron as vt
+
+    t0 = time.time()
+    spec = vt.vt_shard_spec_create(lib_dims(wl.dims), wl.fracs, wl.fracs, wl.device)
+    dims, info = vt.vt_shard_spec_query(spec)
+    H, d, nkv, nq, F, L = (dims.hidden, dims.head_dim, info.n_kv_heads, info.n_q_heads,
+                           info.n_cols, wl.n_layers)
+    ntok = warmup + steps + per_layer_tokens
+    cap = wl.ctx + ntok
+    normal = device_normal(7046 * 1000 + wl.seed_id)
+    fill = lambda name, shape: (normal(shape, 0.1, 1.0) if name.startswith("g_")
+                                else normal(shape, wl.weight_sigma))
+    st = pack.alloc_stack(dims, info, L, fill=fill)
+    kc = torch.zeros((L, nkv, cap, d), dtype=torch.float16, device="cuda")
+    vc = torch.zeros_like(kc)
+    kc[:, :, :wl.ctx] = normal((L, nkv, wl.ctx, d), 1.0)
+    vc[:, :, :wl.ctx] = normal((L, nkv, wl.ctx, d), 1.0)
+    kv = vt.vt_kv_stack(k=kc.data_ptr(), v=vc.data_ptr(), n_layers=L, capacity=cap,
+                        n_kv_heads=nkv, head_dim=d, len=wl.ctx)
+    xs = normal((ntok, H), 1.0)
+    ws_bytes = vt.vt_workspace_size(spec, 1, cap)
+    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device="cuda")
+    outs = {k: torch.empty((L, H), dtype=torch.float16, device="cuda")
+            for k in ("p_attn", "h", "p_ffn", "y")}
+    io = vt.vt_layer_io(x=None, peer_attn=None, peer_ffn=None,
+                        attn_partial=outs["p_attn"].data_ptr(), h=outs["h"].data_ptr(),
+                        ffn_partial=outs["p_ffn"].data_ptr(), y=outs["y"].data_ptr())
+    torch.cuda.synchronize()
+    setup_s = time.time() - t0
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def token(i):
+        io.x = xs[i].data_ptr()
+        vt.vt_stack_decode(spec, st.struct, kv, io, wl.ctx + i, ws.data_ptr(), ws_bytes, stream)
+
+    for i in range(warmup):
+        token(i)
+    torch.cuda.synchronize()
+    wins = windows(steps)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(len(wins) + 1)]
+    i = warmup
+    evs[0].record()
+    for w, n in enumerate(wins):
+        for _ in range(n):
+            token(i)
+            i += 1
+        evs[w + 1].record()
+    torch.cuda.synchronize()
+    ms = evs[0].elapsed_time(evs[-1])
+    ms_step = ms / steps
+    win_ms = np.array([evs[w].elapsed_time(evs[w + 1]) / wins[w] for w in range(len(wins))])
+    err = int(ws[vt.VT_WS_ERROR_WORD:vt.VT_WS_ERROR_WORD + 4].view(torch.int32).item())
+    if err:
+        raise SystemExit("stack: a grid barrier's bounded wait expired (error word set)")
+    if not torch.isfinite(outs["y"].float()).all():
+        raise SystemExit("stack: non-finite output")
+    if kv.len != wl.ctx + warmup + steps:
+        raise SystemExit("stack: the KV length did not advance once per token")
+    tok_bytes = [algorithmic_bytes(dims, info, wl.ctx + t) * L for t in range(warmup, warmup + steps)]
+    mean_bytes = sum(tok_bytes) / steps
+    res = {"ms_per_step": ms_step, "win_ms": win_ms, "bytes": mean_bytes, "setup_s": setup_s,
+           "dims": dims, "info": info,
+           "positions": f"{wl.ctx + warmup}..{wl.ctx + warmup + steps - 1} timed "
+                        f"({warmup} warm-up tokens before)"}
+
+    if per_layer_tokens > 0:
+        # the same layers, one vt_layer_decode launch per layer, continuing the positions
+        kvs = [vt.vt_kv_view(k=kc[l].data_ptr(), v=vc[l].data_ptr(), capacity=cap,
+                             n_kv_heads=nkv, head_dim=d, len=kv.len) for l in range(L)]
+        lw = [st.layer(l) for l in range(L)]
+        lio = [vt.vt_layer_io(x=None, peer_attn=None, peer_ffn=None,
+                              attn_partial=outs["p_attn"][l].data_ptr(),
+                              h=outs["h"][l].data_ptr(), ffn_partial=outs["p_ffn"][l].data_ptr(),
+                              y=outs["y"][l].data_ptr()) for l in range(L)]
+        both = vt.VT_ATTN | vt.VT_FFN
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        p0 = kv.len
+        a.record()
+        for t in range(per_layer_tokens):
+            for l in range(L):
+                lio[l].x = xs[p0 - wl.ctx + t].data_ptr() if l == 0 else outs["y"][l - 1].data_ptr()
+                vt.vt_layer_decode(spec, lw[l], kvs[l], lio[l], p0 + t, both, ws.data_ptr(),
+                                   ws_bytes, stream)
+        b.record()
+        torch.cuda.synchronize()
+        pl_ms = a.elapsed_time(b) / per_layer_tokens
+        pl_bytes = sum(algorithmic_bytes(dims, info, p0 + t) * L
+                       for t in range(per_layer_tokens)) / per_layer_tokens
+        res["per_layer"] = {
+            "ms_per_token": round(pl_ms, 4), "tokens_s": round(1e3 / pl_ms, 1),
+            "us_per_layer": round(pl_ms * 1e3 / L, 2),
+            "hbm_GBps": round(pl_bytes / (pl_ms * 1e-3) / 1e9, 1),
+            "hbm_frac": round(pl_bytes / (pl_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+            "positions": f"{p0}..{p0 + per_layer_tokens - 1}",
+            "launch": f"{L} vt_layer_decode launches per token, eager"}
+    del st, kc, vc
+    torch.cuda.empty_cache()
+    return res
+
+
+def chain_section(wl, steps, warmup):
+    """A single-layer decode workload: step i decodes weight/KV copy i mod R
+    (R copies, >= 768 MB in all, so the Infinity Cache cannot serve the
+    weights) at the workload's position and feeds its y to step i+1 as x.
+    Steps are captured in HIP graphs keyed by (first step mod the rotation
+    length, count), so every window continues the rotation and the chain
+    where the previous one stopped; a window holds up to about 128 steps (a
+    whole number of rotations), so graph launches do not add to the step."""
+    import torch
+
+    from paper_2607_07046_amd import pack
+    from paper_2607_07046_amd import voltron as vt
+    from synth.gen import LayerInputs
+
+    spec = vt.vt_shard_spec_create(lib_dims(wl.dims), wl.fracs, wl.fracs, wl.device)
+    dims, info = vt.vt_shard_spec_query(spec)
+    pos = wl.ctx
+    step_bytes = algorithmic_bytes(dims, info, pos)
+    copies = max(2, math.ceil(MALL_DEFEAT_BYTES / step_bytes))
+    H, d, nkv, cap = dims.hidden, dims.head_dim, info.n_kv_heads, pos + 1
+    li = LayerInputs(wl)
+    w0 = pack.pack_shard(li, dims, info)
+    k, v = li.kv_context_heads(info.kv_head_begin, info.kv_head_begin + nkv)
+    layers = []
+    for c in range(copies):
+        t = {n: x.clone() for n, x in w0.tensors.items()} if c else w0.tensors
+        kc = torch.zeros((nkv, cap, d), dtype=torch.float16, device="cuda")
+        vc = torch.zeros_like(kc)
+        kc[:, :pos] = torch.from_numpy(k).cuda()
+        vc[:, :pos] = torch.from_numpy(v).cuda()
+        kvv = vt.vt_kv_view(k=kc.data_ptr(), v=vc.data_ptr(), capacity=cap, n_kv_heads=nkv,
+                            head_dim=d, len=pos)
+        layers.append((t, pack.struct_of(t, dims, info, w0.struct.ld_d), kc, vc, kvv))
+    ws_bytes = vt.vt_workspace_size(spec, 1, cap)
+    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device="cuda")
+    x0 = torch.from_numpy(li.x(0)).cuda()
+    bufs = [x0.clone(), torch.empty_like(x0)]
+    p_attn, h, p_ffn = (torch.empty(H, dtype=torch.float16, device="cuda") for _ in range(3))
+    both = vt.VT_ATTN | vt.VT_FFN
+
+    def enqueue(i, stream):
+        _, stw, _, _, kvv = layers[i % copies]
+        kvv.len = pos  # every step re-decodes position `pos` of its copy
+        io = vt.vt_layer_io(x=bufs[i % 2].data_ptr(), peer_attn=None, peer_ffn=None,
+                            attn_partial=p_attn.data_ptr(), h=h.data_ptr(),
+                            ffn_partial=p_ffn.data_ptr(), y=bufs[(i + 1) % 2].data_ptr())
+        vt.vt_layer_decode(spec, stw, kvv, io, pos, both, ws.data_ptr(), ws_bytes, stream)
+
+    group = copies * (2 if copies % 2 else 1)  # the copy and buffer pattern repeats after this
+    unit = group * max(1, 128 // group)       # steps per window (whole rotations)
+    graphs = {}
+
+    def graph(start, n):
+        key = (start % group, n)
+        if key not in graphs:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                s = torch.cuda.current_stream().cuda_stream
+                for j in range(n):
+                    enqueue(start + j, s)
+            graphs[key] = g
+        return graphs[key]
+
+    def plan(start, n):
+        """(start, count) windows of at most ``unit`` steps covering n steps, each
+        ending on a multiple of ``unit`` where it can."""
+        out = []
+        while n > 0:
+            c = min(n, unit - start % unit)
+            out.append((start, c))
+            start, n = start + c, n - c
+        return out
+
+    warm = plan(0, warmup)
+    timed = plan(warmup, steps)
+    for s0, n in warm + timed:  # capture everything before any timing
+        graph(s0, n)
+    for s0, n in warm:
+        graph(s0, n).replay()
+    torch.cuda.synchronize()
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(len(timed) + 1)]
+    evs[0].record()
+    for wi, (s0, n) in enumerate(timed):
+        graph(s0, n).replay()
+        evs[wi + 1].record()
+    torch.cuda.synchronize()
+    ms = evs[0].elapsed_time(evs[-1])
+    ms_step = ms / steps
+    win = np.array([evs[i].elapsed_time(evs[i + 1]) / timed[i][1] for i in range(len(timed))])
+    if int(ws[vt.VT_WS_ERROR_WORD:vt.VT_WS_ERROR_WORD + 4].view(torch.int32).item()):
+        raise SystemExit(f"{wl.key}: a grid barrier's bounded wait expired (error word set)")
+    last = bufs[(warmup + steps) % 2]  # the y of the last timed step
+    if not torch.isfinite(last.float()).all():
+        raise SystemExit(f"{wl.key}: non-finite output after the timed steps")
+    gbps = step_bytes / (ms_step * 1e-3) / 1e9
+    out = {
+        "workload": wl.key,
+        "shape": f"hidden {H}, {wl.dims.n_heads}x{d} heads, {wl.dims.n_kv_heads} KV heads, "
+                 f"FFN {wl.dims.ffn}; device {wl.device} of {list(wl.fracs)}: "
+                 f"{info.n_q_heads} q / {info.n_kv_heads} kv heads, {info.n_cols} FFN cols",
+        "pos": pos, "steps": steps, "warmup": warmup, "weight_copies": copies,
+        "ms_per_step": round(ms_step, 6),
+        "ms_per_step_windows": {"windows": len(timed),
+                                "p10": round(float(np.percentile(win, 10)), 6),
+                                "median": round(float(np.median(win)), 6),
+                                "p90": round(float(np.percentile(win, 90)), 6)},
+        "tokens_s": round(1e3 / ms_step, 1),
+        "algorithmic_bytes_per_step": step_bytes,
+        "hbm_GBps": round(gbps, 1),
+        "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
+        "roofline": roofline(step_bytes, ms_step, "decode_kernel<0, 4, 0>", wl.key),
+        "launch": "persistent + hipgraph (windows keyed by rotation phase)",
+    }
+    res = (out, spec, dims, info, enqueue, copies, w0)
+    return res
+
+
 def main():
     args = parse()
     if args.copy_calibration:
@@ -141,190 +407,89 @@ def main():
         sys.exit(2)
     import torch
 
-    from paper_2607_07046_amd import pack
-    from paper_2607_07046_amd import voltron as vt
     from synth import get
-    from synth.gen import LayerInputs
 
     wl = get(args.config)
     if wl.chunk:
         raise SystemExit("bench.py times decode workloads; the prefill chunk is reported "
                          "by its own section")
     torch.cuda.init()
-    dev = torch.device("cuda:0")
-    dims = vt.vt_layer_dims(hidden=wl.dims.hidden, n_heads=wl.dims.n_heads,
-                            n_kv_heads=wl.dims.n_kv_heads, head_dim=wl.dims.head_dim,
-                            ffn=wl.dims.ffn, rms_eps=wl.dims.rms_eps,
-                            rope_base=wl.dims.rope_base, window=wl.dims.window)
-    spec = vt.vt_shard_spec_create(dims, wl.fracs, wl.fracs, wl.device)
-    dims, info = vt.vt_shard_spec_query(spec)
-    pos = wl.ctx
-    step_bytes = algorithmic_bytes(dims, info, pos)
-    copies = args.copies or max(1, math.ceil(MALL_DEFEAT_BYTES / step_bytes))
-    H, d, nkv, cap = dims.hidden, dims.head_dim, info.n_kv_heads, pos + 1
-
-    t0 = time.time()
-    layers = []
-    for c in range(copies):
-        li = LayerInputs(wl, layer=c)
-        w = pack.pack_shard(li, dims, info, dev)
-        kc = torch.zeros((nkv, cap, d), dtype=torch.float16, device=dev)
-        vc = torch.zeros_like(kc)
-        k, v = li.kv_context_heads(info.kv_head_begin, info.kv_head_begin + nkv)
-        kc[:, :pos] = torch.from_numpy(k).to(dev)
-        vc[:, :pos] = torch.from_numpy(v).to(dev)
-        kv = vt.vt_kv_view(k=kc.data_ptr(), v=vc.data_ptr(), capacity=cap, n_kv_heads=nkv,
-                           head_dim=d, len=pos)
-        layers.append((w, kc, vc, kv))
-    ws_bytes = vt.vt_workspace_size(spec, 1, cap)
-    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device=dev)
-    x0 = torch.from_numpy(LayerInputs(wl).x(0)).to(dev)
-    bufs = [x0.clone(), torch.empty_like(x0)]
-    p_attn, h, p_ffn = (torch.empty(H, dtype=torch.float16, device=dev) for _ in range(3))
-    torch.cuda.synchronize()
-    setup_s = time.time() - t0
-
-    phases = vt.VT_ATTN | vt.VT_FFN | (vt.VT_STAGED if args.staged else 0)
-
-    def enqueue(i, stream):
-        w, kc, vc, kv = layers[i % copies]
-        kv.len = pos  # every step re-decodes position `pos` of its copy
-        io = vt.vt_layer_io(x=bufs[i % 2].data_ptr(), peer_attn=None, peer_ffn=None,
-                            attn_partial=p_attn.data_ptr(), h=h.data_ptr(),
-                            ffn_partial=p_ffn.data_ptr(), y=bufs[(i + 1) % 2].data_ptr())
-        vt.vt_layer_decode(spec, w.struct, kv, io, pos, phases, ws.data_ptr(), ws_bytes,
-                           stream)
-
-    # a graph covers a whole number of rotations and an even number of steps
-    group = copies * (2 if copies % 2 else 1)
-    use_graph = not args.eager
-    graphs = {}
-
-    def graph_for(n):
-        if n not in graphs:
-            g = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(g):
-                s = torch.cuda.current_stream().cuda_stream
-                for i in range(n):
-                    enqueue(i, s)
-            graphs[n] = g
-        return graphs[n]
-
-    def run(n):
-        s = torch.cuda.current_stream().cuda_stream
-        if not use_graph:
-            for i in range(n):
-                enqueue(i, s)
-            return
-        reps, rem = divmod(n, group * 8)
-        for _ in range(reps):
-            graph_for(group * 8).replay()
-        if rem:
-            graph_for(rem).replay()
-
-    graph_error = None
-    if use_graph:
-        try:
-            run(group * 8)
-            torch.cuda.synchronize()
-        except Exception as e:  # capture not supported: report and time eagerly
-            graph_error = f"{type(e).__name__}: {e}"
-            use_graph = False
-            torch.cuda.synchronize()
-
-    # The timed steps run as up to 20 back-to-back windows, each bracketed by
-    # events (no synchronisation between them), for a distribution of the
-    # per-step time besides the mean; every window size is run once in the
-    # warm-up so that no graph is captured inside the timed region.
-    nwin = max(1, min(20, args.steps))
-    wins = [args.steps // nwin + (1 if w < args.steps % nwin else 0) for w in range(nwin)]
-    run(args.warmup)
-    for n in sorted(set(wins)):
-        run(n)
-    torch.cuda.synchronize()
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(nwin + 1)]
-    torch.cuda.synchronize()
-    evs[0].record()
-    for w, n in enumerate(wins):
-        run(n)
-        evs[w + 1].record()
-    torch.cuda.synchronize()
-    ms = evs[0].elapsed_time(evs[-1])
-    ms_step = ms / args.steps
-    win_ms = np.array([evs[w].elapsed_time(evs[w + 1]) / wins[w] for w in range(nwin)])
-    err_words = ws[:4 * (3072 + 32 * (info.n_q_heads + 1))].view(torch.int32).cpu().numpy()
-    if np.any(err_words):
-        raise SystemExit(f"decode kernel left synchronisation words set: {err_words[:4]}")
-    if not torch.isfinite(bufs[args.steps % 2].float()).all():
-        raise SystemExit("non-finite output after the timed steps")
-
-    tokens_s = 1e3 / ms_step
-    gbps = step_bytes / (ms_step * 1e-3) / 1e9
-    n_launch = 1 if not args.staged else (5 if info.n_q_heads else 3)
-    out = {
-        "metric": METRIC,
-        "value": round(tokens_s, 1),
-        "unit": "tokens/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 6),
-        "ms_per_step_windows": {"windows": nwin, "p10": round(float(np.percentile(win_ms, 10)), 6),
-                                "median": round(float(np.median(win_ms)), 6),
-                                "p90": round(float(np.percentile(win_ms, 90)), 6)},
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f16",
-        "data": "synthetic",
-        "config": {
-            "workload": wl.key,
-            "layer": f"hidden {H}, {wl.dims.n_heads}x{d} heads, {wl.dims.n_kv_heads} KV heads, "
-                     f"FFN {wl.dims.ffn}",
-            "shard": f"device {wl.device} of fractions {list(wl.fracs)}: "
-                     f"{info.n_q_heads} q heads, {info.n_kv_heads} kv heads, "
-                     f"{info.n_cols} FFN cols",
-            "pos": pos,
-            "weight_copies": copies,
-            "launch": ("staged" if args.staged else "persistent") +
-                      ("+hipgraph" if use_graph else "+eager"),
-        },
-        "hbm_GBps": round(gbps, 1),
-        "hbm_frac_of_peak": round(gbps / HBM_PEAK_GBPS, 4),
-        "algorithmic_bytes_per_step": step_bytes,
-        "roofline": {
-            "bound": "hbm",
-            "kernel": "decode_kernel" if not args.staged else "decode_kernel (5 launches)",
-            "achieved": round(gbps, 1),
-            "peak": HBM_PEAK_GBPS,
-            "unit": "GB/s",
-            "frac": round(gbps / HBM_PEAK_GBPS, 4),
-            "traffic": (measured_traffic() if (wl.key == "7b" and not args.staged) else None),
-            "traffic_unit": "B per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-scaled)",
-            "launches_per_step": n_launch,
-        },
-        "setup_s": round(setup_s, 1),
-    }
-    if graph_error:
-        out["graph_error"] = graph_error
+    out = {"metric": METRIC}
+    if wl.n_layers > 1:
+        r = stack_headline(wl, args.steps, args.warmup, args.per_layer_tokens)
+        dims, info = r["dims"], r["info"]
+        ms_step = r["ms_per_step"]
+        out.update({
+            "value": round(1e3 / ms_step, 2), "unit": "tokens/s", "n_gpus": 1,
+            "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 6),
+            "ms_per_step_windows": {"windows": len(r["win_ms"]),
+                                    "p10": round(float(np.percentile(r["win_ms"], 10)), 6),
+                                    "median": round(float(np.median(r["win_ms"])), 6),
+                                    "p90": round(float(np.percentile(r["win_ms"], 90)), 6)},
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f16",
+            "data": "synthetic",
+            "config": {
+                "workload": wl.key,
+                "layer": f"{wl.n_layers} layers, hidden {dims.hidden}, {wl.dims.n_heads}x"
+                         f"{dims.head_dim} heads, {wl.dims.n_kv_heads} KV heads, FFN {wl.dims.ffn}",
+                "shard": f"device {wl.device} of fractions {list(wl.fracs)}: {info.n_q_heads} q "
+                         f"heads, {info.n_kv_heads} kv heads, {info.n_cols} FFN cols",
+                "positions": r["positions"],
+                "launch": "one vt_stack_decode launch per token (all 40 layers), eager",
+            },
+            "hbm_GBps": round(r["bytes"] / (ms_step * 1e-3) / 1e9, 1),
+            "hbm_frac_of_peak": round(r["bytes"] / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+            "algorithmic_bytes_per_step": int(r["bytes"]),
+            "roofline": roofline(r["bytes"], ms_step, "decode_kernel<0, 4, 0> (40 layers per launch)",
+                                 wl.key),
+            "setup_s": round(r["setup_s"], 1),
+        })
+        if "per_layer" in r:
+            out["per_layer_launches"] = r["per_layer"]
+        sections = ("7b", "70b_gqa")
+    else:
+        sec, *_ = chain_section(wl, args.steps, args.warmup)
+        out.update({
+            "value": sec["tokens_s"], "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": sec["ms_per_step"],
+            "ms_per_step_windows": sec["ms_per_step_windows"], "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": "f16", "data": "synthetic",
+            "config": {"workload": wl.key, "shard": sec["shape"], "pos": sec["pos"],
+                       "weight_copies": sec["weight_copies"], "launch": sec["launch"]},
+            "hbm_GBps": sec["hbm_GBps"], "hbm_frac_of_peak": sec["hbm_frac"],
+            "algorithmic_bytes_per_step": sec["algorithmic_bytes_per_step"],
+            "roofline": sec["roofline"]})
+        sections = tuple(k for k in ("7b", "70b_gqa") if k != wl.key)
+    c2 = None
+    if args.decode_steps > 0:
+        for key in sections:
+            sec, spec2, dims2, info2, enq, copies, w0 = chain_section(
+                get(key), args.decode_steps, max(1, args.decode_steps // 10))
+            out["decode_" + key] = sec
+            if key == "7b":
+                c2 = (spec2, dims2, info2, enq, copies, w0)
+            else:
+                del enq, w0
+            torch.cuda.empty_cache()
     if args.prefill_steps > 0:
-        out["prefill"] = prefill_section(args.prefill_steps, max(1, args.prefill_steps // 10),
-                                         args.eager)
+        out["prefill"] = prefill_section(args.prefill_steps, max(1, args.prefill_steps // 10))
     if args.comm_steps > 0:
         out["comm"] = comm_section(args.comm_steps)
-    if args.repack_reps > 0:
-        out["repack"] = repack_section(spec, dims, info, wl, args.repack_reps, enqueue, copies)
-    if args.quant_steps > 0:
-        out["quant"] = quant_section(spec, dims, info, wl, args.quant_steps,
-                                     max(1, args.quant_steps // 10), layers[0][0], args.eager)
+    if c2 is not None and args.repack_reps > 0:
+        spec2, dims2, info2, enq, copies, w0 = c2
+        out["repack"] = repack_section(spec2, dims2, info2, get("7b"), args.repack_reps, enq, copies)
+    if c2 is not None and args.quant_steps > 0:
+        spec2, dims2, info2, enq, copies, w0 = c2
+        out["quant"] = quant_section(spec2, dims2, info2, get("7b"), args.quant_steps,
+                                     max(1, args.quant_steps // 10), w0)
+    c2 = None
+    torch.cuda.empty_cache()
     if args.moe_steps > 0:
-        out["moe"] = moe_section(args.moe_steps, max(1, args.moe_steps // 10), args.eager)
-    if args.stack_tokens > 0:
-        out["stack"] = stack_section(args.stack_tokens, 4)
+        out["moe"] = moe_section(args.moe_steps, max(1, args.moe_steps // 10))
     if args.fraction_sweep:
         out["fraction_sweep"] = fraction_sweep_section()
     if args.cpu_seconds > 0:
-        out["cpu_baseline"] = cpu_baseline(wl, pos, args.cpu_seconds, step_bytes)
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(out), flush=True)
 
 
@@ -608,112 +773,6 @@ def fraction_sweep_section():
     return out
 
 
-def stack_section(tokens, warmup):
-    """The 13B-shaped 40-layer stack, 40% shard (16 of 40 heads, 5530 of
-    13824 FFN columns): consecutive tokens from position 2048, each token
-    one fused decode launch per layer, layer l's y the input x of layer l+1
-    (the other devices' partials taken as zero), every layer appending to
-    its own KV cache. The 40 layers' shard weights (10.2 GB) are drawn on
-    the device from a seeded generator with the workload's distributions
-    (weights N(0, 0.02), gains 1 + N(0, 0.1), cached K/V and token inputs
-    N(0, 1)); the stack's parity against the oracle chain is a test, this
-    section only times it. Tokens are enqueued eagerly (40 launches each)."""
-    import torch
-
-    from paper_2607_07046_amd import pack
-    from paper_2607_07046_amd import voltron as vt
-    from synth import get
-
-    wl = get("13b_stack")
-    wd = wl.dims
-    dims = vt.vt_layer_dims(hidden=wd.hidden, n_heads=wd.n_heads, n_kv_heads=wd.n_kv_heads,
-                            head_dim=wd.head_dim, ffn=wd.ffn, rms_eps=wd.rms_eps,
-                            rope_base=wd.rope_base, window=wd.window)
-    spec = vt.vt_shard_spec_create(dims, wl.fracs, wl.fracs, wl.device)
-    dims, info = vt.vt_shard_spec_query(spec)
-    H, d, nkv, nq, F = dims.hidden, dims.head_dim, info.n_kv_heads, info.n_q_heads, info.n_cols
-    ntok = warmup + tokens
-    cap = wl.ctx + ntok
-    gen = torch.Generator(device="cuda")
-    gen.manual_seed(7046 * 1000 + wl.seed_id)
-
-    def normal(shape, sigma, mean=0.0):
-        t = torch.empty(shape, dtype=torch.float32, device="cuda")
-        t.normal_(mean, sigma, generator=gen)
-        return t.half()
-
-    ld_d = max(8, pack.round_up(F, 8))
-    layers = []
-    t0 = time.time()
-    for _ in range(wl.n_layers):
-        t = {"g_attn": normal((H,), 0.1, 1.0), "g_ffn": normal((H,), 0.1, 1.0),
-             "wq": normal((nq * d, H), wl.weight_sigma), "wk": normal((nkv * d, H), wl.weight_sigma),
-             "wv": normal((nkv * d, H), wl.weight_sigma), "wo": normal((H, nq * d), wl.weight_sigma),
-             "wg": normal((F, H), wl.weight_sigma), "wu": normal((F, H), wl.weight_sigma)}
-        wdn = torch.zeros((H, ld_d), dtype=torch.float16, device="cuda")
-        wdn[:, :F] = normal((H, F), wl.weight_sigma)
-        t["wd"] = wdn
-        kc = torch.zeros((nkv, cap, d), dtype=torch.float16, device="cuda")
-        vc = torch.zeros_like(kc)
-        kc[:, :wl.ctx] = normal((nkv, wl.ctx, d), 1.0)
-        vc[:, :wl.ctx] = normal((nkv, wl.ctx, d), 1.0)
-        kv = vt.vt_kv_view(k=kc.data_ptr(), v=vc.data_ptr(), capacity=cap, n_kv_heads=nkv,
-                           head_dim=d, len=wl.ctx)
-        layers.append((t, pack.struct_of(t, dims, info, ld_d), kc, vc, kv))
-    xs = normal((ntok, H), 1.0)
-    ws_bytes = vt.vt_workspace_size(spec, 1, cap)
-    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device="cuda")
-    bufs = [torch.empty(H, dtype=torch.float16, device="cuda") for _ in range(2)]
-    p_attn, h, p_ffn = (torch.empty(H, dtype=torch.float16, device="cuda") for _ in range(3))
-    torch.cuda.synchronize()
-    setup_s = time.time() - t0
-    both = vt.VT_ATTN | vt.VT_FFN
-    s = torch.cuda.current_stream().cuda_stream
-
-    def token(tk):
-        pos = wl.ctx + tk
-        for li, (_, st, _, _, kv) in enumerate(layers):
-            x = xs[tk] if li == 0 else bufs[li % 2]
-            io = vt.vt_layer_io(x=x.data_ptr(), peer_attn=None, peer_ffn=None,
-                                attn_partial=p_attn.data_ptr(), h=h.data_ptr(),
-                                ffn_partial=p_ffn.data_ptr(), y=bufs[(li + 1) % 2].data_ptr())
-            vt.vt_layer_decode(spec, st, kv, io, pos, both, ws.data_ptr(), ws_bytes, s)
-
-    for tk in range(warmup):
-        token(tk)
-    torch.cuda.synchronize()
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    start.record()
-    for tk in range(warmup, ntok):
-        token(tk)
-    end.record()
-    torch.cuda.synchronize()
-    ms_tok = start.elapsed_time(end) / tokens
-    err = int(ws[vt.VT_WS_ERROR_WORD:vt.VT_WS_ERROR_WORD + 4].view(torch.int32).item())
-    if err:
-        raise SystemExit("stack section: a decode wait expired (error word set)")
-    if not torch.isfinite(bufs[wl.n_layers % 2].float()).all():
-        raise SystemExit("stack section: non-finite output")
-    if any(kv.len != cap for (_, _, _, _, kv) in layers):
-        raise SystemExit("stack section: a layer's KV length did not advance once per token")
-    tok_bytes = sum(algorithmic_bytes(dims, info, wl.ctx + tk) for tk in range(warmup, ntok)) \
-        * wl.n_layers / tokens
-    gbps = tok_bytes / (ms_tok * 1e-3) / 1e9
-    return {
-        "workload": "13b_stack",
-        "shape": f"40 layers, hidden {H}, {nq} q / {nkv} kv heads, {F} FFN cols (40% shard)",
-        "positions": f"{wl.ctx + warmup}..{wl.ctx + ntok - 1} timed ({warmup} warm-up tokens before)",
-        "ms_per_token": round(ms_tok, 4),
-        "tokens_s": round(1e3 / ms_tok, 1),
-        "us_per_layer": round(ms_tok * 1e3 / wl.n_layers, 2),
-        "bytes_per_token": int(tok_bytes),
-        "hbm_GBps": round(gbps, 1),
-        "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
-        "launch": "one persistent launch per layer, eager",
-        "setup_s": round(setup_s, 1),
-    }
-
-
 def moe_section(steps, warmup, eager=False):
     """Batch-1 decode through the MoE FFN shard (device 0 of the MoE
     workload) with vt_moe_ffn_decode: 16 distinct tokens (each selects its
@@ -978,9 +1037,11 @@ def prefill_section(steps, warmup, eager=False):
     }
 
 
-def cpu_baseline(wl, pos, budget_s, step_bytes):
+def cpu_baseline(wl, budget_s):
     """The fp64 oracle, as it stands, on the host cores: decode steps of the
-    same shard (copy 0) at the same position, until the budget is spent."""
+    workload's shard (for a stack: layers 0 and 1 in turn) at its first
+    decode position, inputs drawn per token, until the budget is spent;
+    scaled to the headline's unit (a stack token is n_layers layer steps)."""
     import oracle
     from synth.gen import LayerInputs
     try:
@@ -989,33 +1050,41 @@ def cpu_baseline(wl, pos, budget_s, step_bytes):
     except Exception:
         threads = 1
     d = wl.dims
-    li = LayerInputs(wl, layer=0)
-    r = oracle.shard_ranges(d.n_heads, d.n_kv_heads, d.ffn, wl.fracs, wl.fracs, wl.device)
     dd = d.head_dim
-    w = oracle.ShardWeights(
-        g_attn=li.g_attn(), wq=li.rows("wq", r.q_head_begin * dd,
-                                       (r.q_head_begin + r.n_q_heads) * dd),
-        wk=li.rows("wk", r.kv_head_begin * dd, (r.kv_head_begin + r.n_kv_heads) * dd),
-        wv=li.rows("wv", r.kv_head_begin * dd, (r.kv_head_begin + r.n_kv_heads) * dd),
-        wo=li.cols("wo", r.q_head_begin * dd, (r.q_head_begin + r.n_q_heads) * dd),
-        g_ffn=li.g_ffn(), wg=li.rows("wg", r.col_begin, r.col_begin + r.n_cols),
-        wu=li.rows("wu", r.col_begin, r.col_begin + r.n_cols),
-        wd=li.cols("wd", r.col_begin, r.col_begin + r.n_cols))
-    kc, vc = li.kv_context_heads(r.kv_head_begin, r.kv_head_begin + r.n_kv_heads)
+    r = oracle.shard_ranges(d.n_heads, d.n_kv_heads, d.ffn, wl.fracs, wl.fracs, wl.device)
+    layers = []
+    for layer in range(min(2, wl.n_layers)):
+        li = LayerInputs(wl, layer=layer)
+        w = oracle.ShardWeights(
+            g_attn=li.g_attn(), wq=li.rows("wq", r.q_head_begin * dd,
+                                           (r.q_head_begin + r.n_q_heads) * dd),
+            wk=li.rows("wk", r.kv_head_begin * dd, (r.kv_head_begin + r.n_kv_heads) * dd),
+            wv=li.rows("wv", r.kv_head_begin * dd, (r.kv_head_begin + r.n_kv_heads) * dd),
+            wo=li.cols("wo", r.q_head_begin * dd, (r.q_head_begin + r.n_q_heads) * dd),
+            g_ffn=li.g_ffn(), wg=li.rows("wg", r.col_begin, r.col_begin + r.n_cols),
+            wu=li.rows("wu", r.col_begin, r.col_begin + r.n_cols),
+            wd=li.cols("wd", r.col_begin, r.col_begin + r.n_cols))
+        kc, vc = li.kv_context_heads(r.kv_head_begin, r.kv_head_begin + r.n_kv_heads)
+        layers.append((li, w, kc, vc))
     n = 0
     t0 = time.perf_counter()
     while True:
+        li, w, kc, vc = layers[n % len(layers)]
         oracle.decode(w, r.n_q_heads, r.n_kv_heads, dd, d.rms_eps, d.rope_base, li.x(n), kc, vc,
-                      pos, window=d.window)
+                      wl.ctx, window=d.window)
         n += 1
         el = time.perf_counter() - t0
         if el >= budget_s:
             break
-    return {"value": round(n / el, 3), "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"{n} fp64 oracle decode steps of the same shard (weight copy 0) at "
-                      f"position {pos}, inputs drawn per token; {el:.1f} s",
-            "GBps_equiv": round(n * step_bytes / el / 1e9, 3),
-            "host_cpus": len(os.sched_getaffinity(0))}
+    per_step = el / n
+    per_token = per_step * wl.n_layers
+    what = (f"{n} fp64 oracle layer decodes (layers 0 and 1 in turn) of the {wl.key} shard at "
+            f"position {wl.ctx}, inputs drawn per token, {el:.1f} s; a token is "
+            f"{wl.n_layers} layer decodes" if wl.n_layers > 1 else
+            f"{n} fp64 oracle decode steps of the {wl.key} shard at position {wl.ctx}, inputs "
+            f"drawn per token; {el:.1f} s")
+    return {"value": round(1.0 / per_token, 4), "unit": "tokens/s", "cores": threads,
+            "kind": "oracle", "sample": what, "host_cpus": len(os.sched_getaffinity(0))}
 
 
 if __name__ == "__main__":

@@ -210,6 +210,48 @@ vt_status vt_layer_decode(const vt_shard_spec* spec, const vt_layer_weights* w,
                           vt_kv_view* kv, const vt_layer_io* io, int32_t pos,
                           uint32_t phases, void* ws, size_t ws_bytes, void* stream);
 
+/* ---- A stack of layers decoded in one launch (paper Sec. 2.1: an LLM
+ * stacks identically structured decoders; Sec. 3.2.1: the tensor-parallel
+ * split repeats at every layer) ----
+ * n_layers consecutive layers of one shard shape decode one token at
+ * position ``pos``: layer 0's input is io->x and layer l's input is layer
+ * l-1's output y (the single-device chain; the aggregation between layers
+ * is what the peers stand for, NULL counting as zero). The results equal
+ * n_layers calls of vt_layer_decode with VT_ATTN | VT_FFN, each fed the
+ * previous call's y, bit for bit; one persistent launch runs them all, so
+ * layer l+1's first weights stream while layer l ends. */
+typedef struct vt_stack_weights {
+  int32_t n_layers;      /* 1..4096 */
+  vt_layer_weights w;    /* each pointer addresses n_layers consecutive copies of its
+                            tensor: layer l's matrix starts l * rows * ld elements past
+                            layer 0's (rows as in vt_layer_weights), its gains l * hidden
+                            elements past; fp16 weights only */
+} vt_stack_weights;
+
+/* KV caches of a stack: k and v are [n_layers][n_kv_heads][capacity][head_dim]
+ * fp16, caller-owned; ``len`` positions are filled in every layer. */
+typedef struct vt_kv_stack {
+  void* k;
+  void* v;
+  int32_t n_layers;
+  int32_t capacity;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t len;
+} vt_kv_stack;
+
+/* One token through the stack. io->x: [hidden] in; io->attn_partial, h,
+ * ffn_partial, y: [n_layers][hidden] out, all required (row l is layer l's
+ * vector, as vt_layer_io describes it); io->peer_attn / peer_ffn: NULL or
+ * [n_layers][hidden]. Every layer appends its token's key and value at slot
+ * ``pos`` (pos must equal kv->len and be < capacity; kv->len becomes pos + 1).
+ * Workspace as for vt_layer_decode (vt_workspace_size of the spec). Errors
+ * as vt_layer_decode, plus VT_ERR_ARG when the weights' and the KV stack's
+ * layer counts differ. */
+vt_status vt_stack_decode(const vt_shard_spec* spec, const vt_stack_weights* w, vt_kv_stack* kv,
+                          const vt_layer_io* io, int32_t pos, void* ws, size_t ws_bytes,
+                          void* stream);
+
 /* Prefill of a chunk of n_tok tokens at positions pos0..pos0+n_tok-1 (paper
  * Sec. 2.1: prompt tokens are processed in parallel). All n_tok keys and
  * values are appended (pos0 must equal kv->len); token t attends to

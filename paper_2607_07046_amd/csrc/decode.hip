@@ -19,7 +19,12 @@
 // bitwise reproducible.
 //
 // The same kernel also runs one phase per launch (VT_STAGED), with no grid
-// barrier; stream order then separates the phases.
+// barrier; stream order then separates the phases. A launch may also run
+// several consecutive layers of a stack (paper Sec. 2.1: identically shaped
+// decoder layers are stacked; Sec. 3.2.1: the TP split repeats at every
+// layer): layer l's output y is layer l+1's input x, handed over across a
+// grid barrier like any other phase's input, so layer l+1's first QKV weight
+// pieces are in flight before layer l has finished.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -59,6 +64,11 @@ struct Params {
   int h_from_ws;    // FFN phases read h from hbuf (1) or from the caller's h (0)
   unsigned* sync;
   int phase_begin, phase_end;
+  // Stacked layers: layer l's tensors sit l strides past layer 0's.
+  int n_layers;        // layers run by one launch (1 unless a stack)
+  int64_t lst_w[7];    // bytes between consecutive layers' q, k, v, o, gate, up, down values / codes
+  int64_t lst_s[7];    // the same for their block scales
+  int64_t lst_kv;      // elements between consecutive layers' K (and V) caches
 };
 
 // ---------------------------------------------------------------------------
@@ -88,7 +98,8 @@ __host__ __device__ __forceinline__ int attn_lds_floats(int d, int nchunk) {
   return d + MAXPASS * ppp + ppp * d + 2 * d + 2 * nchunk + 4;
 }
 
-__device__ __forceinline__ void phase_attn(const Params& P, float* lds, bool wait, unsigned nbar) {
+template <class PT>
+__device__ __forceinline__ void phase_attn(PT& P, int layer, float* lds, bool wait, unsigned nbar) {
   const int d = P.d, G = P.G, CL = P.cl;
   const int TPP = d / 8, PPP = NT / TPP, NPASS = CL / PPP;
   const int t = threadIdx.x, wave = t / kWave, lane = t % kWave;
@@ -106,7 +117,9 @@ __device__ __forceinline__ void phase_attn(const Params& P, float* lds, bool wai
   float* vn = kn + d;
   float* W = vn + d;
   int* flag = reinterpret_cast<int*>(W + 2 * P.nchunk);
-  const rsrc_t rk = make_rsrc(P.kc, P.kv_bytes), rv = make_rsrc(P.vc, P.kv_bytes);
+  uint16_t* const kcl = P.kc + layer * P.lst_kv;  // this layer's cache
+  uint16_t* const vcl = P.vc + layer * P.lst_kv;
+  const rsrc_t rk = make_rsrc(kcl, P.kv_bytes), rv = make_rsrc(vcl, P.kv_bytes);
 
   // rotation of pair t at the new position (independent of phase 0; the
   // same for every item)
@@ -173,14 +186,14 @@ __device__ __forceinline__ void phase_attn(const Params& P, float* lds, bool wai
         kn[2 * t] = h2f(k0);
         kn[2 * t + 1] = h2f(k1);
         if (writer) {
-          P.kc[slot + 2 * t] = k0;
-          P.kc[slot + 2 * t + 1] = k1;
+          kcl[slot + 2 * t] = k0;
+          kcl[slot + 2 * t + 1] = k1;
         }
       } else if (t < half + d) {
         const int i = t - half;
         const uint16_t v0 = f2h(vv);
         vn[i] = h2f(v0);
-        if (writer) P.vc[slot + i] = v0;
+        if (writer) vcl[slot + i] = v0;
       }
     }
     __syncthreads();
@@ -339,10 +352,10 @@ __device__ __forceinline__ void phase_attn(const Params& P, float* lds, bool wai
 // ---------------------------------------------------------------------------
 // the kernel
 // ---------------------------------------------------------------------------
-// One phase; ``wait``: a grid barrier is in front of it, the ``nbar``-th of
-// the launch.
-template <int PH, int F>
-__device__ __forceinline__ void run_phase(const Params& P, float* lds, uint16_t* xs, float* slots,
+// One phase of layer ``layer``; ``wait``: a grid barrier is in front of it,
+// the ``nbar``-th of the launch.
+template <int PH, int F, class PT>
+__device__ __forceinline__ void run_phase(PT& P, int layer, float* lds, uint16_t* xs, float* slots,
                                           float* red, bool wait, unsigned nbar) {
   uint16_t* scl = reinterpret_cast<uint16_t*>(red + 16);  // block scales (quantised formats)
   // The fields that describe the weight matrices are read again in each
@@ -362,32 +375,61 @@ __device__ __forceinline__ void run_phase(const Params& P, float* lds, uint16_t*
   for (int i = 0; i < static_cast<int>(sizeof(Params) / 4); ++i) words[i] = pk[i];
   Params PW;
   __builtin_memcpy(&PW, words, sizeof(Params));
+  // this layer's weight matrix i (values / codes and block scales)
+  auto wmat = [&](int i, const uint8_t* w, int64_t ld, int64_t rows, const uint16_t* s, int64_t lds) {
+    return make_mat(w + layer * PW.lst_w[i], ld, rows, s ? s + layer * (PW.lst_s[i] / 2) : s, lds);
+  };
+  const int64_t io = static_cast<int64_t>(layer) * P.H;  // this layer's vectors
+  // the layer's input: the caller's x, or the previous layer's y written in
+  // this launch (read through the coherent path)
+  const bool x_shared = layer > 0;
+  const uint16_t* x = x_shared ? P.y + io - P.H : P.x;
   if constexpr (PH == PH_QKV) {
-    RowsQKV rows{make_mat(PW.wq, PW.ld_q, PW.nq * PW.d, PW.sq, PW.lds_q),
-                 make_mat(PW.wk, PW.ld_k, PW.nkv * PW.d, PW.sk, PW.lds_k),
-                 make_mat(PW.wv, PW.ld_v, PW.nkv * PW.d, PW.sv, PW.lds_v), PW.nq * PW.d, PW.nkv * PW.d};
+    RowsQKV rows{wmat(0, PW.wq, PW.ld_q, PW.nq * PW.d, PW.sq, PW.lds_q),
+                 wmat(1, PW.wk, PW.ld_k, PW.nkv * PW.d, PW.sk, PW.lds_k),
+                 wmat(2, PW.wv, PW.ld_v, PW.nkv * PW.d, PW.sv, PW.lds_v), PW.nq * PW.d, PW.nkv * PW.d};
     // x and the gains depend on nothing in this launch: their loads go out
     // ahead of the first weight pieces instead of queueing behind them
     // (fp16 7B shard 47.6 -> 47.4 us, 70B 108.1 -> 106.4, INT4 40.9 -> 39.7;
     // INT8, whose scale rows also load up front, measured 43.7 -> 44.1 and
-    // keeps them behind)
+    // keeps them behind). A stacked layer's x is the previous layer's y:
+    // only its gains can go early.
     constexpr bool kEarlyX = F != FMT_Q8;
+    const uint16_t* g = P.g_attn + io;
     RmsInH<4> xin;
     gemv_phase<1, F>(
         rows, (P.nq + 2 * P.nkv) * P.d, P.H, xs, slots, scl,
         [&]() {
-          if constexpr (kEarlyX) xin.load(P.x, P.g_attn, P.H);
+          if constexpr (kEarlyX) {
+            if (x_shared)
+              xin.load_g(g, P.H);
+            else
+              xin.load(x, g, P.H);
+          }
         },
         [&]() {
-          if constexpr (!kEarlyX) xin.load(P.x, P.g_attn, P.H);
+          if (wait) grid_wait(P.sync, nbar);
+          if constexpr (!kEarlyX) {
+            if (x_shared) {
+              xin.load_x(x, P.H, true);
+              xin.load_g(g, P.H);
+            } else {
+              xin.load(x, g, P.H);
+            }
+          } else {
+            if (x_shared) xin.load_x(x, P.H, true);
+          }
           xin.finish(P.H, padded(P.H, F), P.eps, xs, red);
         },
         [&](int r, const float* v) { st_shared(P.qkv + r, v[0]); });
   } else if constexpr (PH == PH_ATTN) {
-    phase_attn(P, lds, wait, nbar);
+    phase_attn(P, layer, lds, wait, nbar);
   } else if constexpr (PH == PH_O) {
-    RowsOne rows{make_mat(PW.wo, PW.ld_o, PW.H, PW.so, PW.lds_o)};
+    RowsOne rows{wmat(3, PW.wo, PW.ld_o, PW.H, PW.so, PW.lds_o)};
     const int K = P.nq * P.d;
+    uint16_t* const pa_out = P.p_attn + io;
+    uint16_t* const h_out = P.h + io;
+    const uint16_t* const peer = P.peer_a ? P.peer_a + io : nullptr;
     gemv_phase<1, F>(
         rows, P.H, K, xs, slots, scl,
         [&]() {
@@ -396,30 +438,37 @@ __device__ __forceinline__ void run_phase(const Params& P, float* lds, uint16_t*
         },
         [&](int r, const float* v) {
           const float pa = v[0];
-          P.p_attn[r] = f2h(pa);
-          const float hv = h2f(P.x[r]) + pa + (P.peer_a ? h2f(P.peer_a[r]) : 0.f);
-          P.h[r] = f2h(hv);
+          pa_out[r] = f2h(pa);
+          const float xr = h2f(x_shared ? ld_h16_shared(x + r) : x[r]);
+          const float hv = xr + pa + (peer ? h2f(peer[r]) : 0.f);
+          h_out[r] = f2h(hv);
           st_shared(P.hbuf + r, hv);
         });
   } else if constexpr (PH == PH_GATEUP) {
-    RowsPair rows{make_mat(PW.wg, PW.ld_g, PW.ncols, PW.sg, PW.lds_g),
-                  make_mat(PW.wu, PW.ld_u, PW.ncols, PW.su, PW.lds_u)};
+    RowsPair rows{wmat(4, PW.wg, PW.ld_g, PW.ncols, PW.sg, PW.lds_g),
+                  wmat(5, PW.wu, PW.ld_u, PW.ncols, PW.su, PW.lds_u)};
+    const uint16_t* const g = P.g_ffn + io;
     gemv_phase<2, F>(
         rows, P.ncols, P.H, xs, slots, scl,
         [&]() {
           if (wait) grid_wait(P.sync, nbar);
           if (P.h_from_ws)
-            stage_rmsnorm_f(P.hbuf, P.g_ffn, P.H, padded(P.H, F), P.eps, xs, red);
+            stage_rmsnorm_f(P.hbuf, g, P.H, padded(P.H, F), P.eps, xs, red);
           else
-            stage_rmsnorm_h(P.h, P.g_ffn, P.H, padded(P.H, F), P.eps, xs, red);
+            stage_rmsnorm_h(P.h + io, g, P.H, padded(P.H, F), P.eps, xs, red);
         },
         [&](int j, const float* v) {
           const float gt = v[0], up = v[1];
           st_shared(P.m + j, gt / (1.0f + __expf(-gt)) * up);
         });
   } else {
-    RowsOne rows{make_mat(PW.wd, PW.ld_d, PW.H, PW.sd, PW.lds_d)};
+    RowsOne rows{wmat(6, PW.wd, PW.ld_d, PW.H, PW.sd, PW.lds_d)};
     const int K = P.ncols;
+    uint16_t* const pf_out = P.p_ffn + io;
+    uint16_t* const y_out = P.y ? P.y + io : nullptr;
+    const uint16_t* const peer = P.peer_f ? P.peer_f + io : nullptr;
+    // a stacked layer's y is the next layer's x: written through the coherent path
+    const bool y_shared = layer + 1 < P.n_layers;
     gemv_phase<1, F>(
         rows, P.H, K, xs, slots, scl,
         [&]() {
@@ -428,30 +477,37 @@ __device__ __forceinline__ void run_phase(const Params& P, float* lds, uint16_t*
         },
         [&](int r, const float* v) {
           const float pf = v[0];
-          P.p_ffn[r] = f2h(pf);
-          if (P.y) {
-            const float hr = P.h_from_ws ? round_h(ld_shared(P.hbuf + r)) : h2f(P.h[r]);
-            P.y[r] = f2h(hr + pf + (P.peer_f ? h2f(P.peer_f[r]) : 0.f));
+          pf_out[r] = f2h(pf);
+          if (y_out) {
+            const float hr = P.h_from_ws ? round_h(ld_shared(P.hbuf + r)) : h2f(P.h[io + r]);
+            const uint16_t yv = f2h(hr + pf + (peer ? h2f(peer[r]) : 0.f));
+            if (y_shared)
+              st_h16_shared(y_out + r, yv);
+            else
+              y_out[r] = yv;
           }
         });
   }
 }
 
-template <int PH, int PE, int PB, int F>
-__device__ __forceinline__ void run_phases(const Params& P, float* lds, uint16_t* xs, float* slots,
+template <int PH, int PE, int PB, int F, class PT>
+__device__ __forceinline__ void run_phases(PT& P, int layer, float* lds, uint16_t* xs, float* slots,
                                            float* red) {
-  run_phase<PH, F>(P, lds, xs, slots, red, PH > PB, static_cast<unsigned>(PH - PB));
+  // barriers so far in this launch: (PE - PB + 1) per earlier layer
+  const unsigned nbar = static_cast<unsigned>(layer * (PE - PB + 1) + PH - PB);
+  run_phase<PH, F>(P, layer, lds, xs, slots, red, nbar > 0, nbar);
   if constexpr (PH < PE) {
     grid_arrive(P.sync);
-    run_phases<PH + 1, PE, PB, F>(P, lds, xs, slots, red);
+    run_phases<PH + 1, PE, PB, F>(P, layer, lds, xs, slots, red);
   }
 }
 
-// Phases PB..PE of one decode step. PB < PE needs every workgroup resident
-// (one per CU): grid barriers separate the phases. Params must stay the only
-// kernel argument (run_phase reads it from the start of the argument
-// segment).
-template <int PB, int PE, int F>
+// Phases PB..PE of one decode step; with STACK, of each of P.n_layers
+// stacked layers. PB < PE or STACK need every workgroup resident (one per
+// CU): grid barriers separate the phases and the layers. Params must stay
+// the only kernel argument (run_phase reads it from the start of the
+// argument segment).
+template <int PB, int PE, int F, bool STACK = false>
 __global__ void __launch_bounds__(NT) decode_kernel(Params P) {
   extern __shared__ float lds[];
   // LDS: xs / attention scratch (aliased) | slots[MAX_SLOTS] | red[16] |
@@ -461,8 +517,22 @@ __global__ void __launch_bounds__(NT) decode_kernel(Params P) {
   uint16_t* xs = reinterpret_cast<uint16_t*>(lds);  // fp16 GEMV input (kmax halfs)
   float* slots = lds + max(kmax / 2, attn);
   float* red = slots + MAX_SLOTS;
-  run_phases<PB, PE, PB, F>(P, lds, xs, slots, red);
-  if constexpr (PE > PB) grid_exit(P.sync);
+  if constexpr (STACK) {
+    // Each layer reads the parameters through a pointer the compiler cannot
+    // follow from one layer to the next: nothing computed from them is
+    // hoisted out of the loop and kept live across every phase (which made
+    // the register allocator spill vector registers to scratch).
+    typedef const __attribute__((address_space(4))) Params KParams;
+    for (int layer = 0; layer < P.n_layers; ++layer) {
+      KParams* pp = (KParams*)__builtin_amdgcn_kernarg_segment_ptr();
+      asm volatile("" : "+s"(pp));
+      if (layer > 0) grid_arrive(pp->sync);
+      run_phases<PB, PE, PB, F>(*pp, layer, lds, xs, slots, red);
+    }
+  } else {
+    run_phases<PB, PE, PB, F>(P, 0, lds, xs, slots, red);
+  }
+  if constexpr (PE > PB || STACK) grid_exit(P.sync);
 }
 
 typedef void (*DecodeKernel)(Params);
@@ -484,6 +554,9 @@ __host__ inline DecodeKernel decode_kernel_fmt(int pb, int pe) {
   }
   return nullptr;
 }
+
+// The persistent kernel of a stack of fp16 layers (all phases, layer loop).
+__host__ inline DecodeKernel decode_stack_kernel() { return decode_kernel<PH_QKV, PH_DOWN, FMT_F16, true>; }
 
 __host__ inline DecodeKernel decode_kernel_for(int pb, int pe, int fmt) {
   switch (fmt) {
@@ -557,6 +630,8 @@ vt_status device_info(DeviceInfo** out) {
         (void)hipFuncSetAttribute(reinterpret_cast<const void*>(dec::decode_kernel_for(r[0], r[1], fmt)),
                                   hipFuncAttributeMaxDynamicSharedMemorySize,
                                   static_cast<int>(di.max_lds));
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(dec::decode_stack_kernel()),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(di.max_lds));
     (void)hipGetLastError();
     di.lds_attr_set = true;
   }
@@ -794,9 +869,18 @@ struct WeightView {
   int64_t lds[7];
 };
 
+// A stack of layers in one launch: their count and the distances from one
+// layer's tensors to the next's (bytes for the matrices, elements for the
+// KV caches).
+struct StackView {
+  int n_layers = 1;
+  int64_t lst_w[7] = {0, 0, 0, 0, 0, 0, 0};
+  int64_t lst_kv = 0;
+};
+
 static vt_status decode_impl(const vt_shard_spec* spec, const WeightView& W, vt_kv_view* kv,
                              const vt_layer_io* io, int32_t pos, uint32_t phases, void* ws,
-                             size_t ws_bytes, void* stream);
+                             size_t ws_bytes, void* stream, const StackView& S = StackView());
 
 static vt_status check_phases(const vt_shard_spec* spec, const vt_layer_io* io, uint32_t phases) {
   if (!spec || !io) return fail(VT_ERR_ARG, "null spec or io");
@@ -846,9 +930,50 @@ extern "C" vt_status vt_layer_decode_q(const vt_shard_spec* spec, const vt_layer
   return decode_impl(spec, W, kv, io, pos, phases, ws, ws_bytes, stream);
 }
 
+extern "C" vt_status vt_stack_decode(const vt_shard_spec* spec, const vt_stack_weights* w,
+                                     vt_kv_stack* kv, const vt_layer_io* io, int32_t pos, void* ws,
+                                     size_t ws_bytes, void* stream) {
+  clear_error();
+  if (!spec || !w || !kv || !io) return fail(VT_ERR_ARG, "null spec, weights, KV or io");
+  const int L = w->n_layers;
+  if (L < 1 || L > 4096) return fail(VT_ERR_ARG, "n_layers %d outside 1..4096", L);
+  if (kv->n_layers != L) return fail(VT_ERR_ARG, "KV stack has %d layers, weights %d", kv->n_layers, L);
+  vt_status st = check_weights(*spec, &w->w, true, true);
+  if (st != VT_OK) return st;
+  if (!io->attn_partial || !io->h || !io->ffn_partial || !io->y)
+    return fail(VT_ERR_ARG, "a stack needs attn_partial, h, ffn_partial and y ([n_layers][hidden] each)");
+  const vt_layer_weights& w0 = w->w;
+  const int64_t H = spec->dims.hidden, d = spec->dims.head_dim;
+  const int64_t qd = static_cast<int64_t>(spec->info.n_q_heads) * d;
+  const int64_t kd = static_cast<int64_t>(spec->info.n_kv_heads) * d;
+  const int64_t F = spec->info.n_cols;
+  // layer l's matrix at l * rows * ld elements past layer 0's (bytes below)
+  const bool heads = spec->info.n_q_heads > 0, cols = F > 0;
+  StackView S;
+  S.n_layers = L;
+  const int64_t rows[7] = {qd, kd, kd, H, F, F, H};
+  const int64_t lds[7] = {w0.ld_q, w0.ld_k, w0.ld_v, w0.ld_o, w0.ld_g, w0.ld_u, w0.ld_d};
+  const bool has[7] = {heads, heads, heads, heads, cols, cols, cols};
+  for (int i = 0; i < 7; ++i) S.lst_w[i] = has[i] ? rows[i] * lds[i] * 2 : 0;
+  S.lst_kv = static_cast<int64_t>(kv->n_kv_heads) * kv->capacity * kv->head_dim;
+  vt_kv_view v0{kv->k, kv->v, kv->capacity, kv->n_kv_heads, kv->head_dim, kv->len};
+  WeightView W{};
+  W.fmt = dec::FMT_F16;
+  W.g_attn = w0.g_attn;
+  W.g_ffn = w0.g_ffn;
+  const void* ptrs[7] = {w0.wq, w0.wk, w0.wv, w0.wo, w0.wg, w0.wu, w0.wd};
+  for (int i = 0; i < 7; ++i) {
+    W.w[i] = ptrs[i];
+    W.ld[i] = lds[i] * 2;
+  }
+  st = decode_impl(spec, W, &v0, io, pos, VT_ATTN | VT_FFN, ws, ws_bytes, stream, S);
+  if (st == VT_OK) kv->len = v0.len;
+  return st;
+}
+
 static vt_status decode_impl(const vt_shard_spec* spec, const WeightView& W, vt_kv_view* kv,
                              const vt_layer_io* io, int32_t pos, uint32_t phases, void* ws,
-                             size_t ws_bytes, void* stream) {
+                             size_t ws_bytes, void* stream, const StackView& S) {
   const bool attn = phases & VT_ATTN, ffn = phases & VT_FFN, staged = phases & VT_STAGED;
   const vt_layer_dims& D = spec->dims;
   const vt_shard_info& in = spec->info;
@@ -921,6 +1046,9 @@ static vt_status decode_impl(const vt_shard_spec* spec, const WeightView& W, vt_
   P.m = reinterpret_cast<float*>(base + L.m);
   P.hbuf = reinterpret_cast<float*>(base + L.hbuf);
   P.h_from_ws = attn ? 1 : 0;
+  P.n_layers = S.n_layers;
+  for (int i = 0; i < 7; ++i) P.lst_w[i] = S.lst_w[i];
+  P.lst_kv = S.lst_kv;
 
   const int kmax = std::max({dec::padded(P.H, W.fmt), dec::padded(P.nq * P.d, W.fmt),
                              dec::padded(P.ncols, W.fmt)});
@@ -934,6 +1062,22 @@ static vt_status decode_impl(const vt_shard_spec* spec, const WeightView& W, vt_
   const int pe = ffn ? dec::PH_DOWN : dec::PH_O;
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = hipSuccess;
+  // The grid barrier needs every workgroup resident at once: one per CU,
+  // and the occupancy query confirms a CU holds at least one. A plain
+  // launch is used (the cooperative launch API adds ~20 us per launch);
+  // the barrier's bounded wait reports rather than hangs if another
+  // kernel were to hold CUs.
+  const bool stack = S.n_layers > 1;
+  if (stack && (staged || W.fmt != dec::FMT_F16 || pb != dec::PH_QKV || pe != dec::PH_DOWN))
+    return fail(VT_ERR_UNSUPPORTED, "a stack runs fp16 layers, all phases, one launch");
+  const dec::DecodeKernel kern = stack ? dec::decode_stack_kernel() : dec::decode_kernel_for(pb, pe, W.fmt);
+  if (!staged) {
+    int per_cu = 0;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, dec::NT, lds);
+    if (e != hipSuccess) return fail(VT_ERR_HIP, "occupancy query: %s", hipGetErrorString(e));
+    if (per_cu < 1)
+      return fail(VT_ERR_UNSUPPORTED, "decode kernel does not fit on a CU with %zu bytes of LDS", lds);
+  }
   if (staged) {
     for (int ph = pb; ph <= pe && e == hipSuccess; ++ph) {
       P.phase_begin = P.phase_end = ph;
@@ -941,17 +1085,6 @@ static vt_status decode_impl(const vt_shard_spec* spec, const WeightView& W, vt_
       e = hipGetLastError();
     }
   } else {
-    // The grid barrier needs every workgroup resident at once: one per CU,
-    // and the occupancy query confirms a CU holds at least one. A plain
-    // launch is used (the cooperative launch API adds ~20 us per launch);
-    // the barrier's bounded wait reports rather than hangs if another
-    // kernel were to hold CUs.
-    const dec::DecodeKernel kern = dec::decode_kernel_for(pb, pe, W.fmt);
-    int per_cu = 0;
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, dec::NT, lds);
-    if (e != hipSuccess) return fail(VT_ERR_HIP, "occupancy query: %s", hipGetErrorString(e));
-    if (per_cu < 1)
-      return fail(VT_ERR_UNSUPPORTED, "decode kernel does not fit on a CU with %zu bytes of LDS", lds);
     P.phase_begin = pb;
     P.phase_end = pe;
     hipLaunchKernelGGL(kern, dim3(di->cus), dim3(dec::NT), lds, s, P);

@@ -181,6 +181,16 @@ __device__ __forceinline__ float buf_ld_shared(rsrc_t r, uint32_t off) {
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kCoherent));
 }
 
+// An fp16 value shared between workgroups of one launch (same agent-scope
+// coherent path as st_shared / ld_shared).
+__device__ __forceinline__ void st_h16_shared(uint16_t* p, uint16_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ uint16_t ld_h16_shared(const uint16_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Two consecutive floats (8-byte aligned) written by other workgroups.
 __device__ __forceinline__ void ld_shared2(const float* p, float& a, float& b) {
   const uint64_t v = __hip_atomic_load(reinterpret_cast<const uint64_t*>(p), __ATOMIC_RELAXED,

@@ -484,6 +484,25 @@ struct RmsInH {
       gv[c] = buf_load16(rg, off);
     }
   }
+  // the gains alone, and the vector alone (``shared``: written by other
+  // workgroups of this launch, read through the agent-scope coherent path)
+  __device__ __forceinline__ void load_g(const uint16_t* g, int n) {
+    const rsrc_t rg = make_rsrc(g, static_cast<uint32_t>(n) * 2u);
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c) gv[c] = buf_load16(rg, static_cast<uint32_t>(threadIdx.x + c * NT) * 16u);
+  }
+  __device__ __forceinline__ void load_x(const uint16_t* v, int n, bool shared) {
+    const rsrc_t rv = make_rsrc(v, static_cast<uint32_t>(n) * 2u);
+    if (shared) {
+#pragma unroll
+      for (int c = 0; c < MAXC; ++c)
+        xv[c] = __builtin_amdgcn_raw_buffer_load_b128(rv, static_cast<uint32_t>(threadIdx.x + c * NT) * 16u, 0,
+                                                      kCoherent);
+    } else {
+#pragma unroll
+      for (int c = 0; c < MAXC; ++c) xv[c] = buf_load16(rv, static_cast<uint32_t>(threadIdx.x + c * NT) * 16u);
+    }
+  }
   // the norm and the fp16 writes to LDS
   __device__ __forceinline__ void finish(int n, int npad, float eps, uint16_t* xs, float* red) const {
     const int nch = n / 8;

@@ -175,3 +175,61 @@ def pack_moe_shard(mi, c0, n_cols, device="cuda", ld_pad=0) -> MoEShardDev:
     st = vt.vt_moe_weights(g_ffn=p(t["g_ffn"]), wr=p(t["wr"]), ld_r=H, wg=p(t["wg"]), ld_g=ldg,
                            wu=p(t["wu"]), ld_u=ldg, wd=p(t["wd"]), ld_d=ldd)
     return MoEShardDev(t, st)
+
+
+@dataclass
+class StackWeightsDev:
+    """A stack of layers' shards, each matrix of every layer in one tensor
+    [n_layers, rows, ld] (gains [n_layers, hidden]): the layout
+    vt_stack_decode takes."""
+    tensors: dict
+    struct: vt.vt_stack_weights
+    dims: vt.vt_layer_dims
+    info: vt.vt_shard_info
+    ld_d: int
+
+    def layer(self, l) -> vt.vt_layer_weights:
+        """Layer l's weights (views into the stacked tensors), as
+        vt_layer_decode takes them."""
+        return struct_of({n: t[l] for n, t in self.tensors.items()}, self.dims, self.info, self.ld_d)
+
+
+def alloc_stack(dims: vt.vt_layer_dims, info: vt.vt_shard_info, n_layers, device="cuda",
+                fill=None) -> StackWeightsDev:
+    """Stacked buffers of n_layers shards (zero-filled, or filled by
+    ``fill(name, shape)`` returning a device fp16 tensor of that shape; the
+    padding columns of wd stay zero)."""
+    H, d = dims.hidden, dims.head_dim
+    qd, kd, nc = info.n_q_heads * d, info.n_kv_heads * d, info.n_cols
+    ld_d = max(8, round_up(nc, 8))
+    shapes = {"g_attn": (H,), "g_ffn": (H,), "wq": (qd, H), "wk": (kd, H), "wv": (kd, H),
+              "wo": (H, qd), "wg": (nc, H), "wu": (nc, H), "wd": (H, ld_d)}
+    t = {}
+    for name, shape in shapes.items():
+        buf = torch.zeros((n_layers, *shape), dtype=torch.float16, device=device)
+        if fill is not None and buf.numel():
+            if name == "wd":
+                buf[:, :, :nc] = fill(name, (n_layers, H, nc))
+            else:
+                buf.copy_(fill(name, (n_layers, *shape)))
+        t[name] = buf
+    return _stack(t, dims, info, n_layers, ld_d)
+
+
+def pack_stack(sources, dims: vt.vt_layer_dims, info: vt.vt_shard_info,
+               device="cuda") -> StackWeightsDev:
+    """The shards of len(sources) layers (each source as for pack_shard)
+    copied into stacked buffers."""
+    st = alloc_stack(dims, info, len(sources), device)
+    for l, src in enumerate(sources):
+        one = pack_shard(src, dims, info, device)
+        for name, t in one.tensors.items():
+            if t.numel():
+                st.tensors[name][l].copy_(t)
+        del one
+    return st
+
+
+def _stack(t, dims, info, n_layers, ld_d):
+    first = struct_of({n: x[0] for n, x in t.items()}, dims, info, ld_d)
+    return StackWeightsDev(t, vt.vt_stack_weights(n_layers=n_layers, w=first), dims, info, ld_d)

@@ -34,7 +34,8 @@ EXPORTS = ("vt_shard_spec_create", "vt_shard_spec_query", "vt_shard_spec_destroy
            "vt_kv_append", "vt_workspace_size", "vt_layer_decode", "vt_layer_prefill_chunk",
            "vt_qplan", "vt_partial_encode", "vt_partial_decode_add",
            "vt_status_string", "vt_last_error", "vt_quantize_rows", "vt_layer_decode_q",
-           "vt_shard_pack", "vt_kv_copy_heads", "vt_moe_workspace_size", "vt_moe_ffn_decode")
+           "vt_shard_pack", "vt_kv_copy_heads", "vt_moe_workspace_size", "vt_moe_ffn_decode",
+           "vt_stack_decode")
 
 
 class VoltronError(RuntimeError):
@@ -95,6 +96,16 @@ class vt_kv_view(ctypes.Structure):
                 ("head_dim", ctypes.c_int32), ("len", ctypes.c_int32)]
 
 
+class vt_stack_weights(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("w", vt_layer_weights)]
+
+
+class vt_kv_stack(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("n_layers", ctypes.c_int32),
+                ("capacity", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("len", ctypes.c_int32)]
+
+
 class vt_layer_io(ctypes.Structure):
     _fields_ = [("x", ctypes.c_void_p), ("peer_attn", ctypes.c_void_p),
                 ("peer_ffn", ctypes.c_void_p), ("attn_partial", ctypes.c_void_p),
@@ -143,6 +154,9 @@ def load_library(path=None):
                                   ctypes.POINTER(vt_layer_weights), P]
     lib.vt_kv_copy_heads.argtypes = [ctypes.POINTER(vt_kv_view), I32, ctypes.POINTER(vt_kv_view),
                                      I32, I32, I32, P]
+    lib.vt_stack_decode.argtypes = [P, ctypes.POINTER(vt_stack_weights),
+                                    ctypes.POINTER(vt_kv_stack), ctypes.POINTER(vt_layer_io), I32,
+                                    P, SZ, P]
     lib.vt_moe_workspace_size.argtypes = [P, I32, I32, ctypes.POINTER(SZ)]
     lib.vt_moe_ffn_decode.argtypes = [P, ctypes.POINTER(vt_moe_weights), I32, I32,
                                       ctypes.POINTER(vt_layer_io), P, P, P, SZ, P]
@@ -150,7 +164,7 @@ def load_library(path=None):
                  "vt_workspace_size", "vt_layer_decode", "vt_layer_prefill_chunk",
                  "vt_qplan", "vt_partial_encode", "vt_partial_decode_add",
                  "vt_quantize_rows", "vt_layer_decode_q", "vt_shard_pack", "vt_kv_copy_heads",
-                 "vt_moe_workspace_size", "vt_moe_ffn_decode"):
+                 "vt_moe_workspace_size", "vt_moe_ffn_decode", "vt_stack_decode"):
         getattr(lib, name).restype = ctypes.c_int
     lib.vt_status_string.argtypes = [ctypes.c_int]
     lib.vt_status_string.restype = ctypes.c_char_p
@@ -218,6 +232,12 @@ def vt_layer_decode(spec: ShardSpec, w: vt_layer_weights, kv, io: vt_layer_io, p
     _check(load_library().vt_layer_decode(spec.handle, ctypes.byref(w),
                                           ctypes.byref(kv) if kv is not None else None,
                                           ctypes.byref(io), pos, phases, ws, ws_bytes, stream))
+
+
+def vt_stack_decode(spec: ShardSpec, w: vt_stack_weights, kv: vt_kv_stack, io: vt_layer_io, pos,
+                    ws, ws_bytes, stream=None):
+    _check(load_library().vt_stack_decode(spec.handle, ctypes.byref(w), ctypes.byref(kv),
+                                          ctypes.byref(io), pos, ws, ws_bytes, stream))
 
 
 def vt_layer_prefill_chunk(spec: ShardSpec, w: vt_layer_weights, kv, io: vt_layer_io, n_tok,

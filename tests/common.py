@@ -10,20 +10,53 @@ import oracle
 from synth import LayerDims, Workload
 from synth.gen import LayerInputs
 
-# Parity bar on fp16 outputs (max relative error 2e-2). Element-wise relative
-# error, with each denominator floored at the root-mean-square of the
-# reference vector: |got_i - ref_i| / max(|ref_i|, rms(ref)). The floor is
-# needed because the error that fp16 activations at the sub-layer boundaries
-# (x, h, the partial sums) carry into a projection scales with the vector's
-# norm, not with each element, so elements near zero by cancellation would
-# otherwise dominate. A normwise bound ||got - ref|| / ||ref|| <= NORM_TOL
-# (an order of magnitude above fp16 rounding noise) also catches small
-# systematic slips such as one wrong column of a wide projection.
+# Parity bar on fp16 outputs: max relative error 2e-2, element-wise, each
+# denominator floored at FLOOR times the root-mean-square of the reference
+# vector: |got_i - ref_i| / max(|ref_i|, FLOOR * rms(ref)) <= REL_TOL, plus a
+# normwise bound ||got - ref|| / ||ref|| <= NORM_TOL.
+#
+# Derivation of the floor. The path rounds a vector to fp16 wherever it
+# becomes the input of a projection (the normalised inputs, the attention
+# output, the SiLU-gate product; in a prefill chunk also the rotated queries
+# and the attention probabilities) and rounds every output. Rounding a
+# vector to fp16 moves each element by up to half an ulp (2^-11 of it), an
+# RMS relative error of 2^-11 / sqrt(3) = 2.8e-4, and a projection carries
+# that into its output as about the same fraction of the output's RMS, the
+# same for small and large elements. An output behind two such roundings
+# (decode p_attn: normalised input and attention output; p_ffn: normalised
+# h and the SiLU-gate product) has an absolute error of sigma ~ 4e-4 * rms
+# (a numpy model of the rounding points, the oracle's own functions plus
+# fp16 casts, gives 3.3e-4 on the 7B shard and up to 6.2e-4 on the 13B
+# stack's layer 20; measured on the device: at most 6.6e-4, the prefill
+# chunk's p_attn). A test compares up to 10^6 elements (256 rows x 4096),
+# whose largest error reaches about 5 sigma = 3.3e-3 * rms. Holding that to
+# REL_TOL needs a floor of 3.3e-3 / 2e-2 = 0.17 of the RMS: FLOOR = 0.2.
+# Elements below 0.2 * rms (16% of a Gaussian vector's) are checked to an
+# absolute 4e-3 * rms, all others to 2e-2 of their own size. NORM_TOL =
+# 1.5e-3 keeps about 2x headroom over the largest measured normwise error
+# and still catches one wrong column of a 3302-wide projection (~1.7e-2).
+#
+# The FFN outputs are compared with the oracle's FFN evaluated at the
+# oracle's h rounded to fp16 (``ffn_at_h16``): the boundary defines the FFN
+# input as h as written, in fp16 (what the aggregation broadcasts).
 REL_TOL = 2e-2
-NORM_TOL = 4e-3
+FLOOR = 0.2
+NORM_TOL = 1.5e-3
+
+# worst errors of the running test, printed by conftest when it ends
+WORST = {}
 
 
-def max_rel_err(got, ref):
+def _record(what, e, n):
+    w = WORST.setdefault("elem", (0.0, ""))
+    if e >= w[0]:
+        WORST["elem"] = (e, what)
+    w = WORST.setdefault("norm", (0.0, ""))
+    if n >= w[0]:
+        WORST["norm"] = (n, what)
+
+
+def max_rel_err(got, ref, floor=FLOOR):
     got = np.asarray(got, np.float64)
     ref = np.asarray(ref, np.float64)
     assert got.shape == ref.shape, (got.shape, ref.shape)
@@ -38,7 +71,7 @@ def max_rel_err(got, ref):
         if np.any(got[zero_rows] != 0):
             return float("inf")
         rms = np.where(rms == 0, 1.0, rms)
-    denom = np.maximum(np.abs(ref), rms)
+    denom = np.maximum(np.abs(ref), floor * rms)
     return float(np.max(np.abs(got - ref) / denom))
 
 
@@ -54,8 +87,28 @@ def norm_rel_err(got, ref):
 
 def assert_close(got, ref, what=""):
     e, n = max_rel_err(got, ref), norm_rel_err(got, ref)
+    _record(what, e, n)
     assert e <= REL_TOL and n <= NORM_TOL, f"{what}: element-wise {e:.3g}, normwise {n:.3g}"
     return e, n
+
+
+def h16(a):
+    """fp16 rounding, returned as float64."""
+    return np.asarray(a, np.float16).astype(np.float64)
+
+
+def ffn_at_h16(w, eps, ref, peer_ffn=None):
+    """Replace ref['p_ffn'] / ref['y'] by the oracle's FFN sub-layer at
+    fp16(ref['h']), the FFN input the boundary defines. Works for one token
+    ([H]) or a chunk ([T, H])."""
+    h = h16(ref["h"])
+    one = h.ndim == 1
+    pf = None if peer_ffn is None else np.asarray(peer_ffn, np.float64)
+    p, y = oracle.ffn_sublayer(w, eps, h[None] if one else h,
+                               None if pf is None else (pf[None] if one else pf))
+    out = dict(ref)
+    out["p_ffn"], out["y"] = (p[0], y[0]) if one else (p, y)
+    return out
 
 
 def oracle_ranges(wl: Workload, device=None):
@@ -87,8 +140,9 @@ def oracle_decode(wl: Workload, li: LayerInputs, r, x, kc, vc, pos, peer_attn=No
                   peer_ffn=None, w=None):
     d = wl.dims
     w = w if w is not None else oracle_shard_weights(li, r)
-    return oracle.decode(w, r.n_q_heads, r.n_kv_heads, d.head_dim, d.rms_eps, d.rope_base,
-                         x, kc, vc, pos, peer_attn, peer_ffn, window=d.window)
+    ref = oracle.decode(w, r.n_q_heads, r.n_kv_heads, d.head_dim, d.rms_eps, d.rope_base,
+                        x, kc, vc, pos, peer_attn, peer_ffn, window=d.window)
+    return ffn_at_h16(w, d.rms_eps, ref, peer_ffn)
 
 
 def tiny_workload(seed_id, hidden, n_heads, n_kv, head_dim, ffn, fracs, device, ctx,

@@ -16,3 +16,16 @@ def pytest_runtest_logstart(nodeid, location):
     # mid-test still shows which case it was in.
     sys.__stderr__.write(f"[start] {nodeid}\n")
     sys.__stderr__.flush()
+
+
+def pytest_runtest_logfinish(nodeid, location):
+    # every parity test reports its worst element-wise and normwise errors
+    # (outside pytest's output capture, like the [start] line)
+    from tests import common
+    if common.WORST:
+        e, ew = common.WORST.get("elem", (0.0, ""))
+        n, nw = common.WORST.get("norm", (0.0, ""))
+        sys.__stderr__.write(f"[parity] {nodeid}: worst element-wise {e:.3g} ({ew}), "
+                             f"normwise {n:.3g} ({nw})\n")
+        sys.__stderr__.flush()
+        common.WORST.clear()

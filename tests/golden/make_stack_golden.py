@@ -15,11 +15,13 @@ the vector's RMS (the tolerance floor) and its values at 40 sampled indices
 (``sample_index``); full vectors of the first and last token at the first
 and last layer.
 
-Teacher forcing at layers TF_LAYERS: the chain's inputs of all 64 tokens at
-that layer, rounded to fp16 (the precision of the layer interface), and the
-oracle's outputs for exactly those inputs (RMS, samples, full vectors of
-tokens TF_FULL_TOKENS). A device run fed these inputs is held to the
-single-layer bar, free of the drift a 40-layer chain accumulates.
+Teacher forcing: at every layer, the chain's inputs of the first TF4
+tokens (``tf4_x``); at layers TF_LAYERS, the chain's inputs of all 64
+tokens (``tf_x``) and the oracle's outputs for exactly those inputs (RMS,
+samples, full vectors of tokens TF_FULL_TOKENS). Inputs are rounded to fp16,
+the precision of the layer interface. A device run fed these inputs is held
+to the single-layer bar (the GPU test evaluates the oracle on them again),
+free of the drift a 40-layer chain accumulates.
 
 Drift model: the same chain computed with fp16 rounding at the points where
 the device rounds (the normalised inputs of the projections, q, the cached
@@ -53,6 +55,7 @@ FULL_LAYERS = (0, 39)
 FULL_TOKENS = (0, 63)
 TF_LAYERS = (20, 39)
 TF_FULL_TOKENS = (0, 31, 63)
+TF4 = 4  # leading tokens teacher-forced at every layer
 
 
 def sample_index(hidden, layer, token):
@@ -130,6 +133,7 @@ def build():
     samples = np.zeros((wl.n_layers, T, len(KEYS), N_SAMPLES))
     full = np.zeros((len(FULL_LAYERS), len(FULL_TOKENS), len(KEYS), H))
     tf_x = np.zeros((len(TF_LAYERS), T, H), np.float16)
+    tf4_x = np.zeros((wl.n_layers, TF4, H), np.float16)
     tf_rms = np.zeros((len(TF_LAYERS), T, len(KEYS)))
     tf_samples = np.zeros((len(TF_LAYERS), T, len(KEYS), N_SAMPLES))
     tf_full = np.zeros((len(TF_LAYERS), len(TF_FULL_TOKENS), len(KEYS), H))
@@ -140,6 +144,7 @@ def build():
         li = li0 if layer == 0 else LayerInputs(wl, layer)
         w = shard_weights(li, r, d)
         kc, vc = li.kv_context_heads(r.kv_head_begin, r.kv_head_begin + r.n_kv_heads)
+        tf4_x[layer] = X[:TF4].astype(np.float16)
         ref = oracle.prefill(w, r.n_q_heads, r.n_kv_heads, d, dm.rms_eps, dm.rope_base, X, kc,
                              vc, wl.ctx)
         rms[layer], samples[layer] = summarize(ref, layer, H, T)
@@ -170,7 +175,7 @@ def build():
                         n_samples=np.array(N_SAMPLES), tf_layers=np.array(TF_LAYERS),
                         tf_x=tf_x, tf_rms=tf_rms, tf_samples=tf_samples.astype(np.float32),
                         tf_full=tf_full.astype(np.float32), tf_full_tokens=np.array(TF_FULL_TOKENS),
-                        model_err=model_err)
+                        tf4_x=tf4_x, model_err=model_err)
     print("wrote", OUT, os.path.getsize(OUT), "bytes")
 
 

@@ -2,8 +2,9 @@
 fp64 oracle, through the C ABI.
 
 Bar: every fp16 output vector within max relative error 2e-2 (element-wise,
-denominator floored at the reference vector's RMS) and normwise relative
-error 4e-3 (see tests/common.py); KV indexing
+denominator floored at 0.2 of the reference vector's RMS) and normwise
+relative error 1.5e-3 (derivation in tests/common.py), the FFN outputs
+against the oracle's FFN at fp16(h); KV indexing
 bit-exact (the appended slot holds the new key/value, every other cache
 byte keeps its sentinel or context value, ``len`` advances by one).
 """
@@ -15,8 +16,9 @@ import oracle
 from paper_2607_07046_amd import voltron as vt
 from synth import get
 from synth.gen import LayerInputs
-from tests.common import (NORM_TOL, REL_TOL, assert_close, full_weights, max_rel_err,
-                          norm_rel_err, oracle_ranges, oracle_shard_weights, tiny_workload)
+from tests.common import (NORM_TOL, REL_TOL, _record, assert_close, ffn_at_h16, full_weights,
+                          max_rel_err, norm_rel_err, oracle_ranges, oracle_shard_weights,
+                          tiny_workload)
 from tests.gpu_common import SENTINEL, GpuShard
 
 pytestmark = pytest.mark.gpu
@@ -39,12 +41,15 @@ def oracle_case(wl, device=None, li=None):
         x = li.x(0)
         ref = oracle.decode(w, r.n_q_heads, r.n_kv_heads, d.head_dim, d.rms_eps, d.rope_base,
                             x, kc, vc, wl.ctx)
+        ref = ffn_at_h16(w, d.rms_eps, ref)
         _cache[key] = (li, r, x, ref)
     return _cache[key]
 
 
 def check_outputs(got, ref, keys=("p_attn", "h", "p_ffn", "y")):
     errs = {k: (max_rel_err(got[k], ref[k]), norm_rel_err(got[k], ref[k])) for k in keys}
+    for k, (e, n) in errs.items():
+        _record(k, e, n)
     bad = {k: e for k, e in errs.items() if not (e[0] <= REL_TOL and e[1] <= NORM_TOL)}
     assert not bad, f"(element-wise, normwise) relative errors {errs}"
     return errs
@@ -102,8 +107,9 @@ def test_all_shards_sum_to_unsharded_layer(key):
     li = LayerInputs(wl)
     x = li.x(0)
     kc, vc = li.kv_context_heads(0, d.n_kv_heads)
-    full = oracle.decode(full_weights(li), d.n_heads, d.n_kv_heads, d.head_dim, d.rms_eps,
-                         d.rope_base, x, kc, vc, wl.ctx)
+    fw = full_weights(li)
+    full = oracle.decode(fw, d.n_heads, d.n_kv_heads, d.head_dim, d.rms_eps, d.rope_base, x, kc,
+                         vc, wl.ctx)
     shards = [GpuShard(wl, device=s, li=li) for s in range(len(wl.fracs))]
     parts = [gs.decode(x, wl.ctx, vt.VT_ATTN) for gs in shards]
     sum_attn = np.sum([p["p_attn"] for p in parts], axis=0)
@@ -112,6 +118,7 @@ def test_all_shards_sum_to_unsharded_layer(key):
     h = (x.astype(np.float64) + sum_attn).astype(np.float16)
     ffn = [gs.decode(None, phases=vt.VT_FFN, h_in=h) for gs in shards]
     sum_ffn = np.sum([f["p_ffn"] for f in ffn], axis=0)
+    full = ffn_at_h16(fw, d.rms_eps, full)
     assert_close(sum_ffn, full["p_ffn"], "sum of FFN partials")
     # peer semantics: shard 0 given the others' partials produces the full h and y
     peer_a = np.sum([p["p_attn"] for p in parts[1:]], axis=0).astype(np.float16)
@@ -136,6 +143,7 @@ def test_consecutive_tokens_match_oracle_chain():
         x = li.x(t)
         ref = oracle.decode(w, r.n_q_heads, r.n_kv_heads, d.head_dim, d.rms_eps, d.rope_base,
                             x, kc, vc, pos)
+        ref = ffn_at_h16(w, d.rms_eps, ref)
         got = gs.decode(x, pos, BOTH | (vt.VT_STAGED if t % 2 else 0))
         check_outputs(got, ref)
         kc = np.concatenate([kc, ref["k_new"][:, None]], axis=1)

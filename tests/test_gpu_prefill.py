@@ -1,8 +1,9 @@
 """GPU parity of the prefill chunk (vt_layer_prefill_chunk, MFMA path)
 against the fp64 oracle, through the C ABI.
 
-Same bar as decode (per-row element-wise relative error with an RMS floor
-<= 2e-2, normwise <= 4e-3); the appended K/V of every chunk token lands in
+Same bar as decode (per-row element-wise relative error <= 2e-2 with the
+denominator floored at 0.2 of the row's RMS, normwise <= 1.5e-3; the FFN
+outputs against the oracle's FFN at fp16(h)); the appended K/V of every chunk token lands in
 its slot and every other cache byte is unchanged.
 """
 import numpy as np
@@ -12,7 +13,7 @@ import oracle
 from paper_2607_07046_amd import voltron as vt
 from synth import get
 from synth.gen import LayerInputs
-from tests.common import (assert_close, max_rel_err, norm_rel_err, oracle_ranges,
+from tests.common import (assert_close, ffn_at_h16, max_rel_err, norm_rel_err, oracle_ranges,
                           oracle_shard_weights, tiny_workload)
 from tests.gpu_common import GpuShard
 
@@ -30,6 +31,7 @@ def run_case(wl, T, li=None, check_kv=True):
     pa, pf = li.peer("attn", rows=T), li.peer("ffn", rows=T)
     ref = oracle.prefill(w, r.n_q_heads, r.n_kv_heads, d.head_dim, d.rms_eps, d.rope_base, X, kc,
                          vc, wl.ctx, pa, pf)
+    ref = ffn_at_h16(w, d.rms_eps, ref, pf)
     gs = GpuShard(wl, li=li, capacity=wl.ctx + T + 3, max_tokens=T)
     k0, v0 = gs.cache()
     got = gs.prefill(X, wl.ctx, BOTH, peer_attn=pa, peer_ffn=pf)
@@ -94,6 +96,7 @@ def test_prefill_then_decode_continues_the_cache():
     x = li.x(77)
     ref = oracle.decode(w, r.n_q_heads, r.n_kv_heads, d.head_dim, d.rms_eps, d.rope_base, x, kc2,
                         vc2, wl.ctx + 9)
+    ref = ffn_at_h16(w, d.rms_eps, ref)
     got = gs.decode(x, wl.ctx + 9, BOTH)
     for k in ("p_attn", "h", "p_ffn", "y"):
         assert_close(got[k], ref[k], k)

@@ -16,7 +16,7 @@ from paper_2607_07046_amd import voltron as vt
 from synth import get
 from synth.configs import LayerDims, Workload
 from synth.gen import LayerInputs
-from tests.common import assert_close, oracle_decode, oracle_ranges
+from tests.common import assert_close, ffn_at_h16, oracle_decode, oracle_ranges, oracle_shard_weights
 from tests.gpu_common import GpuShard
 
 pytestmark = pytest.mark.gpu
@@ -74,9 +74,9 @@ def test_prefill_chunk_window(window):
     got = gs.prefill(X, wl.ctx)
     r = oracle_ranges(wl)
     kc, vc = gs.context()
-    from tests.common import oracle_shard_weights
-    ref = oracle.prefill(oracle_shard_weights(li, r), r.n_q_heads, r.n_kv_heads, d.head_dim,
-                         d.rms_eps, d.rope_base, X, kc, vc, wl.ctx, window=window)
-    for k in ("p_attn", "h", "p_ffn", "y"):
-        for t in range(0, 128, 9):
-            assert_close(got[k][t], ref[k][t], f"window {window} {k} token {t}")
+    w = oracle_shard_weights(li, r)
+    ref = oracle.prefill(w, r.n_q_heads, r.n_kv_heads, d.head_dim, d.rms_eps, d.rope_base, X, kc,
+                         vc, wl.ctx, window=window)
+    ref = ffn_at_h16(w, d.rms_eps, ref)
+    for k in ("p_attn", "h", "p_ffn", "y"):   # every row of the chunk
+        assert_close(got[k], ref[k], f"window {window} {k}")

@@ -19,7 +19,7 @@ from oracle import wquant as W
 from paper_2607_07046_amd import voltron as vt
 from synth import get
 from synth.gen import LayerInputs
-from tests.common import assert_close, oracle_qshard_weights, oracle_ranges, tiny_workload
+from tests.common import assert_close, ffn_at_h16, oracle_qshard_weights, oracle_ranges, tiny_workload
 from tests.gpu_common import GpuShard
 
 pytestmark = pytest.mark.gpu
@@ -93,6 +93,7 @@ def case(wl, level):
         x = li.x(0)
         ref = oracle.decode(w, r.n_q_heads, r.n_kv_heads, d.head_dim, d.rms_eps, d.rope_base, x,
                             kc, vc, wl.ctx)
+        ref = ffn_at_h16(w, d.rms_eps, ref)
         _cache[key] = (li, x, ref)
     return _cache[key]
 

@@ -174,6 +174,35 @@ def test_decode_validation_errors(lib):
     assert kv.len == 128
 
 
+def test_stack_decode_validation_errors(lib):
+    spec = _tiny_spec()
+    ws_need = vt.vt_workspace_size(spec, 1, 129)
+    A = 1 << 20
+    kv = vt.vt_kv_stack(k=A, v=A, n_layers=3, capacity=200, n_kv_heads=4, head_dim=64, len=128)
+
+    def call(n_layers=3, kv_=kv, io=None, pos=128, ws=A, wsb=ws_need, w=None):
+        sw = vt.vt_stack_weights(n_layers=n_layers, w=w or _fake_weights())
+        io = io or vt.vt_layer_io(x=A, peer_attn=None, peer_ffn=None, attn_partial=A, h=A,
+                                  ffn_partial=A, y=A)
+        with pytest.raises(vt.VoltronError) as e:
+            vt.vt_stack_decode(spec, sw, kv_, io, pos, ws, wsb)
+        return e.value.status
+
+    assert call(n_layers=2) == vt.VT_ERR_ARG       # weights and caches disagree
+    assert call(n_layers=0) == vt.VT_ERR_ARG
+    assert call(pos=127) == vt.VT_ERR_POS
+    assert call(wsb=256) == vt.VT_ERR_WORKSPACE
+    io = vt.vt_layer_io(x=A, peer_attn=None, peer_ffn=None, attn_partial=A, h=A, ffn_partial=A,
+                        y=None)
+    assert call(io=io) == vt.VT_ERR_ARG            # every layer's y is required
+    w = _fake_weights()
+    w.wg = A + 2
+    assert call(w=w) == vt.VT_ERR_ALIGN
+    full = vt.vt_kv_stack(k=A, v=A, n_layers=3, capacity=128, n_kv_heads=4, head_dim=64, len=128)
+    assert call(kv_=full) == vt.VT_ERR_KV_FULL
+    assert kv.len == 128
+
+
 def test_kv_append_validation_errors(lib):
     A = 1 << 20
     kv = vt.vt_kv_view(k=A, v=A, capacity=10, n_kv_heads=2, head_dim=128, len=4)
