@@ -210,6 +210,26 @@ vt_status vt_layer_decode(const vt_shard_spec* spec, const vt_layer_weights* w,
                           vt_kv_view* kv, const vt_layer_io* io, int32_t pos,
                           uint32_t phases, void* ws, size_t ws_bytes, void* stream);
 
+/* ---- Decode without a caller workspace ----
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * step as vt_layer_decode, its workspace taken from a scratch array of
+ * VT_NOALLOC_SCRATCH_BYTES that the library holds on each GPU it runs on
+ * (until the process ends). Nothing is allocated and nothing synchronises.
+ * Every call on a GPU shares that GPU's array: the call clears what must
+ * start at zero (a small kernel on ``stream`` ahead of the decode), and
+ * calls that may overlap on one GPU (other streams or threads) race.
+ * VT_ERR_UNSUPPORTED when the shape and context need a larger workspace
+ * than the array (vt_workspace_size of the spec with max_ctx = pos + 1).
+ * ``wait_error`` (nullable, device, 4-byte aligned): receives the barrier
+ * error word of this call (nonzero if a bounded grid wait expired and the
+ * outputs are undefined), written on ``stream`` after the decode. Other
+ * arguments, outputs and errors as vt_layer_decode. */
+#define VT_NOALLOC_SCRATCH_BYTES (4u << 20)
+vt_status vt_layer_decode_noalloc(const vt_shard_spec* spec, const vt_layer_weights* w,
+                                  vt_kv_view* kv, const vt_layer_io* io, int32_t pos,
+                                  uint32_t phases, uint32_t* wait_error, void* stream);
+
 /* ---- A stack of layers decoded in one launch (paper Sec. 2.1: an LLM
  * stacks identically structured decoders; Sec. 3.2.1: the tensor-parallel
  * split repeats at every layer) ----

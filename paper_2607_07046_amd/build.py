@@ -17,7 +17,7 @@ OUT = os.path.join(HERE, "libvoltron.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 SOURCES = ["spec.cpp", "decode.hip", "moe.hip", "prefill.hip", "comm.hip", "wquant.hip",
-           "repack.hip"]
+           "repack.hip", "noalloc.hip"]
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-Wno-unused-command-line-argument"]

@@ -589,6 +589,12 @@ __global__ void __launch_bounds__(256) kv_append_kernel(const uint16_t* __restri
   }
 }
 
+// Zero ``n`` 32-bit words (the synchronisation words of a workspace that
+// may hold a previous call's contents).
+__global__ void __launch_bounds__(256) zero_words(uint32_t* p, int n) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0u;
+}
+
 }  // namespace dec
 
 // ---------------------------------------------------------------------------
@@ -876,6 +882,7 @@ struct StackView {
   int n_layers = 1;
   int64_t lst_w[7] = {0, 0, 0, 0, 0, 0, 0};
   int64_t lst_kv = 0;
+  bool clear_sync = false;  // zero the workspace's synchronisation words first
 };
 
 static vt_status decode_impl(const vt_shard_spec* spec, const WeightView& W, vt_kv_view* kv,
@@ -893,6 +900,12 @@ extern "C" vt_status vt_layer_decode(const vt_shard_spec* spec, const vt_layer_w
                                      vt_kv_view* kv, const vt_layer_io* io, int32_t pos,
                                      uint32_t phases, void* ws, size_t ws_bytes, void* stream) {
   clear_error();
+  return vt::layer_decode_ws(spec, w, kv, io, pos, phases, ws, ws_bytes, stream, false);
+}
+
+vt_status vt::layer_decode_ws(const vt_shard_spec* spec, const vt_layer_weights* w, vt_kv_view* kv,
+                              const vt_layer_io* io, int32_t pos, uint32_t phases, void* ws,
+                              size_t ws_bytes, void* stream, bool clear_sync) {
   vt_status st = check_phases(spec, io, phases);
   if (st != VT_OK) return st;
   if ((st = check_weights(*spec, w, phases & VT_ATTN, phases & VT_FFN)) != VT_OK) return st;
@@ -906,7 +919,9 @@ extern "C" vt_status vt_layer_decode(const vt_shard_spec* spec, const vt_layer_w
     W.w[i] = ptrs[i];
     W.ld[i] = lds[i] * 2;
   }
-  return decode_impl(spec, W, kv, io, pos, phases, ws, ws_bytes, stream);
+  StackView S;
+  S.clear_sync = clear_sync;
+  return decode_impl(spec, W, kv, io, pos, phases, ws, ws_bytes, stream, S);
 }
 
 extern "C" vt_status vt_layer_decode_q(const vt_shard_spec* spec, const vt_layer_qweights* w,
@@ -1077,6 +1092,14 @@ static vt_status decode_impl(const vt_shard_spec* spec, const WeightView& W, vt_
     if (e != hipSuccess) return fail(VT_ERR_HIP, "occupancy query: %s", hipGetErrorString(e));
     if (per_cu < 1)
       return fail(VT_ERR_UNSUPPORTED, "decode kernel does not fit on a CU with %zu bytes of LDS", lds);
+  }
+  // every check has passed: the launches below are the call's
+  if (S.clear_sync) {
+    const int nwords = static_cast<int>(L.qkv / 4);
+    hipLaunchKernelGGL(dec::zero_words, dim3((nwords + 255) / 256), dim3(256), 0, s,
+                       static_cast<uint32_t*>(ws), nwords);
+    e = hipGetLastError();
+    if (e != hipSuccess) return fail(VT_ERR_HIP, "workspace clear launch: %s", hipGetErrorString(e));
   }
   if (staged) {
     for (int ph = pb; ph <= pe && e == hipSuccess; ++ph) {

@@ -35,4 +35,10 @@ size_t prefill_workspace_bytes(const vt_shard_spec& s, int32_t max_tokens, int32
 // Leading workspace bytes that hold the decode kernel's synchronisation words
 // (zero between calls; no other entry point writes them).
 size_t workspace_sync_bytes(const vt_shard_spec& s);
+// vt_layer_decode; with ``clear_sync`` the workspace's synchronisation words
+// are zeroed (by a kernel on ``stream``) once the arguments have passed
+// validation, before the decode launch.
+vt_status layer_decode_ws(const vt_shard_spec* spec, const vt_layer_weights* w, vt_kv_view* kv,
+                          const vt_layer_io* io, int32_t pos, uint32_t phases, void* ws,
+                          size_t ws_bytes, void* stream, bool clear_sync);
 }  // namespace vt

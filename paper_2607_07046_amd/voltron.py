@@ -28,6 +28,7 @@ VT_STAGED = 0x100
 VT_PREC_FP16, VT_PREC_INT8, VT_PREC_INT4, VT_PREC_PRUNED = 0, 1, 2, 3
 VT_W_INT8, VT_W_INT4 = 1, 2
 VT_WS_ERROR_WORD = 8192  # byte offset of the workspace's barrier error word
+VT_NOALLOC_SCRATCH_BYTES = 4 << 20  # the scratch array of vt_layer_decode_noalloc
 
 # every symbol include/voltron.h declares
 EXPORTS = ("vt_shard_spec_create", "vt_shard_spec_query", "vt_shard_spec_destroy",
@@ -35,7 +36,7 @@ EXPORTS = ("vt_shard_spec_create", "vt_shard_spec_query", "vt_shard_spec_destroy
            "vt_qplan", "vt_partial_encode", "vt_partial_decode_add",
            "vt_status_string", "vt_last_error", "vt_quantize_rows", "vt_layer_decode_q",
            "vt_shard_pack", "vt_kv_copy_heads", "vt_moe_workspace_size", "vt_moe_ffn_decode",
-           "vt_stack_decode")
+           "vt_stack_decode", "vt_layer_decode_noalloc")
 
 
 class VoltronError(RuntimeError):
@@ -157,6 +158,9 @@ def load_library(path=None):
     lib.vt_stack_decode.argtypes = [P, ctypes.POINTER(vt_stack_weights),
                                     ctypes.POINTER(vt_kv_stack), ctypes.POINTER(vt_layer_io), I32,
                                     P, SZ, P]
+    lib.vt_layer_decode_noalloc.argtypes = [P, ctypes.POINTER(vt_layer_weights),
+                                            ctypes.POINTER(vt_kv_view),
+                                            ctypes.POINTER(vt_layer_io), I32, U32, P, P]
     lib.vt_moe_workspace_size.argtypes = [P, I32, I32, ctypes.POINTER(SZ)]
     lib.vt_moe_ffn_decode.argtypes = [P, ctypes.POINTER(vt_moe_weights), I32, I32,
                                       ctypes.POINTER(vt_layer_io), P, P, P, SZ, P]
@@ -164,7 +168,8 @@ def load_library(path=None):
                  "vt_workspace_size", "vt_layer_decode", "vt_layer_prefill_chunk",
                  "vt_qplan", "vt_partial_encode", "vt_partial_decode_add",
                  "vt_quantize_rows", "vt_layer_decode_q", "vt_shard_pack", "vt_kv_copy_heads",
-                 "vt_moe_workspace_size", "vt_moe_ffn_decode", "vt_stack_decode"):
+                 "vt_moe_workspace_size", "vt_moe_ffn_decode", "vt_stack_decode",
+                 "vt_layer_decode_noalloc"):
         getattr(lib, name).restype = ctypes.c_int
     lib.vt_status_string.argtypes = [ctypes.c_int]
     lib.vt_status_string.restype = ctypes.c_char_p
@@ -232,6 +237,14 @@ def vt_layer_decode(spec: ShardSpec, w: vt_layer_weights, kv, io: vt_layer_io, p
     _check(load_library().vt_layer_decode(spec.handle, ctypes.byref(w),
                                           ctypes.byref(kv) if kv is not None else None,
                                           ctypes.byref(io), pos, phases, ws, ws_bytes, stream))
+
+
+def vt_layer_decode_noalloc(spec: ShardSpec, w: vt_layer_weights, kv, io: vt_layer_io, pos,
+                            phases, wait_error=None, stream=None):
+    _check(load_library().vt_layer_decode_noalloc(spec.handle, ctypes.byref(w),
+                                                  ctypes.byref(kv) if kv is not None else None,
+                                                  ctypes.byref(io), pos, phases, wait_error,
+                                                  stream))
 
 
 def vt_stack_decode(spec: ShardSpec, w: vt_stack_weights, kv: vt_kv_stack, io: vt_layer_io, pos,

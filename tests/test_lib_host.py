@@ -203,6 +203,30 @@ def test_stack_decode_validation_errors(lib):
     assert kv.len == 128
 
 
+def test_noalloc_decode_rejects_oversized_workspace(lib):
+    """The allocation-free decode holds VT_NOALLOC_SCRATCH_BYTES of scratch:
+    a context whose attention records need more is refused before anything
+    is enqueued (nothing here touches a GPU)."""
+    with open(os.path.join(ROOT, "include", "voltron.h")) as f:
+        hdr = f.read()
+    m = re.search(r"#define\s+VT_NOALLOC_SCRATCH_BYTES\s+\((\d+)u\s*<<\s*(\d+)\)", hdr)
+    assert m and int(m.group(1)) << int(m.group(2)) == vt.VT_NOALLOC_SCRATCH_BYTES
+    spec = _tiny_spec()
+    A = 1 << 20
+    pos = 300000
+    assert vt.vt_workspace_size(spec, 1, pos + 1) > vt.VT_NOALLOC_SCRATCH_BYTES
+    kv = vt.vt_kv_view(k=A, v=A, capacity=pos + 1, n_kv_heads=4, head_dim=64, len=pos)
+    with pytest.raises(vt.VoltronError) as e:
+        vt.vt_layer_decode_noalloc(spec, _fake_weights(), kv, _fake_io(), pos,
+                                   vt.VT_ATTN | vt.VT_FFN)
+    assert e.value.status == vt.VT_ERR_UNSUPPORTED
+    with pytest.raises(vt.VoltronError) as e:
+        vt.vt_layer_decode_noalloc(spec, _fake_weights(), kv, _fake_io(), pos,
+                                   vt.VT_ATTN | vt.VT_FFN, A + 2)
+    assert e.value.status == vt.VT_ERR_ALIGN
+    assert kv.len == pos
+
+
 def test_kv_append_validation_errors(lib):
     A = 1 << 20
     kv = vt.vt_kv_view(k=A, v=A, capacity=10, n_kv_heads=2, head_dim=128, len=4)
