@@ -74,11 +74,14 @@ struct Params {
 // ---------------------------------------------------------------------------
 // phase 1: attention
 //
-// Work item = (query head j, chunk of CL consecutive positions). A thread
-// holds 8 of the d dimensions of one position per pass (d/8 threads per
-// position, PPP positions per pass, CL = passes * PPP). The chunk's keys and
-// values do not depend on phase 0, so they are loaded into registers before
-// the grid barrier. Items of the G query heads that share a KV head and a
+// Work item = (query head j, chunk of CL consecutive cached positions). A
+// thread holds 8 of the d dimensions of one position per pass (d/8 threads
+// per position, PPP positions per pass, CL = passes * PPP). The chunks
+// cover the cached positions p_first..pos-1; the last chunk also takes the
+// new token (its score in one extra slot), so a context of k * CL + 1
+// positions needs k chunks, not k + 1. The chunk's keys and values do not
+// depend on phase 0, so they are loaded into registers before the grid
+// barrier. Items of the G query heads that share a KV head and a
 // chunk are placed on workgroups with equal index mod 8, i.e. on one XCD, so
 // the group reads each K/V tile from HBM once and from that XCD's L2 after.
 // Each item writes (unnormalised sum of p*V, running max m, sum l); the last
@@ -95,7 +98,7 @@ __host__ __device__ __forceinline__ int attn_ppp(int d) { return NT / (d / 8); }
 
 __host__ __device__ __forceinline__ int attn_lds_floats(int d, int nchunk) {
   const int ppp = attn_ppp(d);
-  return d + MAXPASS * ppp + ppp * d + 2 * d + 2 * nchunk + 4;
+  return d + MAXPASS * ppp + 4 + ppp * d + 2 * d + 2 * nchunk + 4;
 }
 
 template <class PT>
@@ -109,10 +112,11 @@ __device__ __forceinline__ void phase_attn(PT& P, int layer, float* lds, bool wa
   const int units = P.nkv * P.nchunk; // (KV head, chunk) pairs
   const int ids = ((units + 7) / 8) * 8 * G;
   const float scale = 1.0f / sqrtf(static_cast<float>(d));
-  // LDS (floats): qs[d] | S[MAXPASS*PPP] | R[PPP*d] | kn[d] | vn[d] | W[2*nchunk] | flag
+  // LDS (floats): qs[d] | S[MAXPASS*PPP + 4] | R[PPP*d] | kn[d] | vn[d] | W[2*nchunk] | flag
+  // (S[CL]: the new token's score in the last chunk)
   float* qs = lds;
   float* S = qs + d;
-  float* R = S + MAXPASS * PPP;
+  float* R = S + MAXPASS * PPP + 4;
   float* kn = R + PPP * d;
   float* vn = kn + d;
   float* W = vn + d;
@@ -176,7 +180,7 @@ __device__ __forceinline__ void phase_attn(PT& P, int layer, float* lds, bool wa
       qs[2 * t] = (qa * c0 - qb * s0) * scale;
       qs[2 * t + 1] = (qa * s0 + qb * c0) * scale;
     }
-    const bool has_new = P.pos >= p0 && P.pos < p0 + CL;
+    const bool has_new = c == P.nchunk - 1;  // the last chunk takes the new token
     if (has_new) {  // the new token's key (rotated) and value, rounded as stored
       const int64_t slot = (static_cast<int64_t>(g) * P.cap + P.pos) * d;
       const bool writer = jj == 0;  // one item per KV head appends to the cache
@@ -205,25 +209,28 @@ __device__ __forceinline__ void phase_attn(PT& P, int layer, float* lds, bool wa
         const int p = p0 + ps * PPP + pl;
         float kf[8];
         unpack8(kr[ps], kf);
-        if (p == P.pos) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) kf[e] = kn[dc + e];
-        }
         float sc = 0.f;
 #pragma unroll
         for (int e = 0; e < 8; ++e) sc = fmaf(qs[dc + e], kf[e], sc);
         sc = group_sum(sc, TPP);
-        if ((t % TPP) == 0) S[ps * PPP + pl] = p <= P.pos ? sc : -INFINITY;
+        if ((t % TPP) == 0) S[ps * PPP + pl] = p < P.pos ? sc : -INFINITY;  // cached positions only
       }
+    }
+    if (t < TPP) {  // the new token's score (its key as stored), in slot CL
+      float sc = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) sc = fmaf(qs[dc + e], kn[dc + e], sc);
+      sc = group_sum(sc, TPP);
+      if (t == 0) S[CL] = has_new ? sc : -INFINITY;
     }
     __syncthreads();
     float* rec = P.part + (static_cast<int64_t>(j) * P.nchunk + c) * RW;
     if (wave == 0) {  // softmax statistics of the chunk
       float mx = -INFINITY;
-      for (int q = lane; q < CL; q += kWave) mx = fmaxf(mx, S[q]);
+      for (int q = lane; q <= CL; q += kWave) mx = fmaxf(mx, S[q]);
       mx = wave_max(mx);
       float l = 0.f;
-      for (int q = lane; q < CL; q += kWave) {
+      for (int q = lane; q <= CL; q += kWave) {
         const float e = S[q] == -INFINITY ? 0.f : __expf(S[q] - mx);
         S[q] = e;
         l += e;
@@ -240,17 +247,17 @@ __device__ __forceinline__ void phase_attn(PT& P, int layer, float* lds, bool wa
 #pragma unroll
     for (int ps = 0; ps < MAXPASS; ++ps) {
       if (ps < NPASS) {
-        const int p = p0 + ps * PPP + pl;
         const float e = S[ps * PPP + pl];
         float vf[8];
         unpack8(vr[ps], vf);
-        if (p == P.pos) {
-#pragma unroll
-          for (int x = 0; x < 8; ++x) vf[x] = vn[dc + x];
-        }
 #pragma unroll
         for (int x = 0; x < 8; ++x) acc[x] = fmaf(e, vf[x], acc[x]);
       }
+    }
+    if (t < TPP && has_new) {  // the new token's value (position group 0)
+      const float e = S[CL];
+#pragma unroll
+      for (int x = 0; x < 8; ++x) acc[x] = fmaf(e, vn[dc + x], acc[x]);
     }
     // two 16-byte stores per thread: eight scalar ones put a wave's 64
     // lanes on a few LDS banks (measured 1.0 us slower per step)
@@ -654,7 +661,8 @@ struct DecodeWs {
   size_t sync, qkv, part, o, m, hbuf, total;
 };
 
-// Chunking of the attention phase: the chunk length is a whole number of
+// Chunking of the attention phase over the L cached positions attended
+// (the new token joins the last chunk): the chunk length is a whole number of
 // passes (at most MAXPASS) chosen so that the (query head, chunk) items fill
 // the grid about once.
 static void attn_chunking(int d, int nq, int L, int grid, int* cl, int* nchunk) {
@@ -663,7 +671,7 @@ static void attn_chunking(int d, int nq, int L, int grid, int* cl, int* nchunk) 
   int passes = (L + ppp * target - 1) / (ppp * target);
   passes = std::min(dec::MAXPASS, std::max(1, passes));
   *cl = passes * ppp;
-  *nchunk = (L + *cl - 1) / *cl;
+  *nchunk = std::max(1, (L + *cl - 1) / *cl);
 }
 
 static DecodeWs decode_ws_layout(const vt_shard_spec& s, int32_t max_ctx) {
@@ -1026,7 +1034,7 @@ static vt_status decode_impl(const vt_shard_spec* spec, const WeightView& W, vt_
   P.pos = pos;
   P.p_first = p_first;
   P.cap = kv ? kv->capacity : 0;
-  attn_chunking(D.head_dim, in.n_q_heads, ctx - p_first, di->cus, &P.cl, &P.nchunk);
+  attn_chunking(D.head_dim, in.n_q_heads, attn ? pos - p_first : 0, di->cus, &P.cl, &P.nchunk);
   P.eps = D.rms_eps;
   P.rope_base = D.rope_base;
   P.g_attn = static_cast<const uint16_t*>(W.g_attn);
