@@ -279,14 +279,16 @@ def stack_headline(wl, steps, warmup, per_layer_tokens):
     return res
 
 
-def chain_section(wl, steps, warmup):
+def chain_section(wl, steps, warmup, emit=False):
     """A single-layer decode workload: step i decodes weight/KV copy i mod R
     (R copies, >= 768 MB in all, so the Infinity Cache cannot serve the
     weights) at the workload's position and feeds its y to step i+1 as x.
     Steps are captured in HIP graphs keyed by (first step mod the rotation
     length, count), so every window continues the rotation and the chain
     where the previous one stopped; a window holds up to about 128 steps (a
-    whole number of rotations), so graph launches do not add to the step."""
+    whole number of rotations), so graph launches do not add to the step.
+    ``emit``: each step also emits both partial sums quantised
+    (vt_layer_decode_emit) under plans that halve the fp16 message."""
     import torch
 
     from paper_2607_07046_amd import pack
@@ -318,6 +320,19 @@ def chain_section(wl, steps, warmup):
     bufs = [x0.clone(), torch.empty_like(x0)]
     p_attn, h, p_ffn = (torch.empty(H, dtype=torch.float16, device="cuda") for _ in range(3))
     both = vt.VT_ATTN | vt.VT_FFN
+    em = None
+    if emit:
+        nb = H // 32
+        rng = np.random.default_rng(11)
+        eplan = {}
+        for name in ("attn", "ffn"):
+            prec, offs, total = vt.vt_qplan(rng.random(nb).astype(np.float32), nb * 64 // 2)
+            eplan[name] = (torch.from_numpy(prec).cuda(), torch.from_numpy(offs).cuda(),
+                          torch.zeros(max(16, total), dtype=torch.uint8, device="cuda"), total)
+        em = vt.vt_emit(prec_attn=eplan["attn"][0].data_ptr(), off_attn=eplan["attn"][1].data_ptr(),
+                        msg_attn=eplan["attn"][2].data_ptr(), msg_attn_bytes=eplan["attn"][3],
+                        prec_ffn=eplan["ffn"][0].data_ptr(), off_ffn=eplan["ffn"][1].data_ptr(),
+                        msg_ffn=eplan["ffn"][2].data_ptr(), msg_ffn_bytes=eplan["ffn"][3])
 
     def enqueue(i, stream):
         _, stw, _, _, kvv = layers[i % copies]
@@ -325,7 +340,11 @@ def chain_section(wl, steps, warmup):
         io = vt.vt_layer_io(x=bufs[i % 2].data_ptr(), peer_attn=None, peer_ffn=None,
                             attn_partial=p_attn.data_ptr(), h=h.data_ptr(),
                             ffn_partial=p_ffn.data_ptr(), y=bufs[(i + 1) % 2].data_ptr())
-        vt.vt_layer_decode(spec, stw, kvv, io, pos, both, ws.data_ptr(), ws_bytes, stream)
+        if em is not None:
+            vt.vt_layer_decode_emit(spec, stw, kvv, io, pos, both, em, ws.data_ptr(), ws_bytes,
+                                    stream)
+        else:
+            vt.vt_layer_decode(spec, stw, kvv, io, pos, both, ws.data_ptr(), ws_bytes, stream)
 
     group = copies * (2 if copies % 2 else 1)  # the copy and buffer pattern repeats after this
     unit = group * max(1, 128 // group)       # steps per window (whole rotations)
@@ -392,6 +411,10 @@ def chain_section(wl, steps, warmup):
         "roofline": roofline(step_bytes, ms_step, "decode_kernel<0, 4, 0, false>", wl.key),
         "launch": "persistent + hipgraph (windows keyed by rotation phase)",
     }
+    if emit:
+        out["emit"] = {name: {"message_bytes": eplan[name][3], "fp16_bytes": 2 * H}
+                       for name in ("attn", "ffn")}
+        out["roofline"] = None  # the roofline block belongs to the plain step
     res = (out, spec, dims, info, enqueue, copies, w0)
     return res
 
@@ -471,6 +494,13 @@ def main():
             else:
                 del enq, w0
             torch.cuda.empty_cache()
+        if args.comm_steps > 0:
+            # the 7B step emitting both partial sums quantised from its epilogues
+            sec, *_ = chain_section(get("7b"), args.decode_steps, max(1, args.decode_steps // 10),
+                                    emit=True)
+            out["decode_7b_emit"] = {k: sec[k] for k in ("ms_per_step", "tokens_s", "emit", "launch")}
+            out["decode_7b_emit"]["us_over_plain_step"] = round(
+                (sec["ms_per_step"] - out["decode_7b"]["ms_per_step"]) * 1e3, 2)
     if args.prefill_steps > 0:
         out["prefill"] = prefill_section(args.prefill_steps, max(1, args.prefill_steps // 10))
     if args.comm_steps > 0:

@@ -469,6 +469,36 @@ vt_status vt_partial_encode(const void* p, int32_t n, const uint8_t* prec, const
 vt_status vt_partial_decode_add(const void* msg, size_t msg_bytes, int32_t n, const uint8_t* prec,
                                 const int32_t* offsets, const void* base, void* out, void* stream);
 
+/* The same quantised messages emitted by the decode step itself: the O and
+ * down projections' epilogues give each workgroup whole blocks of 32 output
+ * rows, so a block's partial sums leave in the message as soon as they are
+ * formed, with no further launch. For each partial (attention: io->
+ * attn_partial; FFN: io->ffn_partial), a plan in device memory (prec and
+ * offsets of hidden / 32 blocks, as vt_qplan writes them) and a message
+ * buffer of msg_bytes (device); the bytes written equal what
+ * vt_partial_encode writes for that partial vector, and nothing is written
+ * outside [msg, msg + msg_bytes). A NULL message is not emitted. */
+typedef struct vt_emit {
+  const uint8_t* prec_attn;
+  const int32_t* off_attn;
+  void* msg_attn;
+  size_t msg_attn_bytes;
+  const uint8_t* prec_ffn;
+  const int32_t* off_ffn;
+  void* msg_ffn;
+  size_t msg_ffn_bytes;
+} vt_emit;
+
+/* vt_layer_decode (fp16 weights, persistent launch) that also emits the
+ * quantised partial sums per ``emit``. Outputs as vt_layer_decode, equal to
+ * it up to the fp32 summation order of each row. VT_ERR_UNSUPPORTED with
+ * VT_STAGED or when hidden is not a multiple of 32; VT_ERR_ARG when a
+ * message is given without a plan or for a phase that does not run. */
+vt_status vt_layer_decode_emit(const vt_shard_spec* spec, const vt_layer_weights* w,
+                               vt_kv_view* kv, const vt_layer_io* io, int32_t pos,
+                               uint32_t phases, const vt_emit* emit, void* ws, size_t ws_bytes,
+                               void* stream);
+
 /* Static text of a status code. */
 const char* vt_status_string(vt_status s);
 

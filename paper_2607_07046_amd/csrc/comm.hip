@@ -6,15 +6,8 @@
 // importance-ordered lowering of Sec. 4.2.2). The receiver reconstructs the
 // values and adds them to its own sum.
 //
-// Message layout: blocks in index order, block b at offsets[b]:
-//   FP16   64 B: the 32 fp16 values
-//   INT8   36 B: fp32 scale s, 32 int8 codes           value = code * s
-//   INT4   20 B: fp32 scale s, 16 bytes of two 4-bit two's-complement codes,
-//                element 2k in the low nibble of byte k
-//   PRUNED  0 B: value 0
-// s = absmax / Q (fp32 division; Q = 127 or 7), code = clamp(rint(x / s),
-// -Q, Q) with x / s an fp32 division and rint rounding half to even; an
-// all-zero block has s = 0 and codes 0.
+// Message layout: blocks in index order, block b at offsets[b]; the block
+// format and quantiser are in comm_block.hpp.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -22,6 +15,7 @@
 #include <numeric>
 #include <vector>
 
+#include "comm_block.hpp"
 #include "device.hpp"
 #include "internal.hpp"
 
@@ -31,9 +25,7 @@ namespace comm {
 constexpr int BLK = 32;
 constexpr int CT = 256;  // threads per workgroup: 8 blocks (one per half-wave)
 
-__host__ __device__ __forceinline__ int block_bytes(int level) {
-  return level == VT_PREC_FP16 ? 64 : level == VT_PREC_INT8 ? 36 : level == VT_PREC_INT4 ? 20 : 0;
-}
+__host__ __device__ __forceinline__ int block_bytes(int level) { return comm_block_bytes(level); }
 
 // One half-wave per block. Every lane takes part in the shuffles (blocks past
 // the end act as pruned); every store goes through the message's buffer
@@ -47,32 +39,7 @@ __global__ void __launch_bounds__(CT) encode_kernel(const uint16_t* p, int nblk,
   const int level = valid ? prec[b] : VT_PREC_PRUNED;
   const int64_t o = valid ? offsets[b] : 0;
   const uint16_t raw = valid ? p[static_cast<int64_t>(b) * BLK + i] : 0;
-  const float x = h2f(raw);
-  float a = fabsf(x);
-#pragma unroll
-  for (int m = 1; m < BLK; m <<= 1) a = fmaxf(a, __shfl_xor(a, m, kWave));  // stays in the half-wave
-  const float qm = level == VT_PREC_INT8 ? 127.f : 7.f;
-  const float s = __fdiv_rn(a, qm);
-  float c = a == 0.f ? 0.f : __builtin_rintf(__fdiv_rn(x, s));
-  c = fminf(fmaxf(c, -qm), qm);
-  const int ci = static_cast<int>(c);
-  const int next = __shfl_down(ci, 1, kWave);  // the odd neighbour's code (INT4 packing)
-
-  const rsrc_t rm = make_rsrc(msg, msg_bytes);
-  auto at = [&](int64_t off, int len) -> uint32_t {  // kOOB unless [off, off + len) fits
-    return (o >= 0 && off + len <= static_cast<int64_t>(msg_bytes)) ? static_cast<uint32_t>(off) : kOOB;
-  };
-  if (level == VT_PREC_FP16) {
-    __builtin_amdgcn_raw_buffer_store_b16(raw, rm, at(o + 2 * i, 2), 0, 0);
-  } else if (level == VT_PREC_INT8 || level == VT_PREC_INT4) {
-    if (i == 0) __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, s), rm, at(o, 4), 0, 0);
-    if (level == VT_PREC_INT8) {
-      __builtin_amdgcn_raw_buffer_store_b8(static_cast<uint8_t>(ci & 0xFF), rm, at(o + 4 + i, 1), 0, 0);
-    } else if ((i & 1) == 0) {
-      const uint8_t byte = static_cast<uint8_t>((ci & 0xF) | ((next & 0xF) << 4));
-      __builtin_amdgcn_raw_buffer_store_b8(byte, rm, at(o + 4 + i / 2, 1), 0, 0);
-    }
-  }
+  comm_encode_block_lanes(raw, i, level, o, make_rsrc(msg, msg_bytes), msg_bytes);
 }
 
 // out[i] = fp16(base[i] + value[i]) with value = code * s (fp32 multiply,

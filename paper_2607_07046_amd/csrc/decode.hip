@@ -32,6 +32,7 @@
 #include <mutex>
 #include <vector>
 
+#include "comm_block.hpp"
 #include "device.hpp"
 #include "gemv.hpp"
 #include "internal.hpp"
@@ -69,6 +70,13 @@ struct Params {
   int64_t lst_w[7];    // bytes between consecutive layers' q, k, v, o, gate, up, down values / codes
   int64_t lst_s[7];    // the same for their block scales
   int64_t lst_kv;      // elements between consecutive layers' K (and V) caches
+  // Quantised emission of the partial sums (the COMM instantiation): plan
+  // (precision and byte offset per block of 32) and message of each partial;
+  // a NULL message is not emitted.
+  const uint8_t *eprec_a, *eprec_f;
+  const int32_t *eoff_a, *eoff_f;
+  uint8_t *emsg_a, *emsg_f;
+  uint32_t emsg_a_bytes, emsg_f_bytes;
 };
 
 // ---------------------------------------------------------------------------
@@ -360,8 +368,9 @@ __device__ __forceinline__ void phase_attn(PT& P, int layer, float* lds, bool wa
 // the kernel
 // ---------------------------------------------------------------------------
 // One phase of layer ``layer``; ``wait``: a grid barrier is in front of it,
-// the ``nbar``-th of the launch.
-template <int PH, int F, class PT>
+// the ``nbar``-th of the launch. COMM: the O and down phases give each
+// workgroup whole blocks of 32 output rows and emit the quantised partials.
+template <int PH, int F, bool COMM, class PT>
 __device__ __forceinline__ void run_phase(PT& P, int layer, float* lds, uint16_t* xs, float* slots,
                                           float* red, bool wait, unsigned nbar) {
   uint16_t* scl = reinterpret_cast<uint16_t*>(red + 16);  // block scales (quantised formats)
@@ -437,20 +446,29 @@ __device__ __forceinline__ void run_phase(PT& P, int layer, float* lds, uint16_t
     uint16_t* const pa_out = P.p_attn + io;
     uint16_t* const h_out = P.h + io;
     const uint16_t* const peer = P.peer_a ? P.peer_a + io : nullptr;
-    gemv_phase<1, F>(
-        rows, P.H, K, xs, slots, scl,
-        [&]() {
-          if (wait) grid_wait(P.sync, nbar);
-          stage_copy_f(P.o, K, padded(K, F), xs);
-        },
-        [&](int r, const float* v) {
-          const float pa = v[0];
-          pa_out[r] = f2h(pa);
-          const float xr = h2f(x_shared ? ld_h16_shared(x + r) : x[r]);
-          const float hv = xr + pa + (peer ? h2f(peer[r]) : 0.f);
-          h_out[r] = f2h(hv);
-          st_shared(P.hbuf + r, hv);
-        });
+    auto stage = [&]() {
+      if (wait) grid_wait(P.sync, nbar);
+      stage_copy_f(P.o, K, padded(K, F), xs);
+    };
+    auto epi = [&](int r, float pa) {
+      pa_out[r] = f2h(pa);
+      const float xr = h2f(x_shared ? ld_h16_shared(x + r) : x[r]);
+      const float hv = xr + pa + (peer ? h2f(peer[r]) : 0.f);
+      h_out[r] = f2h(hv);
+      st_shared(P.hbuf + r, hv);
+    };
+    if constexpr (COMM) {
+      // whole blocks of 32 rows per workgroup: the block's quantised message
+      // (paper Sec. 4.3.2) leaves with the partial sums, lane j holding row j
+      gemv_phase<32, F>(rows, P.H / 32, K, xs, slots, scl, stage, [&](int blk, int j, float v) {
+        epi(blk * 32 + j, v);
+        if (P.emsg_a)
+          comm_encode_block_lanes(f2h(v), j, P.eprec_a[blk], P.eoff_a[blk],
+                                  make_rsrc(P.emsg_a, P.emsg_a_bytes), P.emsg_a_bytes);
+      });
+    } else {
+      gemv_phase<1, F>(rows, P.H, K, xs, slots, scl, stage, [&](int r, const float* v) { epi(r, v[0]); });
+    }
   } else if constexpr (PH == PH_GATEUP) {
     RowsPair rows{wmat(4, PW.wg, PW.ld_g, PW.ncols, PW.sg, PW.lds_g),
                   wmat(5, PW.wu, PW.ld_u, PW.ncols, PW.su, PW.lds_u)};
@@ -476,36 +494,43 @@ __device__ __forceinline__ void run_phase(PT& P, int layer, float* lds, uint16_t
     const uint16_t* const peer = P.peer_f ? P.peer_f + io : nullptr;
     // a stacked layer's y is the next layer's x: written through the coherent path
     const bool y_shared = layer + 1 < P.n_layers;
-    gemv_phase<1, F>(
-        rows, P.H, K, xs, slots, scl,
-        [&]() {
-          if (wait) grid_wait(P.sync, nbar);
-          stage_copy_f(P.m, K, padded(K, F), xs);
-        },
-        [&](int r, const float* v) {
-          const float pf = v[0];
-          pf_out[r] = f2h(pf);
-          if (y_out) {
-            const float hr = P.h_from_ws ? round_h(ld_shared(P.hbuf + r)) : h2f(P.h[io + r]);
-            const uint16_t yv = f2h(hr + pf + (peer ? h2f(peer[r]) : 0.f));
-            if (y_shared)
-              st_h16_shared(y_out + r, yv);
-            else
-              y_out[r] = yv;
-          }
-        });
+    auto stage = [&]() {
+      if (wait) grid_wait(P.sync, nbar);
+      stage_copy_f(P.m, K, padded(K, F), xs);
+    };
+    auto epi = [&](int r, float pf) {
+      pf_out[r] = f2h(pf);
+      if (y_out) {
+        const float hr = P.h_from_ws ? round_h(ld_shared(P.hbuf + r)) : h2f(P.h[io + r]);
+        const uint16_t yv = f2h(hr + pf + (peer ? h2f(peer[r]) : 0.f));
+        if (y_shared)
+          st_h16_shared(y_out + r, yv);
+        else
+          y_out[r] = yv;
+      }
+    };
+    if constexpr (COMM) {
+      gemv_phase<32, F>(rows, P.H / 32, K, xs, slots, scl, stage, [&](int blk, int j, float v) {
+        epi(blk * 32 + j, v);
+        if (P.emsg_f)
+          comm_encode_block_lanes(f2h(v), j, P.eprec_f[blk], P.eoff_f[blk],
+                                  make_rsrc(P.emsg_f, P.emsg_f_bytes), P.emsg_f_bytes);
+      });
+    } else {
+      gemv_phase<1, F>(rows, P.H, K, xs, slots, scl, stage, [&](int r, const float* v) { epi(r, v[0]); });
+    }
   }
 }
 
-template <int PH, int PE, int PB, int F, class PT>
+template <int PH, int PE, int PB, int F, bool COMM, class PT>
 __device__ __forceinline__ void run_phases(PT& P, int layer, float* lds, uint16_t* xs, float* slots,
                                            float* red) {
   // barriers so far in this launch: (PE - PB + 1) per earlier layer
   const unsigned nbar = static_cast<unsigned>(layer * (PE - PB + 1) + PH - PB);
-  run_phase<PH, F>(P, layer, lds, xs, slots, red, nbar > 0, nbar);
+  run_phase<PH, F, COMM>(P, layer, lds, xs, slots, red, nbar > 0, nbar);
   if constexpr (PH < PE) {
     grid_arrive(P.sync);
-    run_phases<PH + 1, PE, PB, F>(P, layer, lds, xs, slots, red);
+    run_phases<PH + 1, PE, PB, F, COMM>(P, layer, lds, xs, slots, red);
   }
 }
 
@@ -514,7 +539,7 @@ __device__ __forceinline__ void run_phases(PT& P, int layer, float* lds, uint16_
 // CU): grid barriers separate the phases and the layers. Params must stay
 // the only kernel argument (run_phase reads it from the start of the
 // argument segment).
-template <int PB, int PE, int F, bool STACK = false>
+template <int PB, int PE, int F, bool STACK = false, bool COMM = false>
 __global__ void __launch_bounds__(NT) decode_kernel(Params P) {
   extern __shared__ float lds[];
   // LDS: xs / attention scratch (aliased) | slots[MAX_SLOTS] | red[16] |
@@ -534,10 +559,10 @@ __global__ void __launch_bounds__(NT) decode_kernel(Params P) {
       KParams* pp = (KParams*)__builtin_amdgcn_kernarg_segment_ptr();
       asm volatile("" : "+s"(pp));
       if (layer > 0) grid_arrive(pp->sync);
-      run_phases<PB, PE, PB, F>(*pp, layer, lds, xs, slots, red);
+      run_phases<PB, PE, PB, F, COMM>(*pp, layer, lds, xs, slots, red);
     }
   } else {
-    run_phases<PB, PE, PB, F>(P, 0, lds, xs, slots, red);
+    run_phases<PB, PE, PB, F, COMM>(P, 0, lds, xs, slots, red);
   }
   if constexpr (PE > PB || STACK) grid_exit(P.sync);
 }
@@ -564,6 +589,14 @@ __host__ inline DecodeKernel decode_kernel_fmt(int pb, int pe) {
 
 // The persistent kernel of a stack of fp16 layers (all phases, layer loop).
 __host__ inline DecodeKernel decode_stack_kernel() { return decode_kernel<PH_QKV, PH_DOWN, FMT_F16, true>; }
+
+// fp16 decode that also emits the quantised partial sums (persistent only).
+__host__ inline DecodeKernel decode_comm_kernel(int pb, int pe) {
+  if (pb == PH_QKV && pe == PH_DOWN) return decode_kernel<PH_QKV, PH_DOWN, FMT_F16, false, true>;
+  if (pb == PH_QKV && pe == PH_O) return decode_kernel<PH_QKV, PH_O, FMT_F16, false, true>;
+  if (pb == PH_GATEUP && pe == PH_DOWN) return decode_kernel<PH_GATEUP, PH_DOWN, FMT_F16, false, true>;
+  return nullptr;
+}
 
 __host__ inline DecodeKernel decode_kernel_for(int pb, int pe, int fmt) {
   switch (fmt) {
@@ -645,6 +678,10 @@ vt_status device_info(DeviceInfo** out) {
                                   static_cast<int>(di.max_lds));
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(dec::decode_stack_kernel()),
                               hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(di.max_lds));
+    for (const auto& r : ranges)
+      if (dec::decode_comm_kernel(r[0], r[1]))
+        (void)hipFuncSetAttribute(reinterpret_cast<const void*>(dec::decode_comm_kernel(r[0], r[1])),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(di.max_lds));
     (void)hipGetLastError();
     di.lds_attr_set = true;
   }
@@ -891,6 +928,7 @@ struct StackView {
   int64_t lst_w[7] = {0, 0, 0, 0, 0, 0, 0};
   int64_t lst_kv = 0;
   bool clear_sync = false;  // zero the workspace's synchronisation words first
+  const vt_emit* emit = nullptr;  // emit the quantised partial sums (fp16, persistent)
 };
 
 static vt_status decode_impl(const vt_shard_spec* spec, const WeightView& W, vt_kv_view* kv,
@@ -951,6 +989,48 @@ extern "C" vt_status vt_layer_decode_q(const vt_shard_spec* spec, const vt_layer
     W.lds[i] = m[i]->ld_scales * 2;
   }
   return decode_impl(spec, W, kv, io, pos, phases, ws, ws_bytes, stream);
+}
+
+extern "C" vt_status vt_layer_decode_emit(const vt_shard_spec* spec, const vt_layer_weights* w,
+                                          vt_kv_view* kv, const vt_layer_io* io, int32_t pos,
+                                          uint32_t phases, const vt_emit* emit, void* ws,
+                                          size_t ws_bytes, void* stream) {
+  clear_error();
+  vt_status st = check_phases(spec, io, phases);
+  if (st != VT_OK) return st;
+  if (!emit) return fail(VT_ERR_ARG, "null emit description");
+  if (phases & VT_STAGED) return fail(VT_ERR_UNSUPPORTED, "emission runs in the persistent launch only");
+  if (spec->dims.hidden % 32) return fail(VT_ERR_UNSUPPORTED, "hidden %d is not a multiple of 32", spec->dims.hidden);
+  auto msg = [&](const uint8_t* prec, const int32_t* off, const void* m, size_t bytes, bool on,
+                 const char* name) -> vt_status {
+    if (!m) return VT_OK;
+    if (!on) return fail(VT_ERR_ARG, "%s message given but its phase does not run", name);
+    if (!prec || !off) return fail(VT_ERR_ARG, "%s message without a plan", name);
+    if (reinterpret_cast<uintptr_t>(off) % 4) return fail(VT_ERR_ALIGN, "%s offsets not 4-byte aligned", name);
+    if (bytes >= static_cast<size_t>(kMaxBufferBytes))
+      return fail(VT_ERR_UNSUPPORTED, "%s message of %zu bytes; at most 2 GiB", name, bytes);
+    return VT_OK;
+  };
+  if ((st = msg(emit->prec_attn, emit->off_attn, emit->msg_attn, emit->msg_attn_bytes, phases & VT_ATTN,
+                "attention")) != VT_OK)
+    return st;
+  if ((st = msg(emit->prec_ffn, emit->off_ffn, emit->msg_ffn, emit->msg_ffn_bytes, phases & VT_FFN, "FFN")) !=
+      VT_OK)
+    return st;
+  if ((st = check_weights(*spec, w, phases & VT_ATTN, phases & VT_FFN)) != VT_OK) return st;
+  WeightView W{};
+  W.fmt = dec::FMT_F16;
+  W.g_attn = w->g_attn;
+  W.g_ffn = w->g_ffn;
+  const void* ptrs[7] = {w->wq, w->wk, w->wv, w->wo, w->wg, w->wu, w->wd};
+  const int64_t lds[7] = {w->ld_q, w->ld_k, w->ld_v, w->ld_o, w->ld_g, w->ld_u, w->ld_d};
+  for (int i = 0; i < 7; ++i) {
+    W.w[i] = ptrs[i];
+    W.ld[i] = lds[i] * 2;
+  }
+  StackView S;
+  S.emit = emit;
+  return decode_impl(spec, W, kv, io, pos, phases, ws, ws_bytes, stream, S);
 }
 
 extern "C" vt_status vt_stack_decode(const vt_shard_spec* spec, const vt_stack_weights* w,
@@ -1072,6 +1152,16 @@ static vt_status decode_impl(const vt_shard_spec* spec, const WeightView& W, vt_
   P.n_layers = S.n_layers;
   for (int i = 0; i < 7; ++i) P.lst_w[i] = S.lst_w[i];
   P.lst_kv = S.lst_kv;
+  if (S.emit) {
+    P.eprec_a = S.emit->prec_attn;
+    P.eoff_a = S.emit->off_attn;
+    P.emsg_a = static_cast<uint8_t*>(S.emit->msg_attn);
+    P.emsg_a_bytes = static_cast<uint32_t>(S.emit->msg_attn_bytes);
+    P.eprec_f = S.emit->prec_ffn;
+    P.eoff_f = S.emit->off_ffn;
+    P.emsg_f = static_cast<uint8_t*>(S.emit->msg_ffn);
+    P.emsg_f_bytes = static_cast<uint32_t>(S.emit->msg_ffn_bytes);
+  }
 
   const int kmax = std::max({dec::padded(P.H, W.fmt), dec::padded(P.nq * P.d, W.fmt),
                              dec::padded(P.ncols, W.fmt)});
@@ -1093,7 +1183,9 @@ static vt_status decode_impl(const vt_shard_spec* spec, const WeightView& W, vt_
   const bool stack = S.n_layers > 1;
   if (stack && (staged || W.fmt != dec::FMT_F16 || pb != dec::PH_QKV || pe != dec::PH_DOWN))
     return fail(VT_ERR_UNSUPPORTED, "a stack runs fp16 layers, all phases, one launch");
-  const dec::DecodeKernel kern = stack ? dec::decode_stack_kernel() : dec::decode_kernel_for(pb, pe, W.fmt);
+  const dec::DecodeKernel kern = stack    ? dec::decode_stack_kernel()
+                                 : S.emit ? dec::decode_comm_kernel(pb, pe)
+                                          : dec::decode_kernel_for(pb, pe, W.fmt);
   if (!staged) {
     int per_cu = 0;
     e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, dec::NT, lds);

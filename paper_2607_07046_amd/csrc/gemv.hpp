@@ -276,6 +276,8 @@ constexpr int SC_PER_WAVE = (SC_ROWS + NW - 1) / NW;
 // in each lane and reducing across the wave at the row's end (or where its
 // sub-run ends) into slots[piece]. ``epi(unit, sums)`` gets each unit's U
 // row sums, added in piece order (a fixed order: bitwise reproducible).
+// With U == 32 (units of 32 rows) the epilogue is ``epi(unit, j, sum of row
+// j)`` on lane j of a half-wave instead.
 template <int U, int F, int SCW, class Rows, class Pre, class Stage, class Epi>
 __device__ __forceinline__ void gemv_impl(const Rows& rows, int units, int K, const uint16_t* xs16,
                                           float* slots, uint16_t* scl, Pre pre, Stage stage, Epi epi) {
@@ -423,18 +425,32 @@ __device__ __forceinline__ void gemv_impl(const Rows& rows, int units, int K, co
     for (int tr = 0; tr + 1 < ntrip; ++tr) trip(q0 + tr * PF, true);
     if (ntrip > 0) trip(q0 + (ntrip - 1) * PF, false);
     lds_barrier();  // every slot written
-    for (int lu = threadIdx.x; lu < ub - ua; lu += NT) {
-      float v[U];
-#pragma unroll
-      for (int j = 0; j < U; ++j) {
+    if constexpr (U == 32) {
+      // a half-wave per unit, lane j taking its row j (the loop bound is
+      // uniform over each half-wave, so the epilogue may use its shuffles)
+      for (int lu = threadIdx.x / 32; lu < ub - ua; lu += NT / 32) {
+        const int j = threadIdx.x % 32;
         float a = 0.f;
         if (K > 0) {
           const float* sl = slots + (lu * U + j) * nseg;
           for (int s = 0; s < nseg; ++s) a += sl[s];
         }
-        v[j] = a;
+        epi(ua + lu, j, a);
       }
-      epi(ua + lu, v);
+    } else {
+      for (int lu = threadIdx.x; lu < ub - ua; lu += NT) {
+        float v[U];
+#pragma unroll
+        for (int j = 0; j < U; ++j) {
+          float a = 0.f;
+          if (K > 0) {
+            const float* sl = slots + (lu * U + j) * nseg;
+            for (int s = 0; s < nseg; ++s) a += sl[s];
+          }
+          v[j] = a;
+        }
+        epi(ua + lu, v);
+      }
     }
     lds_barrier();  // slots, scales and xs free for reuse
     ua = ub;

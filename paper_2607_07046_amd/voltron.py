@@ -36,7 +36,7 @@ EXPORTS = ("vt_shard_spec_create", "vt_shard_spec_query", "vt_shard_spec_destroy
            "vt_qplan", "vt_partial_encode", "vt_partial_decode_add",
            "vt_status_string", "vt_last_error", "vt_quantize_rows", "vt_layer_decode_q",
            "vt_shard_pack", "vt_kv_copy_heads", "vt_moe_workspace_size", "vt_moe_ffn_decode",
-           "vt_stack_decode", "vt_layer_decode_noalloc")
+           "vt_stack_decode", "vt_layer_decode_noalloc", "vt_layer_decode_emit")
 
 
 class VoltronError(RuntimeError):
@@ -95,6 +95,13 @@ class vt_kv_view(ctypes.Structure):
     _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p),
                 ("capacity", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("len", ctypes.c_int32)]
+
+
+class vt_emit(ctypes.Structure):
+    _fields_ = [("prec_attn", ctypes.c_void_p), ("off_attn", ctypes.c_void_p),
+                ("msg_attn", ctypes.c_void_p), ("msg_attn_bytes", ctypes.c_size_t),
+                ("prec_ffn", ctypes.c_void_p), ("off_ffn", ctypes.c_void_p),
+                ("msg_ffn", ctypes.c_void_p), ("msg_ffn_bytes", ctypes.c_size_t)]
 
 
 class vt_stack_weights(ctypes.Structure):
@@ -161,6 +168,9 @@ def load_library(path=None):
     lib.vt_layer_decode_noalloc.argtypes = [P, ctypes.POINTER(vt_layer_weights),
                                             ctypes.POINTER(vt_kv_view),
                                             ctypes.POINTER(vt_layer_io), I32, U32, P, P]
+    lib.vt_layer_decode_emit.argtypes = [P, ctypes.POINTER(vt_layer_weights),
+                                         ctypes.POINTER(vt_kv_view), ctypes.POINTER(vt_layer_io),
+                                         I32, U32, ctypes.POINTER(vt_emit), P, SZ, P]
     lib.vt_moe_workspace_size.argtypes = [P, I32, I32, ctypes.POINTER(SZ)]
     lib.vt_moe_ffn_decode.argtypes = [P, ctypes.POINTER(vt_moe_weights), I32, I32,
                                       ctypes.POINTER(vt_layer_io), P, P, P, SZ, P]
@@ -169,7 +179,7 @@ def load_library(path=None):
                  "vt_qplan", "vt_partial_encode", "vt_partial_decode_add",
                  "vt_quantize_rows", "vt_layer_decode_q", "vt_shard_pack", "vt_kv_copy_heads",
                  "vt_moe_workspace_size", "vt_moe_ffn_decode", "vt_stack_decode",
-                 "vt_layer_decode_noalloc"):
+                 "vt_layer_decode_noalloc", "vt_layer_decode_emit"):
         getattr(lib, name).restype = ctypes.c_int
     lib.vt_status_string.argtypes = [ctypes.c_int]
     lib.vt_status_string.restype = ctypes.c_char_p
@@ -245,6 +255,14 @@ def vt_layer_decode_noalloc(spec: ShardSpec, w: vt_layer_weights, kv, io: vt_lay
                                                   ctypes.byref(kv) if kv is not None else None,
                                                   ctypes.byref(io), pos, phases, wait_error,
                                                   stream))
+
+
+def vt_layer_decode_emit(spec: ShardSpec, w: vt_layer_weights, kv, io: vt_layer_io, pos, phases,
+                         emit: vt_emit, ws, ws_bytes, stream=None):
+    _check(load_library().vt_layer_decode_emit(spec.handle, ctypes.byref(w),
+                                               ctypes.byref(kv) if kv is not None else None,
+                                               ctypes.byref(io), pos, phases, ctypes.byref(emit), ws,
+                                               ws_bytes, stream))
 
 
 def vt_stack_decode(spec: ShardSpec, w: vt_stack_weights, kv: vt_kv_stack, io: vt_layer_io, pos,

@@ -130,3 +130,120 @@ def test_decode_step_partial_sent_quantized():
             half_step = 0.0 if level == C.FP16 else np.max(np.abs(p[sl])) / C.QMAX[level] / 2
             bound = 1.05 * half_step + 2e-2 * np.maximum(np.abs(p[sl]), rms)
             assert np.all(np.abs(recv[sl] - p[sl]) <= bound), (budget, b, level)
+
+
+def emit_case(wl, plans, staged=False, msg_bytes=None, li=None):
+    """vt_layer_decode_emit with per-partial plans {'attn': (prec, offs, total), 'ffn': ...}:
+    returns the outputs, the two messages (host bytes, filled with 0xA5 past what
+    was written) and the device plan tensors."""
+    li = li or LayerInputs(wl)
+    gs = GpuShard(wl, li=li)
+    x = li.x(2)
+    H = gs.dims.hidden
+    xt = torch.from_numpy(x).cuda()
+    out = {k: torch.full((H,), float("nan"), dtype=torch.float16, device="cuda")
+           for k in ("p_attn", "h", "p_ffn", "y")}
+    dv = {}
+    for name in ("attn", "ffn"):
+        prec, offs, total = plans[name]
+        cap = max(16, total + 64)
+        dv[name] = (dev(prec.astype(np.uint8)), dev(offs.astype(np.int32)),
+                    torch.full((cap,), 0xA5, dtype=torch.uint8, device="cuda"), total)
+    em = vt.vt_emit(prec_attn=dv["attn"][0].data_ptr(), off_attn=dv["attn"][1].data_ptr(),
+                    msg_attn=dv["attn"][2].data_ptr(),
+                    msg_attn_bytes=dv["attn"][3] if msg_bytes is None else msg_bytes,
+                    prec_ffn=dv["ffn"][0].data_ptr(), off_ffn=dv["ffn"][1].data_ptr(),
+                    msg_ffn=dv["ffn"][2].data_ptr(),
+                    msg_ffn_bytes=dv["ffn"][3] if msg_bytes is None else msg_bytes)
+    io = vt.vt_layer_io(x=xt.data_ptr(), peer_attn=None, peer_ffn=None,
+                        attn_partial=out["p_attn"].data_ptr(), h=out["h"].data_ptr(),
+                        ffn_partial=out["p_ffn"].data_ptr(), y=out["y"].data_ptr())
+    vt.vt_layer_decode_emit(gs.spec, gs.w.struct, gs.kv, io, wl.ctx,
+                            vt.VT_ATTN | vt.VT_FFN | (vt.VT_STAGED if staged else 0), em,
+                            gs.ws.data_ptr(), gs.ws_bytes, None)
+    torch.cuda.synchronize()
+    got = {k: v.float().cpu().numpy().astype(np.float64) for k, v in out.items()}
+    msgs = {k: dv[k][2].cpu().numpy() for k in dv}
+    assert not np.any(gs.sync_words()), "synchronisation words not cleared"
+    return gs, x, got, msgs, dv
+
+
+def plans_for(nb, rng, kind):
+    if kind == "mixed":
+        return {n: vt.vt_qplan(rng.random(nb).astype(np.float32), int(nb * 64 * f))
+                for n, f in (("attn", 0.45), ("ffn", 0.3))}
+    p = plan_for(kind, nb, rng)
+    return {"attn": p, "ffn": p}
+
+
+@pytest.mark.parametrize("kind", ["mixed", "fp16", "int8", "int4", "pruned"])
+@pytest.mark.parametrize("key", ["tiny", "7b", "70b_gqa"])
+def test_decode_emits_quantized_partials(key, kind):
+    """The O and down epilogues emit exactly the message vt_partial_encode
+    makes of the same call's partial sums; the decode outputs still match
+    the oracle; a received partial is within the quantisation bound of the
+    oracle's."""
+    from synth import get
+    from tests.common import assert_close, ffn_at_h16, oracle_shard_weights
+    wl = get(key)
+    li = LayerInputs(wl)
+    nb = wl.dims.hidden // 32
+    plans = plans_for(nb, np.random.default_rng(21), kind)
+    gs, x, got, msgs, dv = emit_case(wl, plans, li=li)
+    for name, part in (("attn", "p_attn"), ("ffn", "p_ffn")):
+        prec, offs, total = plans[name]
+        ref_msg, *_ = run_encode(got[part].astype(np.float16), prec, offs, total)
+        assert np.array_equal(msgs[name][:total], ref_msg[:total]), name
+        assert np.all(msgs[name][total:] == 0xA5), name      # nothing past the message
+    kc, vc = gs.context()
+    r = oracle_ranges(wl)
+    ref = oracle_decode(wl, li, r, x, kc, vc, wl.ctx)
+    for k in ("p_attn", "h", "p_ffn", "y"):
+        assert_close(got[k], ref[k], f"{key} {kind} {k}")
+    # the attention partial as the aggregating device receives it
+    prec, offs, total = plans["attn"]
+    n = wl.dims.hidden
+    outr = torch.empty(n, dtype=torch.float16, device="cuda")
+    vt.vt_partial_decode_add(dv["attn"][2].data_ptr(), total, n, dv["attn"][0].data_ptr(),
+                             dv["attn"][1].data_ptr(), None, outr.data_ptr())
+    torch.cuda.synchronize()
+    recv = outr.float().cpu().numpy().astype(np.float64)
+    p = ref["p_attn"]
+    rms = np.sqrt(np.mean(p * p))
+    for b in range(nb):
+        sl = slice(32 * b, 32 * b + 32)
+        level = int(prec[b])
+        if level == C.PRUNED:
+            assert not recv[sl].any()
+            continue
+        half_step = 0.0 if level == C.FP16 else np.max(np.abs(p[sl])) / C.QMAX[level] / 2
+        bound = 1.05 * half_step + 2e-2 * np.maximum(np.abs(p[sl]), 0.2 * rms)
+        assert np.all(np.abs(recv[sl] - p[sl]) <= bound), (key, kind, b, level)
+
+
+def test_emit_message_bounded_by_its_size():
+    """A message buffer shorter than the plan: bytes past msg_bytes stay as
+    they were (the epilogue's stores are range-checked)."""
+    wl = tiny_workload(402, 512, 8, 8, 64, 1000, (0.5, 0.5), 1, 32, sigma=0.03)
+    nb = 512 // 32
+    plans = plans_for(nb, np.random.default_rng(3), "int8")
+    total = plans["attn"][2]
+    gs, x, got, msgs, dv = emit_case(wl, plans, msg_bytes=total // 2)
+    for name, part in (("attn", "p_attn"), ("ffn", "p_ffn")):
+        prec, offs, tot = plans[name]
+        ref_msg, *_ = run_encode(got[part].astype(np.float16), prec, offs, tot)
+        half = total // 2
+        # blocks that fit entirely below msg_bytes are written; nothing at or past it
+        assert np.all(msgs[name][half:] == 0xA5), name
+        whole = [b for b in range(nb) if offs[b] + 36 <= half]
+        for b in whole:
+            assert np.array_equal(msgs[name][offs[b]:offs[b] + 36], ref_msg[offs[b]:offs[b] + 36])
+
+
+def test_emit_rejects_staged_and_planless_messages():
+    wl = tiny_workload(403, 512, 8, 8, 64, 1000, (0.5, 0.5), 0, 16, sigma=0.03)
+    nb = 512 // 32
+    plans = plans_for(nb, np.random.default_rng(4), "fp16")
+    with pytest.raises(vt.VoltronError) as e:
+        emit_case(wl, plans, staged=True)
+    assert e.value.status == vt.VT_ERR_UNSUPPORTED
