@@ -1063,7 +1063,7 @@ def prefill_section(steps, warmup, eager=False):
         "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
         "bound_us": round(max(flops / (MFMA_F16_PEAK_TFLOPS * 1e12),
                               nbytes / (HBM_PEAK_GBPS * 1e9)) * 1e6, 2),
-        "launch": "10 kernels per chunk, " + ("eager" if eager else "hipgraph"),
+        "launch": "6 kernels per chunk, " + ("eager" if eager else "hipgraph"),
     }
 
 

@@ -194,7 +194,8 @@ vt_status vt_kv_append(vt_kv_view* kv, const void* k, const void* v, int32_t n_t
  * 32-bit error word at byte offset VT_WS_ERROR_WORD of the workspace to
  * nonzero instead of hanging; the call's outputs are then undefined. The
  * library never clears that word: a caller that checks it reads it after
- * synchronising and zeroes it itself. */
+ * synchronising and zeroes it itself. A prefill chunk's GEMMs wait only for
+ * workgroups that are already running, under the same bound and report. */
 #define VT_WS_ERROR_WORD 8192
 vt_status vt_workspace_size(const vt_shard_spec* spec, int32_t max_tokens,
                             int32_t max_ctx, size_t* bytes);

@@ -5,16 +5,20 @@
 // tensor-parallel shard of Sec. 3.2.1 each device does its heads and FFN
 // columns. For T tokens at positions pos0..pos0+T-1 the projections are
 // dense GEMMs (M = T), run here on fp16 MFMA (v_mfma_f32_32x32x16_f16) with
-// fp32 accumulation:
-//   rmsnorm_rows   U = fp16(RMSNorm(X) * g_attn)
-//   gemm           QKV = U [Wq; Wk; Wv]^T              (fp32 out)
-//   rope_append    Q = fp16(RoPE(q) / sqrt(d)); K, V -> cache at pos0+t
+// fp32 accumulation; every elementwise step runs in the epilogue of the
+// GEMM that produces its input:
+//   rmsnorm_rows   U = fp16(RMSNorm(X) * g_attn), and the rotary angles
+//   gemm  QKV      [q | k | v] = U [Wq; Wk; Wv]^T; epilogue: Q = fp16(RoPE(q)
+//                  / sqrt(d)), K = fp16(RoPE(k)) and V = fp16(v) into the
+//                  cache at positions pos0 + t
 //   attn_prefill   O = causal softmax(Q K^T) V, token t sees 0..pos0+t
-//   gemm           P_attn = O Wo^T; H = X + P_attn + peer (epilogue)
-//   rmsnorm_rows   W = fp16(RMSNorm(H) * g_ffn)
-//   gemm           GU = W [Wg; Wu]^T                   (fp32 out)
-//   silu_gate      M = fp16(silu(G) * U), zero-padded to the row stride
-//   gemm           P_ffn = M Wd^T; Y = H + P_ffn + peer (epilogue)
+//   gemm  O        P_attn = O Wo^T; epilogue: H = fp16(X + P_attn + peer),
+//                  the FFN input fp16(H * g_ffn) and per-tile sums of H^2
+//   gemm  gate/up  G, Up = (H * g_ffn) [Wg | Wu]^T, gate and up rows
+//                  interleaved in blocks of 64; epilogue: the RMSNorm's
+//                  1 / rms per token from the sums of H^2 scales G and Up,
+//                  M = fp16(silu(G) * Up)
+//   gemm  down     P_ffn = M Wd^T; epilogue: Y = fp16(H + P_ffn + peer)
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -43,15 +47,46 @@ __device__ __forceinline__ int64_t kmajor(int k, int m, int M) {
   return (static_cast<int64_t>(k >> 4) * M + m) * 16 + (k & 15);
 }
 
+// Lane-group sums through DPP (no LDS round trip): dpp_xor1 adds lane l ^ 1;
+// sum16 leaves every lane of each aligned group of 16 with the group's sum.
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float dpp_xor1(float v) { return v + dpp_mov<0xB1>(v); }  // quad_perm [1,0,3,2]
+__device__ __forceinline__ float sum16(float v) {
+  v = dpp_xor1(v);
+  v += dpp_mov<0x4E>(v);   // quad_perm [2,3,0,1]: the quad's sum
+  v += dpp_mov<0x141>(v);  // row_half_mirror: the other quad of the 8
+  v += dpp_mov<0x140>(v);  // row_mirror: the other 8 of the 16
+  return v;
+}
+
+// Split sp's share of a tile sum: the own registers for the own split.
+__device__ __forceinline__ f32x4 sp_pick(int sp, int split, f32x4 own, f32x4 loaded) {
+  return sp == split ? own : loaded;
+}
+
+// The 8 halves of w with those at index >= v set to zero.
+__device__ __forceinline__ u32x4 zero_past(u32x4 w, int v) {
+  w.x = v >= 2 ? w.x : (v >= 1 ? (w.x & 0xFFFFu) : 0u);
+  w.y = v >= 4 ? w.y : (v >= 3 ? (w.y & 0xFFFFu) : 0u);
+  w.z = v >= 6 ? w.z : (v >= 5 ? (w.z & 0xFFFFu) : 0u);
+  w.w = v >= 8 ? w.w : (v >= 7 ? (w.w & 0xFFFFu) : 0u);
+  return w;
+}
+
 // ---------------------------------------------------------------------------
-// Split-K GEMM   P[s][m][n] = sum over k-slice s of A[m][k] * B[n][k]
-// (fp16 in, fp32 out). M is the chunk's tokens, N the shard's output
-// features, K the input features (a multiple of 8). A is k-step-major (see
-// kmajor) with zeros past K; B is row-major. The weights (B) are the large
-// operand and are streamed once; A is small and re-read from L2 by every N
-// tile. The K range is cut into ``splits`` slices so that one launch has
-// about one workgroup per compute unit; each slice writes its own fp32 slab
-// and the consumer kernel adds the slabs (no atomics, fixed summation order).
+// Split-K GEMM   C[m][n] = sum over k of A[m][k] * B[n][k]  (fp16 in, fp32
+// accumulate), followed by one of four epilogues (EPI_*) that turns the
+// 128 x 128 output tile into the layer's next operands. M is the chunk's
+// tokens, N the shard's output features, K the input features. A is
+// k-step-major (see kmajor) with zeros past K; B is row-major. The weights
+// (B) are the large operand and are streamed once; A is small and re-read
+// from L2 by every N tile. The K range is cut into ``splits`` slices so that
+// one launch has about one workgroup per compute unit; the slices of a tile
+// meet through a counter, and the last to arrive adds them in slice order
+// (a fixed summation order) and runs the epilogue.
 //
 // Tile 128 tokens x 128 features x 64 k per 256-thread workgroup, two
 // workgroups per compute unit (one's barrier and LDS waits are covered by the
@@ -75,9 +110,15 @@ constexpr int KSTEPS = GBK / 16;           // MFMA k-steps per k-tile
 constexpr int RING = 2 * KSTEPS;           // A k-steps in flight
 constexpr int B_CH = GBN * GBK / 8 / GT;   // 16-byte B chunks per thread per k-tile
 constexpr int STAGE = GBN * GLD;           // halves per LDS stage
-constexpr int GEMM_LDS_BYTES = 2 * STAGE * 2;
+constexpr int TLD = GBN + 4;               // LDS row of the epilogue's fp32 tile
+// two B stages in the main loop; the fp32 output tile and a per-token
+// factor in the epilogue (two workgroups per compute unit still fit)
+constexpr int GEMM_LDS_BYTES = (GBM * TLD + GBM) * 4 > 2 * STAGE * 2 ? (GBM * TLD + GBM) * 4 : 2 * STAGE * 2;
+static_assert(2 * GEMM_LDS_BYTES <= 160 * 1024, "two workgroups per compute unit");
 constexpr int GEMM_SLOTS = 512;            // two workgroups per compute unit
-constexpr int MAX_SPLITS = 8;
+constexpr int MAX_SPLITS = 4;
+constexpr unsigned kWaitLimit = 1u << 22;  // polls of the split-K wait: far beyond any slice's stores
+
 
 struct BSrc {
   const uint16_t* p;
@@ -85,14 +126,36 @@ struct BSrc {
   int start, rows;  // virtual rows [start, start + rows); start a multiple of 8
 };
 
+// What the last split of an output tile does with the summed tile.
+enum { EPI_QKV = 0, EPI_O = 1, EPI_GU = 2, EPI_DOWN = 3 };
+
 struct GemmArgs {
   const uint16_t* A;  // k-step-major, ceil(K / 16) k-steps of M tokens
   BSrc b[3];
   int nb;
-  float* P;
-  int64_t ldp, slab;
+  int interleave;     // b[0] and b[1] rows interleaved in blocks of 64 (gate/up)
+  float* P;           // split-K partial tiles (fragment order)
+  unsigned* cnt;      // per output tile: slices arrived, slices stored (zero at launch)
+  unsigned* err;      // the workspace's error word (set if a wait ever times out)
   int M, N, K;
   int m_tiles, n_tiles, splits, kps;  // kps: k-tiles per split
+  int epi;
+  // epilogue operands (fp16 unless stated; [M][H] row-major)
+  int H;
+  float eps;
+  const uint16_t* base;  // O: x; DOWN: h
+  const uint16_t* peer;  // nullable
+  uint16_t* partial;     // O: attention partial; DOWN: FFN partial
+  uint16_t* out;         // O: h; DOWN: y (nullable)
+  const uint16_t* gain;  // O: g_ffn when the FFN follows (else NULL)
+  uint16_t* U;           // O: FFN input fp16(h * g_ffn), k-step-major
+  float* rowsq;          // O: [M][n_tiles] sums of h^2 over each tile's columns; GU: read (NULL: 1 / rms = 1)
+  int rowsq_tiles;       // GU: column tiles of the O GEMM
+  uint16_t *Q, *kc, *vc; // QKV outputs: Q [M][nq][d], the KV cache [n_kv][cap][d]
+  const float* rope;     // [M][d / 2][2] cos, sin of each rotary angle
+  int nq, nkv, d, cap, pos0;
+  uint16_t* Mo;          // GU: fp16(silu(G) * Up), k-step-major, kpad columns
+  int F, kpad;
 };
 
 __global__ void __launch_bounds__(GT, 2) gemm_kernel(GemmArgs g) {
@@ -143,13 +206,18 @@ __global__ void __launch_bounds__(GT, 2) gemm_kernel(GemmArgs g) {
 #pragma unroll
   for (int u = 0; u < B_CH; ++u) {
     const int r0 = n0 + wave * 8 + u * 32;  // first row of this wave's 8-row group (uniform)
-    int j = 2;
-    if (r0 < g.b[1].start || g.nb < 2) j = 0;
-    else if (r0 < g.b[2].start || g.nb < 3) j = 1;
+    const int n = n0 + (t + u * GT) / 8;
+    int j = 2, r;
+    if (g.interleave) {  // blocks of 64 rows alternate between b[0] and b[1]
+      j = (r0 / 64) % 2;
+      r = (n / 128) * 64 + n % 64;
+    } else {
+      if (r0 < g.b[1].start || g.nb < 2) j = 0;
+      else if (r0 < g.b[2].start || g.nb < 3) j = 1;
+      r = n - (j == 0 ? g.b[0].start : (j == 1 ? g.b[1].start : g.b[2].start));
+    }
     const BSrc src = j == 0 ? g.b[0] : (j == 1 ? g.b[1] : g.b[2]);
     rsel[u] = j == 0 ? rs[0] : (j == 1 ? rs[1] : rs[2]);
-    const int n = n0 + (t + u * GT) / 8;
-    const int r = n - src.start;
     boff[u] = (n < g.N && r >= 0 && r < src.rows) ? static_cast<uint32_t>(r * src.ld * 2) : kOOB;
   }
   auto load_b = [&](int kt, u32x4 (&vb)[B_CH]) {  // k-tile kt (absolute)
@@ -159,7 +227,14 @@ __global__ void __launch_bounds__(GT, 2) gemm_kernel(GemmArgs g) {
     for (int u = 0; u < B_CH; ++u)
       vb[u] = buf_load16(rsel[u], (boff[u] + static_cast<uint32_t>(k) * 2u) | out | (boff[u] & kOOB));
   };
-  auto store_b = [&](uint16_t* st, const u32x4 (&vb)[B_CH]) {
+  // k-tile kt into LDS; a chunk that straddles K keeps only its columns
+  // below K (the row padding past K may hold anything)
+  auto store_b = [&](uint16_t* st, u32x4 (&vb)[B_CH], int kt) {
+    if (g.K & 7) {
+      const int v = g.K - (kt * GBK + ccol);
+#pragma unroll
+      for (int u = 0; u < B_CH; ++u) vb[u] = zero_past(vb[u], v);
+    }
 #pragma unroll
     for (int u = 0; u < B_CH; ++u)
       *reinterpret_cast<u32x4*>(st + ((t + u * GT) / 8) * GLD + ccol) = vb[u];
@@ -198,7 +273,7 @@ __global__ void __launch_bounds__(GT, 2) gemm_kernel(GemmArgs g) {
   for (int s = 0; s < RING; ++s) load_a(s, ar[s]);
   load_b(kt0, rb0);
   load_b(kt0 + 1, rb1);
-  store_b(L0, rb0);
+  store_b(L0, rb0, kt0);
   __syncthreads();
   // two k-tiles per trip; an odd count runs one all-zero tile at the end
   // (the scheduling barriers keep the B prefetch ahead of the MFMAs)
@@ -206,61 +281,334 @@ __global__ void __launch_bounds__(GT, 2) gemm_kernel(GemmArgs g) {
     load_b(kt0 + i + 2, rb0);
     __builtin_amdgcn_sched_barrier(0);
     compute(L0, i * KSTEPS, 0);
-    store_b(L1, rb1);
+    store_b(L1, rb1, kt0 + i + 1);
     __syncthreads();
     load_b(kt0 + i + 3, rb1);
     __builtin_amdgcn_sched_barrier(0);
     compute(L1, (i + 1) * KSTEPS, KSTEPS);
-    store_b(L0, rb0);
+    store_b(L0, rb0, kt0 + i + 2);
     __syncthreads();
   }
 
-  // accumulator i of tile b: token 8(i/4) + 4(l/32) + i%4, feature l%32
-  float* out = g.P + split * g.slab;
+  // Split-K: the slices of a tile take arrival tickets when their k range
+  // is done. All but the last to arrive park their sums in their slot of
+  // the partial buffer (fragment order: each lane's 64 values as 16
+  // contiguous 16-byte chunks, chunk-major over the workgroup, so each
+  // store and load instruction moves 4 KiB contiguously) and count
+  // themselves stored; the last waits for those stores, which are already
+  // under way (every slice it waits for has arrived, so is running), adds
+  // the slices in slice order (its own from registers: the order, and so
+  // the result, does not depend on which slice arrives last) and runs the
+  // epilogue. Tiles cross XCDs through the agent-scope coherent path.
+  // The epilogue's global inputs (rotary table rows; residual base and
+  // peer rows and the FFN gain; the tokens' partial sums of squares) are
+  // loaded ahead of the split-K wait and reduction, so their round trip
+  // overlaps those. Thread t takes features f..f+7 (f = 8 (t%16)) of tokens
+  // t / 16 + 16 j of the tile; for the gate/up epilogue, the first RQ
+  // partial sums of half t % 2 of token t / 2.
+  constexpr int RJ = GBM / 16;
+  const int ef = 8 * (t % 16), en = n0 + ef;
+  const int qd = g.nq * g.d, kd = g.nkv * g.d;
+  constexpr int RQ = 16;
+  const int nt = g.rowsq_tiles, half = t % 2;
+  const int q0 = half * ((nt + 1) / 2), q1 = half ? nt : (nt + 1) / 2;
+  u32x4 pre[2 * RJ], pre_g;
+  auto prefetch = [&]() {
+    if (g.epi == EPI_QKV) {
+      if (en < g.N && en < qd + kd) {
+        const int c = (en < qd ? en : en - qd) % g.d;
+#pragma unroll
+        for (int j = 0; j < RJ; ++j) {
+          const int m = m0 + t / 16 + 16 * j;
+          if (m < g.M) {
+            const float* cs = g.rope + (static_cast<int64_t>(m) * (g.d / 2) + c / 2) * 2;
+            pre[2 * j] = *reinterpret_cast<const u32x4*>(cs);
+            pre[2 * j + 1] = *reinterpret_cast<const u32x4*>(cs + 4);
+          }
+        }
+      }
+    } else if (g.epi == EPI_O || g.epi == EPI_DOWN) {
+      if (en < g.N) {
+#pragma unroll
+        for (int j = 0; j < RJ; ++j) {
+          const int m = m0 + t / 16 + 16 * j;
+          const int64_t e = static_cast<int64_t>(m) * g.H + en;
+          if (m < g.M) {
+            pre[j] = load16(g.base + e);
+            if (g.peer) pre[RJ + j] = load16(g.peer + e);
+          }
+        }
+        if (g.epi == EPI_O && g.gain) pre_g = load16(g.gain + en);
+      }
+    } else if (g.rowsq) {  // EPI_GU
+      const int m = m0 + t / 2;
+      if (m < g.M) {
+        float* rq = reinterpret_cast<float*>(pre);
+#pragma unroll
+        for (int k = 0; k < RQ; ++k)
+          if (q0 + k < q1) rq[k] = g.rowsq[static_cast<int64_t>(m) * nt + q0 + k];
+      }
+    }
+  };
+
+  if (g.splits > 1) {
+    __shared__ unsigned ticket;
+    const int tile = m_tile * g.n_tiles + n_tile;
+    unsigned* arrived = g.cnt + 2 * tile;
+    unsigned* stored = arrived + 1;
+    const int64_t tile_floats = static_cast<int64_t>(GBM) * GBN;
+    const uint32_t tile_bytes = static_cast<uint32_t>(tile_floats * 4);
+    auto slot = [&](int sp) {
+      return make_rsrc(g.P + (static_cast<int64_t>(sp) * g.m_tiles * g.n_tiles + tile) * tile_floats,
+                       sp < g.splits ? tile_bytes : 0u);
+    };
+    auto chunk_off = [&](int c) { return static_cast<uint32_t>(((c * GT) + t) * 16); };
+    if (t == 0) ticket = __hip_atomic_fetch_add(arrived, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    if (ticket != static_cast<unsigned>(g.splits - 1)) {
+      const rsrc_t mine = slot(split);
+#pragma unroll
+      for (int c = 0; c < 16; ++c) {
+        const f32x4 v = f32x4{acc[c / 4][4 * (c % 4)], acc[c / 4][4 * (c % 4) + 1], acc[c / 4][4 * (c % 4) + 2],
+                              acc[c / 4][4 * (c % 4) + 3]};
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), mine, chunk_off(c), 0, kCoherent);
+      }
+      mem_done();
+      __syncthreads();
+      if (t == 0) __hip_atomic_fetch_add(stored, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      return;
+    }
+    prefetch();
+    if (t == 0) {
+      unsigned n = 0;
+      while (__hip_atomic_load(stored, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) <
+             static_cast<unsigned>(g.splits - 1)) {
+        __builtin_amdgcn_s_sleep(1);
+        if (++n > kWaitLimit) {  // never expected: report instead of hanging
+          __hip_atomic_fetch_or(g.err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          break;
+        }
+      }
+    }
+    __syncthreads();
+    // At most MAX_SPLITS slices; those past g.splits read zero (an empty
+    // range) and are added last, which leaves the sum unchanged. A quarter
+    // of the tile at a time, every load is issued before the first add, so
+    // the slices' data arrive in one memory round trip per quarter.
+    rsrc_t sr[MAX_SPLITS];
+#pragma unroll
+    for (int sp = 0; sp < MAX_SPLITS; ++sp) sr[sp] = slot(sp);
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      f32x4 v[4][MAX_SPLITS];
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int sp = 0; sp < MAX_SPLITS; ++sp)
+          v[c][sp] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                   sr[sp], sp == split ? kOOB : chunk_off(4 * h + c), 0, kCoherent));
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int cc = 4 * h + c;
+        const f32x4 own = f32x4{acc[cc / 4][4 * (cc % 4)], acc[cc / 4][4 * (cc % 4) + 1],
+                                acc[cc / 4][4 * (cc % 4) + 2], acc[cc / 4][4 * (cc % 4) + 3]};
+        f32x4 sum = sp_pick(0, split, own, v[c][0]);
+#pragma unroll
+        for (int sp = 1; sp < MAX_SPLITS; ++sp) sum += sp_pick(sp, split, own, v[c][sp]);
+        acc[cc / 4][4 * (cc % 4)] = sum.x;
+        acc[cc / 4][4 * (cc % 4) + 1] = sum.y;
+        acc[cc / 4][4 * (cc % 4) + 2] = sum.z;
+        acc[cc / 4][4 * (cc % 4) + 3] = sum.w;
+      }
+    }
+  } else {
+    prefetch();
+  }
+
+  // The summed tile goes through LDS (fp32, rows of TLD floats) so that the
+  // epilogue reads rows of 8 consecutive features per thread: every global
+  // access below is one 16-byte load or store, and 16 consecutive threads
+  // cover one token's 128 features.
+  // Accumulator i of tile b: token 8(i/4) + 4(l/32) + i%4 of the wave's 32,
+  // feature b * 32 + l%32.
+  float* tl = reinterpret_cast<float*>(lds);
 #pragma unroll
   for (int b = 0; b < 4; ++b)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int m = m0 + wave * 32 + 8 * (i / 4) + 4 * (lane / 32) + i % 4;
-      const int n = n0 + b * 32 + lane % 32;
-      if (m < g.M && n < g.N) out[m * g.ldp + n] = acc[b][i];
+    for (int i = 0; i < 16; ++i)
+      tl[(wave * 32 + 8 * (i / 4) + 4 * (lane / 32) + i % 4) * TLD + b * 32 + lane % 32] = acc[b][i];
+  __syncthreads();
+  // k-step-major outputs (the next GEMM's activation operand) are staged as
+  // fp16 in the first half of each token's LDS row (written over values its
+  // own wave has already read) and then copied out with consecutive threads
+  // on consecutive tokens, so each k-step's 16 features of the tile's tokens
+  // leave as one contiguous run.
+  auto stage8 = [&](int mm, int f, u32x4 v) {
+    *reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(tl + mm * TLD) + f) = v;
+  };
+  auto copy_kmajor = [&](uint16_t* dst, int groups, int col0, int limit) {
+    __syncthreads();
+    for (int q = t / GBM; q < groups; q += GT / GBM) {
+      const int mm = t % GBM, m = m0 + mm, col = col0 + 16 * q;
+      if (m < g.M && col < limit) {
+        const uint16_t* src = reinterpret_cast<const uint16_t*>(tl + mm * TLD) + 16 * q;
+        uint16_t* o = dst + kmajor(col, m, g.M);
+        *reinterpret_cast<u32x4*>(o) = *reinterpret_cast<const u32x4*>(src);
+        *reinterpret_cast<u32x4*>(o + 8) = *reinterpret_cast<const u32x4*>(src + 8);
+      }
     }
-}
+  };
+  auto row8 = [&](int mm, int f, float (&v)[8]) {
+    const f32x4 lo = *reinterpret_cast<const f32x4*>(tl + mm * TLD + f);
+    const f32x4 hi = *reinterpret_cast<const f32x4*>(tl + mm * TLD + f + 4);
+    v[0] = lo.x; v[1] = lo.y; v[2] = lo.z; v[3] = lo.w;
+    v[4] = hi.x; v[5] = hi.y; v[6] = hi.z; v[7] = hi.w;
+  };
 
-// Sum over the S split-K slabs of 4 consecutive fp32 values at element i
-// (i a multiple of 4); all S loads are issued before the adds.
-template <int S>
-__device__ __forceinline__ f32x4 slab_sum4(const float* P, int64_t slab, int64_t i) {
-  f32x4 v[S];
+  if (g.epi == EPI_QKV) {
+    // features f..f+7 of one head; rotary pairs (2c, 2c+1) are adjacent
+    const int f = ef, n = en;
+    if (n < g.N) {
+      const bool rot = n < qd + kd;
+      const int c = (n < qd ? n : n - qd) % g.d;
+      const float sc = n < qd ? 1.0f / sqrtf(static_cast<float>(g.d)) : 1.f;
 #pragma unroll
-  for (int s = 0; s < S; ++s) v[s] = *reinterpret_cast<const f32x4*>(P + s * slab + i);
+      for (int j = 0; j < RJ; ++j) {
+        const int mm = t / 16 + 16 * j, m = m0 + mm;
+        if (m >= g.M) break;
+        float v[8];
+        row8(mm, f, v);
+        uint16_t h[8];
+        if (rot) {
+          const f32x4 r0 = __builtin_bit_cast(f32x4, pre[2 * j]), r1 = __builtin_bit_cast(f32x4, pre[2 * j + 1]);
+          const float co[4] = {r0.x, r0.z, r1.x, r1.z}, si[4] = {r0.y, r0.w, r1.y, r1.w};
 #pragma unroll
-  for (int s = 1; s < S; ++s) v[0] += v[s];
-  return v[0];
-}
-
-template <int S>
-__device__ __forceinline__ float slab_sum1(const float* P, int64_t slab, int64_t i) {
-  float v[S];
+          for (int p = 0; p < 4; ++p) {
+            h[2 * p] = f2h((v[2 * p] * co[p] - v[2 * p + 1] * si[p]) * sc);
+            h[2 * p + 1] = f2h((v[2 * p] * si[p] + v[2 * p + 1] * co[p]) * sc);
+          }
+          uint16_t* dst = n < qd ? g.Q + (static_cast<int64_t>(m) * g.nq + n / g.d) * g.d + c
+                                 : g.kc + (static_cast<int64_t>((n - qd) / g.d) * g.cap + g.pos0 + m) * g.d + c;
+          *reinterpret_cast<u32x4*>(dst) = pack8(h);
+        } else {
+          const int nv = n - qd - kd;
 #pragma unroll
-  for (int s = 0; s < S; ++s) v[s] = P[s * slab + i];
+          for (int e = 0; e < 8; ++e) h[e] = f2h(v[e]);
+          *reinterpret_cast<u32x4*>(g.vc + (static_cast<int64_t>(nv / g.d) * g.cap + g.pos0 + m) * g.d + nv % g.d) =
+              pack8(h);
+        }
+      }
+    }
+  } else if (g.epi == EPI_O || g.epi == EPI_DOWN) {
+    // partial = fp16(p); out = fp16(base + p + peer); for O with the FFN to
+    // follow also the FFN input fp16(out * g_ffn) and each token's sum of
+    // out^2 over this tile's 128 columns (the RMSNorm is finished by the
+    // gate/up epilogue)
+    const bool norm = g.epi == EPI_O && g.gain;
+    const int f = ef, n = en;
+    const int hpad = (g.H + 15) / 16 * 16;
+    const bool in = n < g.N;
+    float gg[8];
+    if (norm && in) unpack8(pre_g, gg);
 #pragma unroll
-  for (int s = 1; s < S; ++s) v[0] += v[s];
-  return v[0];
+    for (int j = 0; j < RJ; ++j) {
+      const int mm = t / 16 + 16 * j, m = m0 + mm;
+      if (m >= g.M) break;  // uniform over each group of 16 threads
+      float sq = 0.f;
+      if (in) {
+        float v[8], b[8], pe[8];
+        row8(mm, f, v);
+        const int64_t e = static_cast<int64_t>(m) * g.H + n;
+        unpack8(pre[j], b);
+        if (g.peer) unpack8(pre[RJ + j], pe);
+        uint16_t ph[8], oh[8], uh[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          ph[k] = f2h(v[k]);
+          oh[k] = f2h(b[k] + v[k] + (g.peer ? pe[k] : 0.f));
+          if (norm) {
+            const float o = h2f(oh[k]);
+            sq = fmaf(o, o, sq);
+            uh[k] = f2h(o * gg[k]);
+          }
+        }
+        *reinterpret_cast<u32x4*>(g.partial + e) = pack8(ph);
+        if (g.out) *reinterpret_cast<u32x4*>(g.out + e) = pack8(oh);
+        if (norm) stage8(mm, f, pack8(uh));
+      } else if (norm && n < hpad) {
+        stage8(mm, f, u32x4{0u, 0u, 0u, 0u});  // K padding
+      }
+      if (norm) {
+        sq = sum16(sq);
+        if (t % 16 == 0) g.rowsq[static_cast<int64_t>(m) * g.n_tiles + n_tile] = sq;
+      }
+    }
+    if (norm) copy_kmajor(g.U, GBN / 16, n0, hpad);
+  } else {  // EPI_GU: tile features 0..63 gate and 64..127 up of the same 64 columns
+    float* rinv = tl + GBM * TLD;  // 1 / rms of the tile's tokens
+    if (g.rowsq) {
+      // thread t: token t / 2 of the tile, column tiles q0..q1-1 (half t % 2)
+      const int mm = t / 2, m = m0 + mm;
+      float ss = 0.f;
+      if (m < g.M) {
+        const float* rq = reinterpret_cast<const float*>(pre);
+#pragma unroll
+        for (int k = 0; k < RQ; ++k)
+          if (q0 + k < q1) ss += rq[k];
+        for (int k = q0 + RQ; k < q1; ++k) ss += g.rowsq[static_cast<int64_t>(m) * nt + k];
+      }
+      ss = dpp_xor1(ss);
+      if (half == 0) rinv[mm] = 1.0f / sqrtf(ss / static_cast<float>(g.H) + g.eps);
+    } else if (t < GBM) {
+      rinv[t] = 1.f;
+    }
+    __syncthreads();
+    const int f = 8 * (t % 8), col0 = (n0 / 128) * 64, col = col0 + f;
+    if (col < g.kpad) {
+#pragma unroll 2
+      for (int j = 0; j < GBM / 32; ++j) {
+        const int mm = t / 8 + 32 * j, m = m0 + mm;
+        if (m >= g.M) break;
+        float gt[8], up[8];
+        row8(mm, f, gt);
+        row8(mm, 64 + f, up);
+        const float r = rinv[mm];
+        uint16_t h[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const float a = gt[k] * r;
+          h[k] = f2h(a / (1.0f + __expf(-a)) * (up[k] * r));
+        }
+        stage8(mm, f, pack8(h));
+      }
+    }
+    copy_kmajor(g.Mo, 4, col0, g.kpad);
+  }
 }
 
 // ---------------------------------------------------------------------------
 // row-wise helpers
 // ---------------------------------------------------------------------------
 constexpr int RT = 256;
-constexpr int RMAX = 16384 / 8 / RT;  // 16-byte chunks per thread at the largest hidden size
 
 // U[t] = fp16(X[t] / sqrt(mean(X[t]^2) + eps) * g), one workgroup per row
-// (grid = the chunk's tokens); U is k-step-major.
+// (grid = the chunk's tokens); U is k-step-major. The chunk's first kernel:
+// it also zeroes the GEMMs' ncnt split-K counters and, when rope is not
+// NULL, writes the rotary (cos, sin) of pair i at position pos0 + t to
+// rope[t][i] (the QKV epilogue reads them).
 __global__ void __launch_bounds__(RT) rmsnorm_rows_kernel(const uint16_t* X, const uint16_t* g,
-                                                          uint16_t* U, int H, float eps) {
+                                                          uint16_t* U, int H, float eps, unsigned* cnt,
+                                                          int ncnt, float* rope, int d, int pos0,
+                                                          float base) {
   __shared__ float red[RT / kWave];
   const int t = blockIdx.x, M = gridDim.x;
+  for (int i = t * RT + threadIdx.x; i < ncnt; i += M * RT) cnt[i] = 0u;
+  if (rope && threadIdx.x < d / 2) {
+    float c, s;
+    rope_angle(pos0 + t, threadIdx.x, d, base, c, s);
+    *reinterpret_cast<float2*>(rope + (static_cast<int64_t>(t) * (d / 2) + threadIdx.x) * 2) = make_float2(c, s);
+  }
   const uint16_t* x = X + static_cast<int64_t>(t) * H;
   float ss = 0.f;
   for (int k8 = threadIdx.x; k8 < H / 8; k8 += RT) {
@@ -283,141 +631,6 @@ __global__ void __launch_bounds__(RT) rmsnorm_rows_kernel(const uint16_t* X, con
   // zero padding of the last k-step when H is not a multiple of 16
   if ((H & 15) && threadIdx.x == 0)
     *reinterpret_cast<u32x4*>(U + kmajor(H, t, M)) = u32x4{0u, 0u, 0u, 0u};
-}
-
-// Residual epilogue of an output projection, one workgroup per token row t:
-// p = sum of the slabs, partial[t] = fp16(p), out[t] = fp16(base[t] + p +
-// peer[t]) (out may be NULL). With NORM also U[t] = fp16(RMSNorm(out[t]) * g),
-// the next sub-layer's normalised input (k-step-major), taken from the
-// fp16-rounded row.
-template <bool NORM, int S>
-__device__ __forceinline__ void resid_body(const float* P, int64_t slab, const uint16_t* base,
-                                           const uint16_t* peer, uint16_t* partial, uint16_t* out,
-                                           const uint16_t* g, uint16_t* U, int H, float eps) {
-  __shared__ float red[RT / kWave];
-  const int64_t row = static_cast<int64_t>(blockIdx.x) * H;
-  u32x4 hv[RMAX];
-  float ss = 0.f;
-#pragma unroll
-  for (int it = 0; it < RMAX; ++it) {
-    const int k8 = threadIdx.x + it * RT;
-    if (k8 >= H / 8) break;
-    const int64_t i = row + k8 * 8;
-    const f32x4 p0 = slab_sum4<S>(P, slab, i), p1 = slab_sum4<S>(P, slab, i + 4);
-    const float p[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
-    float b[8], pe[8];
-    unpack8(load16(base + i), b);
-    if (peer) unpack8(load16(peer + i), pe);
-    uint16_t ph[8], oh[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      ph[e] = f2h(p[e]);
-      oh[e] = f2h(b[e] + p[e] + (peer ? pe[e] : 0.f));
-      const float o = h2f(oh[e]);
-      ss = fmaf(o, o, ss);
-    }
-    *reinterpret_cast<u32x4*>(partial + i) = pack8(ph);
-    hv[it] = pack8(oh);
-    if (out) *reinterpret_cast<u32x4*>(out + i) = hv[it];
-  }
-  if (!NORM) return;
-  ss = block_sum<RT>(ss, red);
-  const float rstd = 1.0f / sqrtf(ss / static_cast<float>(H) + eps);
-#pragma unroll
-  for (int it = 0; it < RMAX; ++it) {
-    const int k8 = threadIdx.x + it * RT;
-    if (k8 >= H / 8) break;
-    float f[8], gg[8];
-    unpack8(hv[it], f);
-    unpack8(load16(g + k8 * 8), gg);
-    uint16_t u[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) u[e] = f2h(f[e] * rstd * gg[e]);
-    *reinterpret_cast<u32x4*>(U + kmajor(k8 * 8, blockIdx.x, gridDim.x)) = pack8(u);
-  }
-  if ((H & 15) && threadIdx.x == 0)
-    *reinterpret_cast<u32x4*>(U + kmajor(H, blockIdx.x, gridDim.x)) = u32x4{0u, 0u, 0u, 0u};
-}
-
-template <int S>
-__global__ void __launch_bounds__(RT) resid_norm_kernel(const float* P, int64_t slab, const uint16_t* base,
-                                                        const uint16_t* peer, uint16_t* partial,
-                                                        uint16_t* out, const uint16_t* g, uint16_t* U,
-                                                        int H, float eps) {
-  resid_body<true, S>(P, slab, base, peer, partial, out, g, U, H, eps);
-}
-
-template <int S>
-__global__ void __launch_bounds__(RT) resid_only_kernel(const float* P, int64_t slab, const uint16_t* base,
-                                                        const uint16_t* peer, uint16_t* partial,
-                                                        uint16_t* out, const uint16_t* g, uint16_t* U,
-                                                        int H, float eps) {
-  resid_body<false, S>(P, slab, base, peer, partial, out, g, U, H, eps);
-}
-
-// From the raw projections QKV[t] = [q (nq*d) | k (nkv*d) | v (nkv*d)] of
-// token t at position pos0 + t (summed over the slabs): Q[t] = fp16(RoPE(q)
-// / sqrt(d)); the rotated k and v go to slot pos0 + t of each KV head. One
-// workgroup per token.
-template <int S>
-__global__ void __launch_bounds__(RT) rope_append_kernel(const float* P, int64_t slab, int ldq,
-                                                         uint16_t* Q, uint16_t* kc, uint16_t* vc, int nq,
-                                                         int nkv, int d, int cap, int pos0, float base) {
-  const int t = blockIdx.x;
-  const int pos = pos0 + t;
-  const int64_t row = static_cast<int64_t>(t) * ldq;
-  const float scale = 1.0f / sqrtf(static_cast<float>(d));
-  // 4 consecutive values (2 rotary pairs) per step, d / 4 steps per head;
-  // RT is a multiple of d / 4, so a thread keeps one column group c4 for all
-  // its heads and evaluates its two angles once.
-  const int per_head = d / 4;
-  const int c4 = (threadIdx.x % per_head) * 4;
-  float ca, sa, cb, sb;
-  rope_angle(pos, c4 / 2, d, base, ca, sa);
-  rope_angle(pos, c4 / 2 + 1, d, base, cb, sb);
-  for (int head = threadIdx.x / per_head; head < nq + nkv; head += RT / per_head) {
-    const f32x4 v = slab_sum4<S>(P, slab, row + head * d + c4);
-    const float r0 = v.x * ca - v.y * sa, r1 = v.x * sa + v.y * ca;
-    const float r2 = v.z * cb - v.w * sb, r3 = v.z * sb + v.w * cb;
-    uint16_t* o;
-    float sc;
-    if (head < nq) {
-      o = Q + static_cast<int64_t>(t) * nq * d + head * d + c4;
-      sc = scale;
-    } else {
-      o = kc + (static_cast<int64_t>(head - nq) * cap + pos) * d + c4;
-      sc = 1.f;
-    }
-    const unsigned w0 = f2h(r0 * sc) | (static_cast<unsigned>(f2h(r1 * sc)) << 16);
-    const unsigned w1 = f2h(r2 * sc) | (static_cast<unsigned>(f2h(r3 * sc)) << 16);
-    *reinterpret_cast<uint2*>(o) = make_uint2(w0, w1);
-  }
-  for (int idx = threadIdx.x; idx < nkv * d / 4; idx += RT) {
-    const int g = (idx * 4) / d, dd = idx * 4 - g * d;
-    const f32x4 v = slab_sum4<S>(P, slab, row + (nq + nkv) * d + idx * 4);
-    const unsigned w0 = f2h(v.x) | (static_cast<unsigned>(f2h(v.y)) << 16);
-    const unsigned w1 = f2h(v.z) | (static_cast<unsigned>(f2h(v.w)) << 16);
-    *reinterpret_cast<uint2*>(vc + (static_cast<int64_t>(g) * cap + pos) * d + dd) = make_uint2(w0, w1);
-  }
-}
-
-// Mg[t][j] = fp16(silu(G[t][j]) * Up[t][j]) for j < F, zero for F <= j < kpad
-// (k-step-major); G and Up are columns j and up0 + j of the summed slabs (row
-// stride ldp). One workgroup per token.
-template <int S>
-__global__ void __launch_bounds__(RT) silu_gate_kernel(const float* P, int64_t slab, int64_t ldp,
-                                                       int up0, uint16_t* Mg, int F, int kpad) {
-  const int t = blockIdx.x;
-  const int64_t row = static_cast<int64_t>(t) * ldp;
-  for (int j = threadIdx.x; j < kpad; j += RT) {
-    float m = 0.f;
-    if (j < F) {
-      const float gt = slab_sum1<S>(P, slab, row + j);
-      const float up = slab_sum1<S>(P, slab, row + up0 + j);
-      m = gt / (1.0f + __expf(-gt)) * up;
-    }
-    Mg[kmajor(j, t, gridDim.x)] = f2h(m);
-  }
 }
 
 // ---------------------------------------------------------------------------
@@ -665,10 +878,12 @@ Split choose_split(int M, int N, int K) {
 }
 
 // The shard's prefill GEMMs for T tokens: QKV, O, gate/up, down. N counts
-// virtual rows of B (the up rows start at the 8-aligned row after the gate
-// rows); K is rounded up to a multiple of 8 (the padding multiplies zeros).
+// virtual rows of B: the QKV GEMM's k rows start at the 8-aligned row after
+// the q rows (likewise v), and the gate/up GEMM interleaves gate and up rows
+// in blocks of 64 (so one output tile holds the gate and up values of the
+// same 64 columns).
 struct PrefillGemms {
-  int M, N[4], K[4], up0;
+  int M, N[4], K[4];
 };
 
 PrefillGemms prefill_gemms(const vt_shard_spec& s, int32_t T) {
@@ -680,16 +895,16 @@ PrefillGemms prefill_gemms(const vt_shard_spec& s, int32_t T) {
   g.K[0] = H;
   g.N[1] = H;
   g.K[1] = in.n_q_heads * d;
-  g.up0 = (in.n_cols + 7) / 8 * 8;
-  g.N[2] = g.up0 + in.n_cols;
+  g.N[2] = (in.n_cols + 63) / 64 * 128;
   g.K[2] = H;
   g.N[3] = H;
-  g.K[3] = std::max(8, g.up0);
+  g.K[3] = in.n_cols;
   return g;
 }
 
 struct PrefillWs {
-  size_t u, q, o, m, part, total;
+  size_t u, q, o, m, part, cnt, rowsq, rope, total;
+  int cnt_off[4], ncnt;
 };
 
 inline int64_t rup(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
@@ -698,12 +913,16 @@ PrefillWs prefill_layout(const vt_shard_spec& s, int32_t T) {
   const vt_shard_info& in = s.info;
   const int64_t H = s.dims.hidden, d = s.dims.head_dim;
   const PrefillGemms gm = prefill_gemms(s, T);
-  int64_t part = 0;  // one region serves the four GEMMs' slabs in turn
+  PrefillWs w{};
+  int64_t part = 0;  // one region serves the four GEMMs' split-K tiles in turn
+  w.ncnt = 0;
   for (int i = 0; i < 4; ++i) {
     const Split sp = choose_split(gm.M, gm.N[i], gm.K[i]);
-    part = std::max<int64_t>(part, static_cast<int64_t>(sp.splits) * T * gm.N[i] * 4);
+    const int64_t tiles = static_cast<int64_t>(sp.m_tiles) * sp.n_tiles;
+    if (sp.splits > 1) part = std::max<int64_t>(part, sp.splits * tiles * pf::GBM * pf::GBN * 4);
+    w.cnt_off[i] = w.ncnt;
+    w.ncnt += 2 * static_cast<int>(tiles);  // arrived, stored
   }
-  PrefillWs w{};
   size_t off = workspace_sync_bytes(s);  // leave the decode synchronisation words alone
   auto take = [&](int64_t bytes) {
     size_t at = off;
@@ -716,12 +935,16 @@ PrefillWs prefill_layout(const vt_shard_spec& s, int32_t T) {
   w.o = take(2 * T * std::max<int64_t>(rup(in.n_q_heads * d, 16), 16));
   w.m = take(2 * T * std::max<int64_t>(rup(in.n_cols, 16), 16));
   w.part = take(part);
+  w.cnt = take(4 * static_cast<int64_t>(w.ncnt));
+  w.rowsq = take(4 * T * ((H + pf::GBN - 1) / pf::GBN));
+  w.rope = take(4 * T * d);
   w.total = off;
   return w;
 }
 
-// Launches P = A B^T as split-K slabs; returns the slab count via *splits.
-vt_status launch_gemm(pf::GemmArgs a, float* P, hipStream_t s, int* splits) {
+// Launches the split-K GEMM with its epilogue; P holds the split-K tiles and
+// cnt the per-tile arrival counters (zero at launch).
+vt_status launch_gemm(pf::GemmArgs a, float* P, unsigned* cnt, unsigned* err, hipStream_t s) {
   {
     // the GEMM's dynamic LDS exceeds the default limit: raise it once per device
     static std::mutex mu;
@@ -745,9 +968,8 @@ vt_status launch_gemm(pf::GemmArgs a, float* P, hipStream_t s, int* splits) {
   a.splits = sp.splits;
   a.kps = sp.kps;
   a.P = P;
-  a.ldp = a.N;
-  a.slab = static_cast<int64_t>(a.M) * a.N;
-  *splits = sp.splits;
+  a.cnt = cnt;
+  a.err = err;
   if (a.M == 0 || a.N == 0) return VT_OK;
   const int units = sp.n_tiles * sp.splits;
   const int groups = (units + 7) / 8;
@@ -760,19 +982,6 @@ vt_status launch_gemm(pf::GemmArgs a, float* P, hipStream_t s, int* splits) {
 pf::BSrc bsrc(const void* p, int64_t ld, int start, int rows) {
   return pf::BSrc{static_cast<const uint16_t*>(p), ld, start, rows};
 }
-
-// Launch helper for kernels templated on the split-K slab count.
-#define VT_SPLIT_DISPATCH(KERNEL, ...)                                           \
-  switch (splits) {                                                              \
-    case 1: hipLaunchKernelGGL(KERNEL<1>, __VA_ARGS__); break;                   \
-    case 2: hipLaunchKernelGGL(KERNEL<2>, __VA_ARGS__); break;                   \
-    case 3: hipLaunchKernelGGL(KERNEL<3>, __VA_ARGS__); break;                   \
-    case 4: hipLaunchKernelGGL(KERNEL<4>, __VA_ARGS__); break;                   \
-    case 5: hipLaunchKernelGGL(KERNEL<5>, __VA_ARGS__); break;                   \
-    case 6: hipLaunchKernelGGL(KERNEL<6>, __VA_ARGS__); break;                   \
-    case 7: hipLaunchKernelGGL(KERNEL<7>, __VA_ARGS__); break;                   \
-    default: hipLaunchKernelGGL(KERNEL<8>, __VA_ARGS__); break;                  \
-  }
 
 }  // namespace
 
@@ -835,38 +1044,54 @@ extern "C" vt_status vt_layer_prefill_chunk(const vt_shard_spec* spec, const vt_
   uint16_t* Ob = reinterpret_cast<uint16_t*>(base + L.o);
   uint16_t* Mb = reinterpret_cast<uint16_t*>(base + L.m);
   float* P = reinterpret_cast<float*>(base + L.part);
+  unsigned* cnt = reinterpret_cast<unsigned*>(base + L.cnt);
+  float* rowsq = reinterpret_cast<float*>(base + L.rowsq);
+  float* rope = reinterpret_cast<float*>(base + L.rope);
+  unsigned* err = reinterpret_cast<unsigned*>(base + VT_WS_ERROR_WORD);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int nq = in.n_q_heads, nkv = in.n_kv_heads, F = in.n_cols;
   const int G = D.n_heads / D.n_kv_heads;
-  const int kpad_f = std::max(16, (F + 15) / 16 * 16);  // k-step-major width of the SiLU-gate output
   const PrefillGemms gm = prefill_gemms(*spec, n_tok);
-  int splits = 1;
   auto check = [&](const char* what) -> vt_status {
     hipError_t e = hipGetLastError();
     return e == hipSuccess ? VT_OK : fail(VT_ERR_HIP, "%s launch: %s", what, hipGetErrorString(e));
   };
-  auto slab = [&](int i) { return static_cast<int64_t>(n_tok) * gm.N[i]; };
+  auto gemm = [&](int i, const uint16_t* A, int epi) {
+    pf::GemmArgs a{};
+    a.A = A;
+    a.M = n_tok;
+    a.N = gm.N[i];
+    a.K = gm.K[i];
+    a.epi = epi;
+    a.H = static_cast<int>(H);
+    a.eps = D.rms_eps;
+    return a;
+  };
 
   if (attn) {
+    // RMSNorm of x, the rotary table, zeroed split-K counters
     hipLaunchKernelGGL(pf::rmsnorm_rows_kernel, dim3(n_tok), dim3(pf::RT), 0, s,
                        static_cast<const uint16_t*>(io->x), static_cast<const uint16_t*>(w->g_attn), U,
-                       static_cast<int>(H), D.rms_eps);
+                       static_cast<int>(H), D.rms_eps, cnt, L.ncnt, rope, static_cast<int>(d), pos0,
+                       D.rope_base);
     if ((st = check("rmsnorm")) != VT_OK) return st;
-    pf::GemmArgs a{};
-    a.A = U;
-    a.K = gm.K[0];
-    a.M = n_tok;
-    a.N = gm.N[0];
+    // QKV; epilogue: RoPE, Q, and the append of K and V at pos0..
+    pf::GemmArgs a = gemm(0, U, pf::EPI_QKV);
     const int qd = nq * static_cast<int>(d), kd = nkv * static_cast<int>(d);
     a.b[0] = bsrc(w->wq, w->ld_q, 0, qd);
     a.b[1] = bsrc(w->wk, w->ld_k, qd, kd);
     a.b[2] = bsrc(w->wv, w->ld_v, qd + kd, kd);
     a.nb = 3;
-    if ((st = launch_gemm(a, P, s, &splits)) != VT_OK) return st;
-    VT_SPLIT_DISPATCH(pf::rope_append_kernel, dim3(n_tok), dim3(pf::RT), 0, s, P, slab(0), gm.N[0], Qr,
-                      static_cast<uint16_t*>(kv->k), static_cast<uint16_t*>(kv->v), nq, nkv,
-                      static_cast<int>(d), kv->capacity, pos0, D.rope_base);
-    if ((st = check("rope_append")) != VT_OK) return st;
+    a.Q = Qr;
+    a.kc = static_cast<uint16_t*>(kv->k);
+    a.vc = static_cast<uint16_t*>(kv->v);
+    a.rope = rope;
+    a.nq = nq;
+    a.nkv = nkv;
+    a.d = static_cast<int>(d);
+    a.cap = kv->capacity;
+    a.pos0 = pos0;
+    if ((st = launch_gemm(a, P, cnt + L.cnt_off[0], err, s)) != VT_OK) return st;
     const int blocks = (nq + 7) / 8 * 8 * ((n_tok + pf::QB - 1) / pf::QB);
     if (d == 128)
       hipLaunchKernelGGL(pf::attn_prefill_kernel<128>, dim3(blocks), dim3(pf::AW * kWave), 0, s, Qr, Ob,
@@ -877,62 +1102,52 @@ extern "C" vt_status vt_layer_prefill_chunk(const vt_shard_spec* spec, const vt_
                          static_cast<const uint16_t*>(kv->k), static_cast<const uint16_t*>(kv->v),
                          n_tok, nq, G, kv->capacity, pos0, D.window);
     if ((st = check("attention")) != VT_OK) return st;
-    pf::GemmArgs o{};
-    o.A = Ob;
-    o.K = gm.K[1];
-    o.M = n_tok;
-    o.N = gm.N[1];
+    // O; epilogue: h = x + p_attn + peer, and with the FFN to follow its
+    // input h * g_ffn and the sums of h^2 its RMSNorm needs
+    pf::GemmArgs o = gemm(1, Ob, pf::EPI_O);
     o.b[0] = bsrc(w->wo, w->ld_o, 0, gm.N[1]);
     o.nb = 1;
-    if ((st = launch_gemm(o, P, s, &splits)) != VT_OK) return st;
-    // h = x + p_attn + peer; with FFN to follow also U = RMSNorm(h) * g_ffn
+    o.base = static_cast<const uint16_t*>(io->x);
+    o.peer = static_cast<const uint16_t*>(io->peer_attn);
+    o.partial = static_cast<uint16_t*>(io->attn_partial);
+    o.out = static_cast<uint16_t*>(io->h);
     if (ffn) {
-      VT_SPLIT_DISPATCH(pf::resid_norm_kernel, dim3(n_tok), dim3(pf::RT), 0, s, P, slab(1),
-                        static_cast<const uint16_t*>(io->x), static_cast<const uint16_t*>(io->peer_attn),
-                        static_cast<uint16_t*>(io->attn_partial), static_cast<uint16_t*>(io->h),
-                        static_cast<const uint16_t*>(w->g_ffn), U, static_cast<int>(H), D.rms_eps);
-    } else {
-      VT_SPLIT_DISPATCH(pf::resid_only_kernel, dim3(n_tok), dim3(pf::RT), 0, s, P, slab(1),
-                        static_cast<const uint16_t*>(io->x), static_cast<const uint16_t*>(io->peer_attn),
-                        static_cast<uint16_t*>(io->attn_partial), static_cast<uint16_t*>(io->h),
-                        static_cast<const uint16_t*>(nullptr), static_cast<uint16_t*>(nullptr),
-                        static_cast<int>(H), D.rms_eps);
+      o.gain = static_cast<const uint16_t*>(w->g_ffn);
+      o.U = U;
+      o.rowsq = rowsq;
     }
-    if ((st = check("attention residual")) != VT_OK) return st;
+    if ((st = launch_gemm(o, P, cnt + L.cnt_off[1], err, s)) != VT_OK) return st;
   }
   if (ffn) {
     if (!attn) {
       hipLaunchKernelGGL(pf::rmsnorm_rows_kernel, dim3(n_tok), dim3(pf::RT), 0, s,
                          static_cast<const uint16_t*>(io->h), static_cast<const uint16_t*>(w->g_ffn),
-                         U, static_cast<int>(H), D.rms_eps);
+                         U, static_cast<int>(H), D.rms_eps, cnt, L.ncnt, static_cast<float*>(nullptr),
+                         static_cast<int>(d), pos0, D.rope_base);
       if ((st = check("rmsnorm")) != VT_OK) return st;
     }
-    pf::GemmArgs a{};
-    a.A = U;
-    a.K = gm.K[2];
-    a.M = n_tok;
-    a.N = gm.N[2];
+    // gate/up; epilogue: the RMSNorm's 1 / rms (when the O epilogue left
+    // the sums of squares) and M = silu(gate) * up
+    pf::GemmArgs a = gemm(2, U, pf::EPI_GU);
     a.b[0] = bsrc(w->wg, w->ld_g, 0, F);
-    a.b[1] = bsrc(w->wu, w->ld_u, gm.up0, F);
+    a.b[1] = bsrc(w->wu, w->ld_u, 0, F);
     a.nb = 2;
-    if ((st = launch_gemm(a, P, s, &splits)) != VT_OK) return st;
-    VT_SPLIT_DISPATCH(pf::silu_gate_kernel, dim3(n_tok), dim3(pf::RT), 0, s, P, slab(2),
-                      static_cast<int64_t>(gm.N[2]), gm.up0, Mb, F, kpad_f);
-    if ((st = check("silu_gate")) != VT_OK) return st;
-    pf::GemmArgs b{};
-    b.A = Mb;
-    b.K = gm.K[3];
-    b.M = n_tok;
-    b.N = gm.N[3];
+    a.interleave = 1;
+    a.rowsq = attn ? rowsq : nullptr;
+    a.rowsq_tiles = static_cast<int>((H + pf::GBN - 1) / pf::GBN);
+    a.Mo = Mb;
+    a.F = F;
+    a.kpad = std::max(16, (F + 15) / 16 * 16);
+    if ((st = launch_gemm(a, P, cnt + L.cnt_off[2], err, s)) != VT_OK) return st;
+    // down; epilogue: y = h + p_ffn + peer
+    pf::GemmArgs b = gemm(3, Mb, pf::EPI_DOWN);
     b.b[0] = bsrc(w->wd, w->ld_d, 0, gm.N[3]);
     b.nb = 1;
-    if ((st = launch_gemm(b, P, s, &splits)) != VT_OK) return st;
-    VT_SPLIT_DISPATCH(pf::resid_only_kernel, dim3(n_tok), dim3(pf::RT), 0, s, P, slab(3),
-                      static_cast<const uint16_t*>(io->h), static_cast<const uint16_t*>(io->peer_ffn),
-                      static_cast<uint16_t*>(io->ffn_partial), static_cast<uint16_t*>(io->y),
-                      static_cast<const uint16_t*>(nullptr), static_cast<uint16_t*>(nullptr),
-                      static_cast<int>(H), D.rms_eps);
-    if ((st = check("ffn residual")) != VT_OK) return st;
+    b.base = static_cast<const uint16_t*>(io->h);
+    b.peer = static_cast<const uint16_t*>(io->peer_ffn);
+    b.partial = static_cast<uint16_t*>(io->ffn_partial);
+    b.out = static_cast<uint16_t*>(io->y);
+    if ((st = launch_gemm(b, P, cnt + L.cnt_off[3], err, s)) != VT_OK) return st;
   }
   if (attn) kv->len = pos0 + n_tok;
   return VT_OK;
