@@ -649,8 +649,11 @@ __global__ void __launch_bounds__(RT) rmsnorm_rows_kernel(const uint16_t* X, con
 // (O^T += V_blk^T P^T) without any shuffle. V is staged row-major like K
 // (16-byte writes) and that MFMA's V^T operand (8 keys of one dimension per
 // lane) is gathered with eight 2-byte reads; with rows of D + 8 halves the
-// two half-waves of each read fall 32 banks apart. A wave only touches its
-// own LDS region inside the loop, so the loop needs no workgroup barrier.
+// two half-waves of each read fall 32 banks apart. The 32 queries are staged
+// in LDS once per workgroup (every wave multiplies the same Q block), which
+// keeps the loop's registers within two waves per SIMD. Apart from reading
+// Q, a wave only touches its own LDS region inside the loop, so the loop
+// needs no workgroup barrier.
 // The output O (the O projection's input) is written k-step-major.
 // ---------------------------------------------------------------------------
 constexpr int QB = 32, KB = 32, AW = 8;
@@ -664,6 +667,7 @@ struct AttnLds {
   static constexpr int KLD = D + 8;   // row stride of the K and V tiles (halves)
   static constexpr int OLD = D + 4;   // row stride of a wave's fp32 output in the merge
   static constexpr int WAVE_HALVES = 2 * KB * KLD;
+  static constexpr int Q_HALVES = QB * KLD;  // the workgroup's Q block (rows of KLD)
   static_assert(WAVE_HALVES * 2 >= (QB * OLD + 2 * QB) * 4, "merge buffer must fit a wave's region");
 };
 
@@ -674,7 +678,7 @@ __global__ void __launch_bounds__(AW * kWave) attn_prefill_kernel(const uint16_t
                                                                   int window) {
   using LY = AttnLds<D>;
   constexpr int KLD = LY::KLD, OLD = LY::OLD;
-  __shared__ __attribute__((aligned(16))) uint16_t smem[AW * LY::WAVE_HALVES];
+  __shared__ __attribute__((aligned(16))) uint16_t smem[AW * LY::WAVE_HALVES + LY::Q_HALVES];
   const int lane = threadIdx.x % kWave;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   uint16_t* Ks = smem + wave * LY::WAVE_HALVES;
@@ -691,14 +695,18 @@ __global__ void __launch_bounds__(AW * kWave) attn_prefill_kernel(const uint16_t
   const int qpos = pos0 + tq;
   constexpr int NKS = D / 16;     // MFMA k-steps over the head dimension
 
-  // Q^T operand: lane supplies Q[tq][16 ks + 8 (l/32) + e]
-  u32x4 qf[NKS];
-  {
-    const int tqc = min(tq, T - 1);
-    const uint16_t* qrow = Q + (static_cast<int64_t>(tqc) * nq + j) * D;
-#pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) qf[ks] = load16(qrow + ks * 16 + 8 * (lane / 32));
+  // the Q block into LDS (queries past T repeat the last one); the Q^T
+  // operand of k-step ks: lane supplies Q[tq][16 ks + 8 (l/32) + e]
+  uint16_t* Qs = smem + AW * LY::WAVE_HALVES;
+  for (int c = threadIdx.x; c < QB * D / 8; c += AW * kWave) {
+    const int q = c / (D / 8), col = (c % (D / 8)) * 8;
+    const int tqc = min(t0 + q, T - 1);
+    *reinterpret_cast<u32x4*>(Qs + q * KLD + col) = load16(Q + (static_cast<int64_t>(tqc) * nq + j) * D + col);
   }
+  __syncthreads();
+  auto qfrag = [&](int ks) {
+    return *reinterpret_cast<const u32x4*>(Qs + (lane % 32) * KLD + ks * 16 + 8 * (lane / 32));
+  };
   f32x16 o[D / 32];
 #pragma unroll
   for (int mt = 0; mt < D / 32; ++mt) o[mt] = f32x16{};
@@ -751,7 +759,7 @@ __global__ void __launch_bounds__(AW * kWave) attn_prefill_kernel(const uint16_t
     for (int ks = 0; ks < NKS; ++ks) {
       const u32x4 kf =
           *reinterpret_cast<const u32x4*>(Ks + (lane % 32) * KLD + ks * 16 + 8 * (lane / 32));
-      s = mfma32(kf, qf[ks], s);
+      s = mfma32(kf, qfrag(ks), s);
     }
     // accumulator i: LDS row 8(i/4) + 4(l/32) + i%4 holds key p0 + swap_bits23(row)
     float bm = -INFINITY;
