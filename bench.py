@@ -408,7 +408,7 @@ def chain_section(wl, steps, warmup, emit=False):
         "algorithmic_bytes_per_step": step_bytes,
         "hbm_GBps": round(gbps, 1),
         "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
-        "roofline": roofline(step_bytes, ms_step, "decode_kernel<0, 4, 0, false>", wl.key),
+        "roofline": roofline(step_bytes, ms_step, "decode_kernel<0, 4, 0, false, false>", wl.key),
         "launch": "persistent + hipgraph (windows keyed by rotation phase)",
     }
     if emit:
@@ -463,7 +463,7 @@ def main():
             "hbm_GBps": round(r["bytes"] / (ms_step * 1e-3) / 1e9, 1),
             "hbm_frac_of_peak": round(r["bytes"] / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
             "algorithmic_bytes_per_step": int(r["bytes"]),
-            "roofline": roofline(r["bytes"], ms_step, "decode_kernel<0, 4, 0, true> (40 layers per launch)",
+            "roofline": roofline(r["bytes"], ms_step, "decode_kernel<0, 4, 0, true, false> (40 layers per launch)",
                                  wl.key),
             "setup_s": round(r["setup_s"], 1),
         })
