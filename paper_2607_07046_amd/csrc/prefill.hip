@@ -254,7 +254,10 @@ __global__ void __launch_bounds__(GT, 2) gemm_kernel(GemmArgs g) {
     for (int b = 0; b < 4; ++b)
       bf[b] = *reinterpret_cast<const u32x4*>(st + (b * 32 + lane % 32) * GLD + kc);
   };
-  auto compute = [&](const uint16_t* st, int ks_base, int s0) {
+  // The next k-tile's B chunks go to the other LDS stage in the middle of
+  // the k-tile (after the second k-step's MFMAs are issued), so the LDS
+  // writes overlap the matrix cores instead of following them.
+  auto compute = [&](const uint16_t* st, int ks_base, int s0, uint16_t* st_next, u32x4 (&vb)[B_CH], int kt_next) {
     u32x4 bf[2][4];
     read_b(st, 0, bf[0]);
 #pragma unroll
@@ -263,6 +266,7 @@ __global__ void __launch_bounds__(GT, 2) gemm_kernel(GemmArgs g) {
 #pragma unroll
       for (int b = 0; b < 4; ++b) acc[b] = mfma32(ar[s0 + ks], bf[ks & 1][b], acc[b]);
       load_a(ks_base + ks + RING, ar[s0 + ks]);
+      if (ks == 1) store_b(st_next, vb, kt_next);
     }
   };
 
@@ -280,13 +284,11 @@ __global__ void __launch_bounds__(GT, 2) gemm_kernel(GemmArgs g) {
   for (int i = 0; i < nkt; i += 2) {
     load_b(kt0 + i + 2, rb0);
     __builtin_amdgcn_sched_barrier(0);
-    compute(L0, i * KSTEPS, 0);
-    store_b(L1, rb1, kt0 + i + 1);
+    compute(L0, i * KSTEPS, 0, L1, rb1, kt0 + i + 1);
     __syncthreads();
     load_b(kt0 + i + 3, rb1);
     __builtin_amdgcn_sched_barrier(0);
-    compute(L1, (i + 1) * KSTEPS, KSTEPS);
-    store_b(L0, rb0, kt0 + i + 2);
+    compute(L1, (i + 1) * KSTEPS, KSTEPS, L0, rb0, kt0 + i + 2);
     __syncthreads();
   }
 
