@@ -4,10 +4,13 @@ against the fp64 oracle, through the C ABI.
 Same bar as decode (per-row element-wise relative error <= 2e-2 with the
 denominator floored at 0.2 of the row's RMS, normwise <= 1.5e-3; the FFN
 outputs against the oracle's FFN at fp16(h)); the appended K/V of every chunk token lands in
-its slot and every other cache byte is unchanged.
+its slot and every other cache byte is unchanged. Also: the sub-layers as
+separate calls, NaN in the weight rows' padding, and bit-identical repeats
+(the split-K reduction's order does not depend on arrival order).
 """
 import numpy as np
 import pytest
+import torch
 
 import oracle
 from paper_2607_07046_amd import voltron as vt
@@ -100,6 +103,78 @@ def test_prefill_then_decode_continues_the_cache():
     got = gs.decode(x, wl.ctx + 9, BOTH)
     for k in ("p_attn", "h", "p_ffn", "y"):
         assert_close(got[k], ref[k], k)
+
+
+def test_prefill_attention_then_ffn_calls():
+    """The two sub-layers as separate calls: VT_ATTN alone (the O GEMM's
+    epilogue without the FFN input), then VT_FFN alone from the device's h
+    (the RMSNorm before the gate/up GEMM computed on its own); the FFN is
+    checked against the oracle's FFN sub-layer at exactly that h."""
+    wl = tiny_workload(307, 512, 8, 4, 64, 700, (0.5, 0.5), 1, 30, sigma=0.03, chunk=37)
+    li = LayerInputs(wl)
+    d = wl.dims
+    r = oracle_ranges(wl)
+    w = oracle_shard_weights(li, r)
+    kc, vc = li.kv_context_heads(r.kv_head_begin, r.kv_head_begin + r.n_kv_heads)
+    X = li.x_chunk(37)
+    pa, pf = li.peer("attn", rows=37), li.peer("ffn", rows=37)
+    ref = oracle.prefill(w, r.n_q_heads, r.n_kv_heads, d.head_dim, d.rms_eps, d.rope_base, X, kc,
+                         vc, wl.ctx, pa, pf)
+    gs = GpuShard(wl, li=li, capacity=wl.ctx + 40, max_tokens=37)
+    a = gs.prefill(X, wl.ctx, vt.VT_ATTN, peer_attn=pa)
+    for k in ("p_attn", "h"):
+        assert_close(a[k], ref[k], k)
+    assert np.isnan(a["p_ffn"]).all() and np.isnan(a["y"]).all()  # not written
+    assert gs.kv.len == wl.ctx + 37
+    f = gs.prefill(None, wl.ctx, vt.VT_FFN, peer_ffn=pf, h_in=a["h"])
+    fr = ffn_at_h16(w, d.rms_eps, {"h": a["h"]}, pf)
+    for k in ("p_ffn", "y"):
+        assert_close(f[k], fr[k], k)
+    assert gs.kv.len == wl.ctx + 37
+
+
+def test_prefill_ignores_row_padding():
+    """Down-projection rows padded past the shard's columns (not a multiple
+    of 8 here) with NaN: the k-chunk that straddles the column count is
+    masked, so the outputs match the oracle."""
+    wl = tiny_workload(308, 1024, 8, 4, 128, 1501, (0.6, 0.4), 0, 40, sigma=0.03, chunk=70)
+    li = LayerInputs(wl)
+    r = oracle_ranges(wl)
+    assert r.n_cols % 8 != 0
+    gs_probe = GpuShard(wl, li=li, capacity=wl.ctx + 73, max_tokens=70)
+    wd = gs_probe.w.tensors["wd"]
+    assert wd.shape[1] > r.n_cols
+    wd[:, r.n_cols:] = float("nan")
+    torch.cuda.synchronize()
+    # the same case as run_case, on the shard whose padding now holds NaN
+    d = wl.dims
+    w = oracle_shard_weights(li, r)
+    kc, vc = li.kv_context_heads(r.kv_head_begin, r.kv_head_begin + r.n_kv_heads)
+    X = li.x_chunk(70)
+    ref = ffn_at_h16(w, d.rms_eps, oracle.prefill(w, r.n_q_heads, r.n_kv_heads, d.head_dim,
+                                                  d.rms_eps, d.rope_base, X, kc, vc, wl.ctx))
+    got = gs_probe.prefill(X, wl.ctx, BOTH)
+    for k in ("p_attn", "h", "p_ffn", "y"):
+        assert np.isfinite(got[k]).all(), k
+        assert_close(got[k], ref[k], k)
+
+
+def test_prefill_repeat_is_bitwise():
+    """The split-K slices of an output tile are added in slice order by
+    whichever arrives last: the same chunk twice gives the same bits."""
+    wl = get("7b_prefill")
+    li = LayerInputs(wl)
+    gs = GpuShard(wl, li=li, capacity=wl.ctx + wl.chunk, max_tokens=wl.chunk)
+    X = li.x_chunk(wl.chunk)
+    outs, caches = [], []
+    for _ in range(2):
+        outs.append(gs.prefill(X, wl.ctx, BOTH))
+        caches.append(gs.cache())
+        gs.kv.len = wl.ctx
+    for k in ("p_attn", "h", "p_ffn", "y"):
+        assert np.array_equal(outs[0][k], outs[1][k]), k
+    assert np.array_equal(caches[0][0], caches[1][0]) and np.array_equal(caches[0][1], caches[1][1])
+    assert not gs.sync_words().any()
 
 
 def test_prefill_rejects_bad_positions():
