@@ -650,8 +650,7 @@ __global__ void __launch_bounds__(RT) rmsnorm_rows_kernel(const uint16_t* X, con
 // operand layout asks for, and the probabilities go to the second MFMA
 // (O^T += V_blk^T P^T) without any shuffle. V is staged row-major like K
 // (16-byte writes) and that MFMA's V^T operand (8 keys of one dimension per
-// lane) is gathered with eight 2-byte reads; with rows of D + 8 halves the
-// two half-waves of each read fall 32 banks apart. The 32 queries are staged
+// lane) is gathered with two transposing 8-byte LDS reads. The 32 queries are staged
 // in LDS once per workgroup (every wave multiplies the same Q block), which
 // keeps the loop's registers within two waves per SIMD. Apart from reading
 // Q, a wave only touches its own LDS region inside the loop, so the loop
@@ -659,6 +658,23 @@ __global__ void __launch_bounds__(RT) rmsnorm_rows_kernel(const uint16_t* X, con
 // The output O (the O projection's input) is written k-step-major.
 // ---------------------------------------------------------------------------
 constexpr int QB = 32, KB = 32, AW = 8;
+
+typedef short v4h16 __attribute__((ext_vector_type(4)));
+
+// 4 fp16 values per lane from LDS, transposed within each group of 16 lanes
+// (ds_read_b64_tr_b16: lane j supplies the 8-byte address of its 4 values;
+// lane i receives value i % 4 of lanes i / 4, 4 + i / 4, 8 + i / 4 and
+// 12 + i / 4 of its group).
+__device__ __forceinline__ v4h16 lds_read_tr16(const uint16_t* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4h16*)(p));
+}
+
+__device__ __forceinline__ u32x4 pack_v4(v4h16 a, v4h16 b) {
+  auto w = [](short x, short y) {
+    return static_cast<unsigned>(static_cast<uint16_t>(x)) | (static_cast<unsigned>(static_cast<uint16_t>(y)) << 16);
+  };
+  return u32x4{w(a.x, a.y), w(a.z, a.w), w(b.x, b.y), w(b.z, b.w)};
+}
 
 __device__ __forceinline__ int swap_bits23(int r) {
   return (r & ~0xC) | ((r & 4) << 1) | ((r & 8) >> 1);
@@ -799,16 +815,18 @@ __global__ void __launch_bounds__(AW * kWave) attn_prefill_kernel(const uint16_t
       pf[s2].w = ph[8 * s2 + 6] | (static_cast<unsigned>(ph[8 * s2 + 7]) << 16);
     }
     // V^T operand for dimension tile mt, key step s2: lane l takes dimension
-    // 32 mt + l%32 of keys 16 s2 + 8 (l/32) .. +7
+    // 32 mt + l%32 of keys 16 s2 + 8 (l/32) .. +7, gathered from the
+    // row-major V tile by two transposing LDS reads: in each group of 16
+    // lanes, lane j reads the 4 dimensions 4 (j%4) .. of key j / 4 and lane
+    // i receives dimension i of the 4 keys
 #pragma unroll
     for (int mt = 0; mt < D / 32; ++mt)
 #pragma unroll
       for (int s2 = 0; s2 < 2; ++s2) {
-        const uint16_t* vcol = Vs + (s2 * 16 + 8 * (lane / 32)) * KLD + mt * 32 + lane % 32;
-        uint16_t vh[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) vh[e] = vcol[e * KLD];
-        o[mt] = mfma32(pack8(vh), pf[s2], o[mt]);
+        const int grp = lane / 16, j = lane % 16;
+        const uint16_t* vp = Vs + (s2 * 16 + 8 * (grp / 2) + j / 4) * KLD + mt * 32 + 16 * (grp % 2) + 4 * (j % 4);
+        const v4h16 lo = lds_read_tr16(vp), hi = lds_read_tr16(vp + 4 * KLD);
+        o[mt] = mfma32(pack_v4(lo, hi), pf[s2], o[mt]);
       }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
