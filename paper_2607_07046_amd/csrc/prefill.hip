@@ -885,10 +885,11 @@ __global__ void __launch_bounds__(AW * kWave) attn_prefill_kernel(const uint16_t
 namespace {
 
 // Split-K choice of a GEMM: enough slices of whole k-tiles for about two
-// rounds of resident workgroups (GEMM_SLOTS each), at most 4. Measured on the
-// 256-token chunk of the 7B 50% shard: 4 slices beat 2, 3, 6 and 8 for the
-// gate/up, O and down GEMMs and are within 4% of 5 for QKV; more slices add
-// fp32 slab traffic, fewer leave compute units idle.
+// rounds of resident workgroups (GEMM_SLOTS each), at most MAX_SPLITS (the
+// in-kernel reduction's width). Measured on the 256-token chunk of the 7B 50%
+// shard with the fused epilogues: a cap of 4 slices beats 2 and 3 (0.162 ms
+// per chunk against 0.189 and 0.184); more slices add fp32 partial-tile
+// traffic and a longer reduction, fewer leave compute units idle.
 struct Split {
   int m_tiles, n_tiles, splits, kps;
 };
@@ -899,7 +900,7 @@ Split choose_split(int M, int N, int K) {
   s.n_tiles = (N + pf::GBN - 1) / pf::GBN;
   const int KT = std::max(1, (K + pf::GBK - 1) / pf::GBK);
   const int tiles = std::max(1, s.m_tiles * s.n_tiles);
-  const int want = std::max(1, std::min({KT, 4, (2 * pf::GEMM_SLOTS + tiles - 1) / tiles}));
+  const int want = std::max(1, std::min({KT, pf::MAX_SPLITS, (2 * pf::GEMM_SLOTS + tiles - 1) / tiles}));
   s.kps = (KT + want - 1) / want;
   s.splits = (KT + s.kps - 1) / s.kps;
   return s;
