@@ -171,6 +171,13 @@ typedef struct vt_layer_io {
 #define VT_STAGED 0x100u    /* decode only: one kernel launch per stage instead
                                of the single persistent kernel (same results
                                up to fp32 rounding order, which is fixed) */
+#define VT_COOPERATIVE 0x200u /* decode only, not with VT_STAGED: launch the
+                               persistent kernel through the cooperative
+                               launch, which guarantees that every workgroup
+                               is resident at once or fails the call
+                               (VT_ERR_HIP) before anything runs, instead of
+                               the bounded wait's asynchronous error word;
+                               costs launch time (same results bit for bit) */
 
 /* Append n_tok tokens' keys and values at positions pos..pos+n_tok-1 of
  * every KV head (paper Sec. 2.1, LLM Inference: the K and V of new tokens
@@ -202,7 +209,7 @@ vt_status vt_workspace_size(const vt_shard_spec* spec, int32_t max_tokens,
 
 /* Batch-1 decode of one token at position ``pos`` through the shard
  * (paper Sec. 2.1 LLM Inference, Sec. 3.2.1 TP shard). ``phases`` is
- * VT_ATTN, VT_FFN or both, optionally with VT_STAGED. With VT_ATTN the
+ * VT_ATTN, VT_FFN or both, optionally with VT_STAGED or VT_COOPERATIVE. With VT_ATTN the
  * token's rotated key and its value are appended at slot ``pos`` of every
  * shard KV head (pos must equal kv->len and be < capacity; kv->len becomes
  * pos + 1) and attention covers positions 0..pos. ``kv`` and ``pos`` are

@@ -937,8 +937,11 @@ static vt_status decode_impl(const vt_shard_spec* spec, const WeightView& W, vt_
 
 static vt_status check_phases(const vt_shard_spec* spec, const vt_layer_io* io, uint32_t phases) {
   if (!spec || !io) return fail(VT_ERR_ARG, "null spec or io");
-  if (phases & ~(VT_ATTN | VT_FFN | VT_STAGED)) return fail(VT_ERR_ARG, "unknown phase bits 0x%x", phases);
+  if (phases & ~(VT_ATTN | VT_FFN | VT_STAGED | VT_COOPERATIVE))
+    return fail(VT_ERR_ARG, "unknown phase bits 0x%x", phases);
   if (!(phases & (VT_ATTN | VT_FFN))) return fail(VT_ERR_ARG, "no phase selected");
+  if ((phases & VT_STAGED) && (phases & VT_COOPERATIVE))
+    return fail(VT_ERR_ARG, "VT_COOPERATIVE applies to the persistent launch, not VT_STAGED");
   return VT_OK;
 }
 
@@ -1078,6 +1081,7 @@ static vt_status decode_impl(const vt_shard_spec* spec, const WeightView& W, vt_
                              const vt_layer_io* io, int32_t pos, uint32_t phases, void* ws,
                              size_t ws_bytes, void* stream, const StackView& S) {
   const bool attn = phases & VT_ATTN, ffn = phases & VT_FFN, staged = phases & VT_STAGED;
+  const bool coop = phases & VT_COOPERATIVE;
   const vt_layer_dims& D = spec->dims;
   const vt_shard_info& in = spec->info;
   vt_status st = VT_OK;
@@ -1210,8 +1214,14 @@ static vt_status decode_impl(const vt_shard_spec* spec, const WeightView& W, vt_
   } else {
     P.phase_begin = pb;
     P.phase_end = pe;
-    hipLaunchKernelGGL(kern, dim3(di->cus), dim3(dec::NT), lds, s, P);
-    e = hipGetLastError();
+    if (coop) {
+      void* args[] = {&P};
+      e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kern), dim3(di->cus), dim3(dec::NT), args,
+                                     static_cast<unsigned>(lds), s);
+    } else {
+      hipLaunchKernelGGL(kern, dim3(di->cus), dim3(dec::NT), lds, s, P);
+      e = hipGetLastError();
+    }
   }
   if (e != hipSuccess) return fail(VT_ERR_HIP, "decode launch: %s", hipGetErrorString(e));
   if (attn) kv->len = pos + 1;

@@ -24,6 +24,7 @@ VT_ERR_WORKSPACE = -7
 VT_ATTN = 1
 VT_FFN = 2
 VT_STAGED = 0x100
+VT_COOPERATIVE = 0x200
 
 VT_PREC_FP16, VT_PREC_INT8, VT_PREC_INT4, VT_PREC_PRUNED = 0, 1, 2, 3
 VT_W_INT8, VT_W_INT4 = 1, 2

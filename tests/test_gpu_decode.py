@@ -86,11 +86,11 @@ def test_decode_matches_oracle(key, mode):
     assert not np.any(gs.sync_words()), "synchronisation words not cleared"
 
 
-def test_fused_staged_and_repeat_are_bitwise_equal():
+def test_fused_staged_cooperative_and_repeat_are_bitwise_equal():
     wl = get("7b")
     li, r, x, ref = oracle_case(wl)
     outs = []
-    for flags in (0, vt.VT_STAGED, 0):
+    for flags in (0, vt.VT_STAGED, 0, vt.VT_COOPERATIVE):
         gs = GpuShard(wl, li=li)
         outs.append((gs.decode(x, wl.ctx, BOTH | flags), gs.cache()))
     for o, c in outs[1:]:

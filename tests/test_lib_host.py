@@ -38,7 +38,7 @@ def test_binding_constants_match_header():
     with open(os.path.join(ROOT, "include", "voltron.h")) as f:
         hdr = f.read()
     defines = dict(re.findall(r"^#define\s+(VT_\w+)\s+(\w+)", hdr, re.M))
-    for name in ("VT_ATTN", "VT_FFN", "VT_STAGED", "VT_WS_ERROR_WORD"):
+    for name in ("VT_ATTN", "VT_FFN", "VT_STAGED", "VT_COOPERATIVE", "VT_WS_ERROR_WORD"):
         assert int(defines[name].rstrip("u"), 0) == getattr(vt, name), name
 
 
@@ -150,6 +150,8 @@ def test_decode_validation_errors(lib):
     assert call(ws=None) == vt.VT_ERR_WORKSPACE
     assert call(phases=0) == vt.VT_ERR_ARG
     assert call(phases=4) == vt.VT_ERR_ARG
+    # the cooperative launch is an option of the persistent launch only
+    assert call(phases=vt.VT_ATTN | vt.VT_STAGED | vt.VT_COOPERATIVE) == vt.VT_ERR_ARG
     w = _fake_weights()
     w.wq = A + 8
     assert call(w=w) == vt.VT_ERR_ALIGN
