@@ -117,7 +117,8 @@ def parse():
                          "of the layer and fit time = fixed + bytes / bandwidth (about a minute)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="instead of the bench: copy MIB MiB device-to-device 10 times "
-                         "(the known-size kernel that scales the HBM byte counters)")
+                         "(the known-size kernel that scales the HBM byte counters), then "
+                         "sum and fill the same bytes 10 times each (cross-checks)")
     return ap.parse_args()
 
 
@@ -130,8 +131,16 @@ def copy_calibration(mib):
     for _ in range(10):
         dst.copy_(src)
     torch.cuda.synchronize()
+    # cross-checks of the scale on kernels that only read or only write the
+    # same size: a sum over src, a fill of dst
+    for _ in range(10):
+        src.sum(dtype=torch.float32)
+    for _ in range(10):
+        dst.fill_(0.5)
+    torch.cuda.synchronize()
     print(json.dumps({"copy_calibration_bytes_read_per_launch": n * 2,
-                      "bytes_written_per_launch": n * 2, "launches": 10}))
+                      "bytes_written_per_launch": n * 2, "launches": 10,
+                      "cross_checks": "10 sums reading the same bytes, 10 fills writing them"}))
 
 
 def lib_dims(wd):
