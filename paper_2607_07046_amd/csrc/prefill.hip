@@ -442,14 +442,17 @@ __global__ void __launch_bounds__(GT, 2) gemm_kernel(GemmArgs g) {
       tl[(wave * 32 + 8 * (i / 4) + 4 * (lane / 32) + i % 4) * TLD + b * 32 + lane % 32] = acc[b][i];
   __syncthreads();
   // k-step-major outputs (the next GEMM's activation operand) are staged as
-  // fp16 in the first half of each token's LDS row (written over values its
-  // own wave has already read) and then copied out with consecutive threads
-  // on consecutive tokens, so each k-step's 16 features of the tile's tokens
-  // leave as one contiguous run.
+  // fp16 in the first half of each token's LDS row and then copied out with
+  // consecutive threads on consecutive tokens, so each k-step's 16 features
+  // of the tile's tokens leave as one contiguous run. A thread's staging
+  // store lands on floats that lanes of its own wave read in the same
+  // straight-line code just before, so only threads that have read their
+  // row may stage into it: the zero padding past the last valid feature
+  // (valid is a multiple of 8) is written at copy time, not staged.
   auto stage8 = [&](int mm, int f, u32x4 v) {
     *reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(tl + mm * TLD) + f) = v;
   };
-  auto copy_kmajor = [&](uint16_t* dst, int groups, int col0, int limit) {
+  auto copy_kmajor = [&](uint16_t* dst, int groups, int col0, int limit, int valid) {
     __syncthreads();
     for (int q = t / GBM; q < groups; q += GT / GBM) {
       const int mm = t % GBM, m = m0 + mm, col = col0 + 16 * q;
@@ -457,7 +460,8 @@ __global__ void __launch_bounds__(GT, 2) gemm_kernel(GemmArgs g) {
         const uint16_t* src = reinterpret_cast<const uint16_t*>(tl + mm * TLD) + 16 * q;
         uint16_t* o = dst + kmajor(col, m, g.M);
         *reinterpret_cast<u32x4*>(o) = *reinterpret_cast<const u32x4*>(src);
-        *reinterpret_cast<u32x4*>(o + 8) = *reinterpret_cast<const u32x4*>(src + 8);
+        *reinterpret_cast<u32x4*>(o + 8) =
+            col + 8 < valid ? *reinterpret_cast<const u32x4*>(src + 8) : u32x4{0u, 0u, 0u, 0u};
       }
     }
   };
@@ -538,15 +542,13 @@ __global__ void __launch_bounds__(GT, 2) gemm_kernel(GemmArgs g) {
         *reinterpret_cast<u32x4*>(g.partial + e) = pack8(ph);
         if (g.out) *reinterpret_cast<u32x4*>(g.out + e) = pack8(oh);
         if (norm) stage8(mm, f, pack8(uh));
-      } else if (norm && n < hpad) {
-        stage8(mm, f, u32x4{0u, 0u, 0u, 0u});  // K padding
       }
       if (norm) {
         sq = sum16(sq);
         if (t % 16 == 0) g.rowsq[static_cast<int64_t>(m) * g.n_tiles + n_tile] = sq;
       }
     }
-    if (norm) copy_kmajor(g.U, GBN / 16, n0, hpad);
+    if (norm) copy_kmajor(g.U, GBN / 16, n0, hpad, g.H);
   } else {  // EPI_GU: tile features 0..63 gate and 64..127 up of the same 64 columns
     float* rinv = tl + GBM * TLD;  // 1 / rms of the tile's tokens
     if (g.rowsq) {
@@ -585,7 +587,7 @@ __global__ void __launch_bounds__(GT, 2) gemm_kernel(GemmArgs g) {
         stage8(mm, f, pack8(h));
       }
     }
-    copy_kmajor(g.Mo, 4, col0, g.kpad);
+    copy_kmajor(g.Mo, 4, col0, g.kpad, g.kpad);
   }
 }
 

@@ -84,6 +84,38 @@ def test_prefill_ragged_shapes(case):
     run_case(wl, T)
 
 
+# Seeded shapes around the GEMM tiles' edges (128 tokens, 128 features,
+# 64 k-columns, 16-column k-steps): tokens one either side of a tile, hidden
+# sizes that are multiples of 8 but not of 16 or 128, odd FFN shares, both
+# head sizes, GQA groups; drawn once from a fixed seed.
+def _edge_cases():
+    rng = np.random.default_rng(20261202)
+    out = []
+    for i, T in enumerate((127, 128, 129, 255, 257)):
+        d = (64, 128)[i % 2]
+        nkv = int(rng.choice([1, 2, 4]))
+        nh = nkv * int(rng.choice([1, 2, 4]))
+        while nh < 2:
+            nh *= 2
+        H = int(rng.choice([520, 776, 1032, 1288]))
+        F = int(rng.integers(300, 1500))
+        fr = (0.5, 0.5) if nh % 2 == 0 and nkv % 2 == 0 else (1.0,)
+        dev = int(rng.integers(0, len(fr)))
+        ctx = int(rng.integers(0, 60))
+        out.append((400 + i, H, nh, nkv, d, F, fr, dev, ctx, T))
+    return out
+
+
+EDGE = _edge_cases()
+
+
+@pytest.mark.parametrize("case", EDGE, ids=[f"T{c[9]}-H{c[1]}-d{c[4]}" for c in EDGE])
+def test_prefill_tile_edges(case):
+    seed, H, nh, nkv, d, F, fr, dev, ctx, T = case
+    wl = tiny_workload(seed, H, nh, nkv, d, F, fr, dev, ctx, sigma=0.03, chunk=T)
+    run_case(wl, T)
+
+
 def test_prefill_then_decode_continues_the_cache():
     wl = tiny_workload(305, 512, 8, 4, 64, 800, (0.5, 0.5), 0, 20, sigma=0.03, chunk=9)
     li = LayerInputs(wl)
