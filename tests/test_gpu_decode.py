@@ -180,6 +180,50 @@ def test_ragged_shapes_and_gqa_groups(mode):
     check_kv(gs, ref, wl.ctx, k0, v0)
 
 
+# Seeded shapes with hidden sizes that are multiples of 8 but not of 16, 32
+# or 64 (the last weight piece of every K = hidden row is ragged), hidden
+# unequal to heads x head_dim, odd FFN shares, both head sizes, GQA groups
+# and contexts over several attention chunks; drawn once from a fixed seed.
+def _ragged_hidden_cases():
+    rng = np.random.default_rng(20261203)
+    out = []
+    for i in range(4):
+        d = (64, 128)[i % 2]
+        nkv = int(rng.choice([1, 2, 4]))
+        nh = max(2, nkv * int(rng.choice([1, 2, 4])))
+        H = int(rng.choice([520, 776, 1032, 1288]))
+        F = int(rng.integers(300, 1500))
+        fr = (0.5, 0.5) if nh % 2 == 0 and nkv % 2 == 0 else (1.0,)
+        dev = int(rng.integers(0, len(fr)))
+        ctx = int(rng.integers(0, 300))
+        out.append((600 + i, H, nh, nkv, d, F, fr, dev, ctx))
+    return out
+
+
+RAGGED_H = _ragged_hidden_cases()
+RAGGED_IDS = [f"H{c[1]}-h{c[2]}-kv{c[3]}-d{c[4]}-F{c[5]}" for c in RAGGED_H]
+
+
+@pytest.mark.parametrize("mode", MODES)
+@pytest.mark.parametrize("case", RAGGED_H, ids=RAGGED_IDS)
+def test_ragged_hidden_sizes(case, mode):
+    wl = tiny_workload(*case, sigma=0.03)
+    li, r, x, ref = oracle_case(wl)
+    gs = GpuShard(wl, li=li)
+    k0, v0 = gs.cache()
+    pa, pf = li.peer("attn"), li.peer("ffn")
+    d = wl.dims
+    w = oracle_shard_weights(li, r)
+    kc, vc = li.kv_context_heads(r.kv_head_begin, r.kv_head_begin + r.n_kv_heads)
+    ref = oracle.decode(w, r.n_q_heads, r.n_kv_heads, d.head_dim, d.rms_eps, d.rope_base, x, kc,
+                        vc, wl.ctx, pa, pf)
+    ref = ffn_at_h16(w, d.rms_eps, ref, pf)
+    got = gs.decode(x, wl.ctx, BOTH | MODES[mode], peer_attn=pa, peer_ffn=pf)
+    check_outputs(got, ref)
+    check_kv(gs, ref, wl.ctx, k0, v0)
+    assert not np.any(gs.sync_words()), "synchronisation words not cleared"
+
+
 def test_empty_shard_outputs_zero_partials():
     """A device that gets no heads and no columns (e.g. one whose share was
     pruned away) contributes zero partials; h and y pass x and peers through."""

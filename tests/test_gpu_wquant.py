@@ -21,6 +21,7 @@ from synth import get
 from synth.gen import LayerInputs
 from tests.common import assert_close, ffn_at_h16, oracle_qshard_weights, oracle_ranges, tiny_workload
 from tests.gpu_common import GpuShard
+from tests.test_gpu_decode import RAGGED_H, RAGGED_IDS
 
 pytestmark = pytest.mark.gpu
 
@@ -129,6 +130,14 @@ def test_decode_q_ragged_columns(level):
     # GQA groups of 2
     wl = tiny_workload(411, 512, 8, 4, 64, 1000, (0.33, 0.34, 0.33), 1, 40)
     run(wl, level)
+
+
+@pytest.mark.parametrize("level", LEVELS)
+@pytest.mark.parametrize("case", RAGGED_H[:2], ids=RAGGED_IDS[:2])
+def test_decode_q_ragged_hidden(case, level):
+    # hidden a multiple of 8 but not of 32: the last 32-column block of every
+    # K = hidden row is partial
+    run(tiny_workload(*case, sigma=0.03), level)
 
 
 @pytest.mark.parametrize("level", LEVELS)
