@@ -137,32 +137,38 @@ def test_prefill_then_decode_continues_the_cache():
         assert_close(got[k], ref[k], k)
 
 
-def test_prefill_attention_then_ffn_calls():
+@pytest.mark.parametrize("shape", [
+    # seed, hidden, heads, kv, d, ffn, fracs, device, ctx, T
+    (307, 512, 8, 4, 64, 700, (0.5, 0.5), 1, 30, 37),
+    (309, 1032, 4, 2, 128, 900, (0.5, 0.5), 0, 11, 130),   # hidden a multiple of 8, not 16
+], ids=["h512", "h1032"])
+def test_prefill_attention_then_ffn_calls(shape):
     """The two sub-layers as separate calls: VT_ATTN alone (the O GEMM's
     epilogue without the FFN input), then VT_FFN alone from the device's h
     (the RMSNorm before the gate/up GEMM computed on its own); the FFN is
     checked against the oracle's FFN sub-layer at exactly that h."""
-    wl = tiny_workload(307, 512, 8, 4, 64, 700, (0.5, 0.5), 1, 30, sigma=0.03, chunk=37)
+    seed, H, nh, nkv, hd, F, fr, dev, ctx, T = shape
+    wl = tiny_workload(seed, H, nh, nkv, hd, F, fr, dev, ctx, sigma=0.03, chunk=T)
     li = LayerInputs(wl)
     d = wl.dims
     r = oracle_ranges(wl)
     w = oracle_shard_weights(li, r)
     kc, vc = li.kv_context_heads(r.kv_head_begin, r.kv_head_begin + r.n_kv_heads)
-    X = li.x_chunk(37)
-    pa, pf = li.peer("attn", rows=37), li.peer("ffn", rows=37)
+    X = li.x_chunk(T)
+    pa, pf = li.peer("attn", rows=T), li.peer("ffn", rows=T)
     ref = oracle.prefill(w, r.n_q_heads, r.n_kv_heads, d.head_dim, d.rms_eps, d.rope_base, X, kc,
                          vc, wl.ctx, pa, pf)
-    gs = GpuShard(wl, li=li, capacity=wl.ctx + 40, max_tokens=37)
+    gs = GpuShard(wl, li=li, capacity=wl.ctx + T + 3, max_tokens=T)
     a = gs.prefill(X, wl.ctx, vt.VT_ATTN, peer_attn=pa)
     for k in ("p_attn", "h"):
         assert_close(a[k], ref[k], k)
     assert np.isnan(a["p_ffn"]).all() and np.isnan(a["y"]).all()  # not written
-    assert gs.kv.len == wl.ctx + 37
+    assert gs.kv.len == wl.ctx + T
     f = gs.prefill(None, wl.ctx, vt.VT_FFN, peer_ffn=pf, h_in=a["h"])
     fr = ffn_at_h16(w, d.rms_eps, {"h": a["h"]}, pf)
     for k in ("p_ffn", "y"):
         assert_close(f[k], fr[k], k)
-    assert gs.kv.len == wl.ctx + 37
+    assert gs.kv.len == wl.ctx + T
 
 
 def test_prefill_ignores_row_padding():

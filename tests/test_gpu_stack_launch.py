@@ -145,6 +145,15 @@ def test_one_layer_stack_equals_layer_decode():
     check_first_layer(st, outs, 2)
 
 
+def test_ragged_hidden_stack_equals_layer_chain():
+    # hidden a multiple of 8 but not of 16 (the last weight piece of every
+    # K = hidden row and the next layer's x staging are ragged)
+    wl = tiny_workload(504, 1032, 4, 2, 128, 900, (0.5, 0.5), 1, 20, sigma=0.03)
+    st = Stack(wl, 3, wl.ctx + 3)
+    outs = check_equal(st, 3)
+    check_first_layer(st, outs, 3)
+
+
 def test_13b_four_layers_equal_layer_chain():
     wl = get("13b_stack")
     st = Stack(wl, 4, wl.ctx + 3)
