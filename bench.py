@@ -1053,6 +1053,8 @@ def prefill_section(steps, warmup, eager=False):
     if not torch.isfinite(outs[3].float()).all():
         raise SystemExit("non-finite prefill output")
     flops = gemm_flops + attn_flops
+    vendor = vendor_gemm_reference(T, [((info.n_q_heads + 2 * nkv) * d, H), (H, info.n_q_heads * d),
+                                       (2 * info.n_cols, H), (H, info.n_cols)], steps)
     return {
         "workload": wl.key,
         "shape": f"{T} tokens at positions {pos0}..{pos0 + T - 1}, {info.n_q_heads} q / "
@@ -1073,7 +1075,42 @@ def prefill_section(steps, warmup, eager=False):
         "bound_us": round(max(flops / (MFMA_F16_PEAK_TFLOPS * 1e12),
                               nbytes / (HBM_PEAK_GBPS * 1e9)) * 1e6, 2),
         "launch": "6 kernels per chunk, " + ("eager" if eager else "hipgraph"),
+        "vendor_gemm": vendor,
     }
+
+
+def vendor_gemm_reference(M, shapes, steps):
+    """For scale only: the vendor fp16 GEMM (torch.matmul, i.e. hipBLASLt)
+    on the chunk's four projection shapes (M tokens x N outputs x K, weights
+    [N][K] row-major as the shard stores them), plain products without the
+    epilogues, rotated weight copies past the memory-side cache."""
+    import torch
+
+    dev = torch.device("cuda:0")
+    gen = torch.Generator(device=dev).manual_seed(7)
+    wbytes = sum(2 * n * k for n, k in shapes)
+    copies = max(1, math.ceil(MALL_DEFEAT_BYTES / wbytes))
+    names = ("qkv", "o", "gate_up", "down")
+    acts = [torch.randn((M, k), generator=gen, device=dev, dtype=torch.float16) for _, k in shapes]
+    ws = [[torch.randn((n, k), generator=gen, device=dev, dtype=torch.float16) * 0.02
+           for n, k in shapes] for _ in range(copies)]
+    outs = [torch.empty((M, n), device=dev, dtype=torch.float16) for n, _ in shapes]
+    reps = max(copies, steps // 4)
+    per = {}
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    for j, name in enumerate(names):
+        for i in range(copies):
+            torch.matmul(acts[j], ws[i][j].t(), out=outs[j])
+        torch.cuda.synchronize()
+        ev[0].record()
+        for i in range(reps):
+            torch.matmul(acts[j], ws[i % copies][j].t(), out=outs[j])
+        ev[1].record()
+        torch.cuda.synchronize()
+        per[name] = round(ev[0].elapsed_time(ev[1]) * 1e3 / reps, 2)
+    del ws
+    return {"what": "torch.matmul (hipBLASLt) fp16, the four GEMM shapes, no epilogues",
+            "us_per_gemm": per, "us_total": round(sum(per.values()), 2)}
 
 
 def cpu_baseline(wl, budget_s):
