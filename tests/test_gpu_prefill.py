@@ -8,6 +8,8 @@ its slot and every other cache byte is unchanged. Also: the sub-layers as
 separate calls, NaN in the weight rows' padding, and bit-identical repeats
 (the split-K reduction's order does not depend on arrival order).
 """
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -66,6 +68,66 @@ def test_prefill_7b_chunk_full_size():
     """256 tokens at positions 768..1023 through the 50% shard of the 7B layer."""
     wl = get("7b_prefill")
     run_case(wl, wl.chunk)
+
+
+def _sample_rows(T, seed, n_random=24):
+    """Rows at both edges of every 128-row GEMM tile plus seeded random ones."""
+    rows = {0, 1, T - 2, T - 1}
+    for e in range(128, T, 128):
+        rows |= {e - 1, e}
+    rng = np.random.default_rng(seed)
+    rows |= set(int(r) for r in rng.integers(0, T, n_random))
+    return sorted(r for r in rows if 0 <= r < T)
+
+
+@pytest.mark.parametrize("T", [1024, 4096])
+def test_prefill_long_chunks(T):
+    """The 7B 50% shard with 1024 and 4096 tokens at positions 768.. : the
+    split-K choice goes from 4 slices down to 3, 2 and 1 (no reduction), and
+    the attention runs over up to 4864 keys. Every appended key and value is
+    checked; the layer outputs on rows at both edges of every 128-row tile
+    and seeded random rows, each against the oracle's decode step of that
+    token over the context and the chunk's earlier keys and values (the
+    oracle's attention sub-layer with a one-position window gives the
+    chunk's keys and values: they do not depend on the window)."""
+    wl = get("7b_prefill")
+    li = LayerInputs(wl)
+    d = wl.dims
+    r = oracle_ranges(wl)
+    w = oracle_shard_weights(li, r)
+    # the same values held as float64 once, so the per-row oracle calls below
+    # do not widen the shard's weights again each time
+    w = oracle.ShardWeights(**{f.name: np.asarray(getattr(w, f.name), np.float64)
+                               for f in dataclasses.fields(w)})
+    kc, vc = li.kv_context_heads(r.kv_head_begin, r.kv_head_begin + r.n_kv_heads)
+    X = li.x_chunk(T)
+    pa, pf = li.peer("attn", rows=T), li.peer("ffn", rows=T)
+    gs = GpuShard(wl, li=li, capacity=wl.ctx + T, max_tokens=T)
+    k0, v0 = gs.cache()
+    got = gs.prefill(X, wl.ctx, BOTH, peer_attn=pa, peer_ffn=pf)
+    assert not gs.sync_words().any()
+    _, _, K, V = oracle.attn_sublayer(w, r.n_q_heads, r.n_kv_heads, d.head_dim, d.rms_eps,
+                                      d.rope_base, X, kc, vc, wl.ctx, window=1)
+    kc1, vc1 = gs.cache()
+    assert gs.kv.len == wl.ctx + T
+    assert np.array_equal(kc1[:, :wl.ctx], k0[:, :wl.ctx])
+    assert np.array_equal(vc1[:, :wl.ctx], v0[:, :wl.ctx])
+    rng = slice(wl.ctx, wl.ctx + T)
+    kn = kc1[:, rng].view(np.float16).astype(np.float64)
+    vn = vc1[:, rng].view(np.float16).astype(np.float64)
+    assert_close(np.transpose(kn, (1, 0, 2)).reshape(T, -1), K.reshape(T, -1), "appended keys")
+    assert_close(np.transpose(vn, (1, 0, 2)).reshape(T, -1), V.reshape(T, -1), "appended values")
+    rows = _sample_rows(T, 7000 + T)
+    ref = {k: [] for k in ("p_attn", "h", "p_ffn", "y")}
+    for t in rows:
+        kt, vt_ = oracle.append_kv(kc, vc, K[:t], V[:t], wl.ctx)
+        o = oracle.decode(w, r.n_q_heads, r.n_kv_heads, d.head_dim, d.rms_eps, d.rope_base, X[t],
+                          kt, vt_, wl.ctx + t, pa[t], pf[t])
+        o = ffn_at_h16(w, d.rms_eps, o, pf[t])
+        for k in ref:
+            ref[k].append(o[k])
+    for k in ref:
+        assert_close(got[k][rows], np.stack(ref[k]), f"{k} on {len(rows)} sampled rows")
 
 
 CASES = [
