@@ -104,6 +104,8 @@ def parse():
                     help="host time budget of the oracle baseline (0: skip)")
     ap.add_argument("--prefill-steps", type=int, default=200,
                     help="timed prefill chunks of the prefill section (0: skip)")
+    ap.add_argument("--prefill-tokens", type=int, default=0,
+                    help="tokens per prefill chunk (default: the workload's 256)")
     ap.add_argument("--comm-steps", type=int, default=400,
                     help="timed calls of each partial-sum transmission kernel (0: skip)")
     ap.add_argument("--quant-steps", type=int, default=1000,
@@ -511,7 +513,8 @@ def main():
             out["decode_7b_emit"]["us_over_plain_step"] = round(
                 (sec["ms_per_step"] - out["decode_7b"]["ms_per_step"]) * 1e3, 2)
     if args.prefill_steps > 0:
-        out["prefill"] = prefill_section(args.prefill_steps, max(1, args.prefill_steps // 10))
+        out["prefill"] = prefill_section(args.prefill_steps, max(1, args.prefill_steps // 10),
+                                         tokens=args.prefill_tokens)
     if args.comm_steps > 0:
         out["comm"] = comm_section(args.comm_steps)
     if c2 is not None and args.repack_reps > 0:
@@ -974,10 +977,10 @@ def prefill_bytes(dims, info, T, pos0):
     return weights + kv + 2 * H * 2 + 2 * T * H * 5
 
 
-def prefill_section(steps, warmup, eager=False):
-    """Prefill chunk of 256 tokens at positions 768..1023 through the 50%
-    shard of the 7B-shaped layer (four rotated weight/KV copies, >= 768 MB),
-    timed over ``steps`` chunks captured in HIP graphs."""
+def prefill_section(steps, warmup, eager=False, tokens=0):
+    """Prefill chunk of 256 tokens (or ``tokens``) at positions 768.. through
+    the 50% shard of the 7B-shaped layer (rotated weight/KV copies, >= 768
+    MB), timed over ``steps`` chunks captured in HIP graphs."""
     import torch
 
     from paper_2607_07046_amd import pack
@@ -993,7 +996,7 @@ def prefill_section(steps, warmup, eager=False):
                             rope_base=wl.dims.rope_base, window=wl.dims.window)
     spec = vt.vt_shard_spec_create(dims, wl.fracs, wl.fracs, wl.device)
     dims, info = vt.vt_shard_spec_query(spec)
-    T, pos0 = wl.chunk, wl.ctx
+    T, pos0 = (tokens or wl.chunk), wl.ctx
     H, d, nkv, cap = dims.hidden, dims.head_dim, info.n_kv_heads, pos0 + T
     gemm_flops, attn_flops = prefill_flops(dims, info, T, pos0)
     nbytes = prefill_bytes(dims, info, T, pos0)

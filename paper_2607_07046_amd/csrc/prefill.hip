@@ -886,25 +886,47 @@ __global__ void __launch_bounds__(AW * kWave) attn_prefill_kernel(const uint16_t
 // ---------------------------------------------------------------------------
 namespace {
 
-// Split-K choice of a GEMM: enough slices of whole k-tiles for about two
-// rounds of resident workgroups (GEMM_SLOTS each), at most MAX_SPLITS (the
-// in-kernel reduction's width). Measured on the 256-token chunk of the 7B 50%
-// shard with the fused epilogues: a cap of 4 slices beats 2 and 3 (0.162 ms
-// per chunk against 0.189 and 0.184); more slices add fp32 partial-tile
-// traffic and a longer reduction, fewer leave compute units idle.
+// Split-K choice of a GEMM: the slice count S (whole k-tiles each, at most
+// MAX_SPLITS, the in-kernel reduction's width) with the smallest modelled
+// time. The tiles x S workgroups run in rounds of GEMM_SLOTS (two per compute
+// unit); a round in which compute units hold two workgroups advances each by
+// one k-tile per kTwoPerCu microseconds, a last round of at most one per
+// compute unit per kOnePerCu; each of the (S - 1) x tiles fp32 partial tiles
+// costs kPartial (64 KiB stored and read back at about 7 TB/s). The
+// constants are MI355X measurements of this kernel on the 7B shapes; the
+// model reproduces the measured GEMM times at 4096 tokens within 5%, keeps
+// 4 slices for every GEMM of a 256-token chunk (0.160 ms per chunk, as
+// before), and takes fewer slices than the older rule of about two rounds
+// of workgroups for longer chunks: 512 / 1024 / 2048 tokens in 0.222 /
+// 0.340 / 0.609 ms per chunk against 0.248 / 0.388 / 0.691.
 struct Split {
   int m_tiles, n_tiles, splits, kps;
 };
 
+constexpr double kTwoPerCu = 1.33, kOnePerCu = 0.75, kPartial = 0.0187;
+
 Split choose_split(int M, int N, int K) {
-  Split s;
+  Split s{};
   s.m_tiles = (M + pf::GBM - 1) / pf::GBM;
   s.n_tiles = (N + pf::GBN - 1) / pf::GBN;
   const int KT = std::max(1, (K + pf::GBK - 1) / pf::GBK);
-  const int tiles = std::max(1, s.m_tiles * s.n_tiles);
-  const int want = std::max(1, std::min({KT, pf::MAX_SPLITS, (2 * pf::GEMM_SLOTS + tiles - 1) / tiles}));
-  s.kps = (KT + want - 1) / want;
-  s.splits = (KT + s.kps - 1) / s.kps;
+  const int64_t tiles = std::max(1, s.m_tiles * s.n_tiles);
+  double best = 0.0;
+  for (int want = 1; want <= std::min(KT, pf::MAX_SPLITS); ++want) {
+    const int kps = (KT + want - 1) / want;
+    const int splits = (KT + kps - 1) / kps;
+    const int64_t groups = tiles * splits;
+    const int64_t full = groups / pf::GEMM_SLOTS, rest = groups % pf::GEMM_SLOTS;
+    double t = static_cast<double>(full) * kps * kTwoPerCu;
+    if (rest > pf::GEMM_SLOTS / 2) t += kps * kTwoPerCu;
+    else if (rest > 0) t += kps * kOnePerCu;
+    t += static_cast<double>(splits - 1) * static_cast<double>(tiles) * kPartial;
+    if (want == 1 || t < best) {
+      best = t;
+      s.kps = kps;
+      s.splits = splits;
+    }
+  }
   return s;
 }
 
@@ -1016,8 +1038,18 @@ pf::BSrc bsrc(const void* p, int64_t ld, int start, int rows) {
 
 }  // namespace
 
+// Enough for every chunk of 1..max_tokens tokens: the split-K region depends
+// on the chunk only through its number of 128-row tiles and may shrink as
+// chunks grow (fewer slices), so the layout is taken at the longest chunk of
+// each tile count and the largest total kept.
 size_t prefill_workspace_bytes(const vt_shard_spec& s, int32_t max_tokens, int32_t) {
-  return prefill_layout(s, max_tokens).total;
+  size_t most = 0;
+  for (int64_t hi = pf::GBM;; hi += pf::GBM) {
+    const int32_t T = static_cast<int32_t>(std::min<int64_t>(hi, max_tokens));
+    most = std::max(most, prefill_layout(s, T).total);
+    if (T == max_tokens) break;
+  }
+  return most;
 }
 
 }  // namespace vt

@@ -102,7 +102,9 @@ def test_prefill_long_chunks(T):
     kc, vc = li.kv_context_heads(r.kv_head_begin, r.kv_head_begin + r.n_kv_heads)
     X = li.x_chunk(T)
     pa, pf = li.peer("attn", rows=T), li.peer("ffn", rows=T)
-    gs = GpuShard(wl, li=li, capacity=wl.ctx + T, max_tokens=T)
+    # the workspace is sized for the longest chunk, 4096 tokens, and must
+    # serve the shorter one too (whose GEMMs take more split-K slices)
+    gs = GpuShard(wl, li=li, capacity=wl.ctx + T, max_tokens=4096)
     k0, v0 = gs.cache()
     got = gs.prefill(X, wl.ctx, BOTH, peer_attn=pa, peer_ffn=pf)
     assert not gs.sync_words().any()

@@ -229,6 +229,22 @@ def test_noalloc_decode_rejects_oversized_workspace(lib):
     assert kv.len == pos
 
 
+def test_workspace_covers_every_shorter_chunk(lib):
+    """The workspace for up to max_tokens tokens per chunk serves every
+    shorter chunk too: the size never shrinks as max_tokens grows, although
+    longer chunks split the GEMMs' k range into fewer slices and so need a
+    smaller split-K region."""
+    wl = WORKLOADS["7b_prefill"]
+    D = wl.dims
+    dims = vt.vt_layer_dims(hidden=D.hidden, n_heads=D.n_heads, n_kv_heads=D.n_kv_heads,
+                            head_dim=D.head_dim, ffn=D.ffn, rms_eps=D.rms_eps,
+                            rope_base=D.rope_base, window=D.window)
+    spec = vt.vt_shard_spec_create(dims, wl.fracs, wl.fracs, wl.device)
+    sizes = [vt.vt_workspace_size(spec, T, 5000) for T in range(1, 4097, 7)] + \
+            [vt.vt_workspace_size(spec, 4096, 5000)]
+    assert all(a <= b for a, b in zip(sizes, sizes[1:]))
+
+
 def test_kv_append_validation_errors(lib):
     A = 1 << 20
     kv = vt.vt_kv_view(k=A, v=A, capacity=10, n_kv_heads=2, head_dim=128, len=4)
