@@ -224,6 +224,27 @@ def test_ragged_hidden_sizes(case, mode):
     assert not np.any(gs.sync_words()), "synchronisation words not cleared"
 
 
+GROUPS = {
+    # seed, hidden, heads, kv, d, ffn, fracs, device, ctx: query heads per KV
+    # head that are not powers of two
+    "g3": (610, 1536, 12, 4, 128, 1000, (0.5, 0.5), 1, 333),
+    "g7": (611, 1792, 28, 4, 64, 1200, (0.5, 0.5), 0, 515),
+}
+
+
+@pytest.mark.parametrize("mode", MODES)
+@pytest.mark.parametrize("key", GROUPS)
+def test_gqa_groups_not_powers_of_two(key, mode):
+    wl = tiny_workload(*GROUPS[key], sigma=0.03)
+    li, r, x, ref = oracle_case(wl)
+    assert r.n_q_heads == r.n_kv_heads * (wl.dims.n_heads // wl.dims.n_kv_heads)
+    gs = GpuShard(wl, li=li)
+    k0, v0 = gs.cache()
+    got = gs.decode(x, wl.ctx, BOTH | MODES[mode])
+    check_outputs(got, ref)
+    check_kv(gs, ref, wl.ctx, k0, v0)
+
+
 def test_empty_shard_outputs_zero_partials():
     """A device that gets no heads and no columns (e.g. one whose share was
     pruned away) contributes zero partials; h and y pass x and peers through."""

@@ -138,6 +138,8 @@ CASES = [
     (302, 512, 8, 2, 64, 1000, (0.5, 0.5), 1, 7, 5),        # GQA group 4, ragged everything
     (303, 1024, 8, 4, 128, 1501, (0.6, 0.4), 0, 40, 70),    # d 128, odd FFN width, 3 query blocks
     (304, 768, 12, 12, 64, 2000, (0.3, 0.7), 1, 100, 129),  # M > one 128-row tile, 5 query blocks
+    (310, 1536, 12, 4, 128, 1000, (0.5, 0.5), 1, 90, 77),   # GQA group 3
+    (311, 1792, 28, 4, 64, 1200, (0.5, 0.5), 0, 45, 140),   # GQA group 7
 ]
 
 
