@@ -608,7 +608,7 @@ __global__ void __launch_bounds__(RT) rmsnorm_rows_kernel(const uint16_t* X, con
   __shared__ float red[RT / kWave];
   const int t = blockIdx.x, M = gridDim.x;
   for (int i = t * RT + threadIdx.x; i < ncnt; i += M * RT) cnt[i] = 0u;
-  if (rope && threadIdx.x < d / 2) {
+  if (rope && static_cast<int>(threadIdx.x) < d / 2) {
     float c, s;
     rope_angle(pos0 + t, threadIdx.x, d, base, c, s);
     *reinterpret_cast<float2*>(rope + (static_cast<int64_t>(t) * (d / 2) + threadIdx.x) * 2) = make_float2(c, s);
@@ -740,18 +740,30 @@ __global__ void __launch_bounds__(AW * kWave) attn_prefill_kernel(const uint16_t
   const uint16_t* vbase = vc + static_cast<int64_t>(g) * cap * D;
   constexpr int CH = KB * D / 8;     // 16-byte chunks per K (or V) tile
   constexpr int CPL = CH / kWave;    // chunks per lane
-  // Key block kb's chunks into registers; positions past last_key (never
-  // attended) read as zero. Loads are unconditional (clamped position) so
-  // the block is fetched in one round trip.
+  // Key block kb's chunks into registers through buffer ranges that end
+  // after last_key: positions past it (never attended) read as zero, and
+  // the block is fetched in one round trip. Chunk u of this lane: key
+  // (lane + 64 u) / (D/8) of the block, 8 dimensions from col; its byte
+  // offset within the block and its LDS offsets do not depend on the block.
+  const uint32_t range = static_cast<uint32_t>(last_key + 1) * D * 2u;
+  const rsrc_t rk = make_rsrc(kbase, range), rv = make_rsrc(vbase, range);
+  uint32_t goff[CPL];
+  int kst[CPL], vst[CPL];
+#pragma unroll
+  for (int u = 0; u < CPL; ++u) {
+    const int c = lane + u * kWave;
+    const int key = c / (D / 8), col = (c % (D / 8)) * 8;
+    goff[u] = static_cast<uint32_t>(key * D + col) * 2u;
+    kst[u] = swap_bits23(key) * KLD + col;
+    vst[u] = key * KLD + col;
+  }
   u32x4 kreg[CPL], vreg[CPL];
   auto fetch = [&](int kb) {
+    const uint32_t base = static_cast<uint32_t>(kb * KB) * D * 2u;
 #pragma unroll
     for (int u = 0; u < CPL; ++u) {
-      const int c = lane + u * kWave;
-      const int key = c / (D / 8), col = (c % (D / 8)) * 8;
-      const int p = min(kb * KB + key, last_key);
-      kreg[u] = load16(kbase + static_cast<int64_t>(p) * D + col);
-      vreg[u] = load16(vbase + static_cast<int64_t>(p) * D + col);
+      kreg[u] = buf_load16(rk, base + goff[u]);
+      vreg[u] = buf_load16(rv, base + goff[u]);
     }
   };
   fetch(min(kb0 + wave, nkb - 1));
@@ -760,13 +772,8 @@ __global__ void __launch_bounds__(AW * kWave) attn_prefill_kernel(const uint16_t
     // stage K (rows permuted) and V (row-major), then start the next block
 #pragma unroll
     for (int u = 0; u < CPL; ++u) {
-      const int c = lane + u * kWave;
-      const int key = c / (D / 8), col = (c % (D / 8)) * 8;
-      const bool live = p0 + key <= last_key;
-      const u32x4 kv = live ? kreg[u] : u32x4{0u, 0u, 0u, 0u};
-      const u32x4 vv = live ? vreg[u] : u32x4{0u, 0u, 0u, 0u};
-      *reinterpret_cast<u32x4*>(Ks + swap_bits23(key) * KLD + col) = kv;
-      *reinterpret_cast<u32x4*>(Vs + key * KLD + col) = vv;
+      *reinterpret_cast<u32x4*>(Ks + kst[u]) = kreg[u];
+      *reinterpret_cast<u32x4*>(Vs + vst[u]) = vreg[u];
     }
     // LDS operations of one wave complete in issue order; this keeps the
     // compiler from moving the tile reads above the writes
@@ -781,24 +788,43 @@ __global__ void __launch_bounds__(AW * kWave) attn_prefill_kernel(const uint16_t
           *reinterpret_cast<const u32x4*>(Ks + (lane % 32) * KLD + ks * 16 + 8 * (lane / 32));
       s = mfma32(kf, qfrag(ks), s);
     }
-    // accumulator i: LDS row 8(i/4) + 4(l/32) + i%4 holds key p0 + swap_bits23(row)
+    // accumulator i: LDS row 8(i/4) + 4(l/32) + i%4 holds key p0 + swap_bits23(row).
+    // Only a block that reaches past the block's first query, lies partly
+    // outside a sliding window, or serves queries past T masks anything;
+    // every other block skips the per-element tests (same values).
+    const bool masked = p0 + KB - 1 > pos0 + t0 || t0 + QB > T ||
+                        (window > 0 && p0 <= pos0 + t0 + QB - 1 - window);
     float bm = -INFINITY;
+    if (masked) {
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int key = swap_bits23(8 * (i / 4) + 4 * (lane / 32) + i % 4);
-      if (p0 + key > qpos || tq >= T || (window > 0 && p0 + key <= qpos - window)) s[i] = -INFINITY;
-      bm = fmaxf(bm, s[i]);
+      for (int i = 0; i < 16; ++i) {
+        const int key = swap_bits23(8 * (i / 4) + 4 * (lane / 32) + i % 4);
+        if (p0 + key > qpos || tq >= T || (window > 0 && p0 + key <= qpos - window)) s[i] = -INFINITY;
+        bm = fmaxf(bm, s[i]);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) bm = fmaxf(bm, s[i]);
     }
     bm = fmaxf(bm, __shfl_xor(bm, 32, kWave));
     const float mnew = fmaxf(mrun, bm);
     const float alpha = mrun == -INFINITY ? 0.f : __expf(mrun - mnew);
     float ps = 0.f;
     uint16_t ph[16];
+    if (masked) {
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const float e = s[i] == -INFINITY ? 0.f : __expf(s[i] - mnew);
-      ps += e;
-      ph[i] = f2h(e);
+      for (int i = 0; i < 16; ++i) {
+        const float e = s[i] == -INFINITY ? 0.f : __expf(s[i] - mnew);
+        ps += e;
+        ph[i] = f2h(e);
+      }
+    } else {  // no score is -inf here, and mnew is finite
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const float e = __expf(s[i] - mnew);
+        ps += e;
+        ph[i] = f2h(e);
+      }
     }
     ps += __shfl_xor(ps, 32, kWave);
     lrun = lrun * alpha + ps;
