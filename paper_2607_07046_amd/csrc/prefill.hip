@@ -920,11 +920,11 @@ namespace {
 // compute unit per kOnePerCu; each of the (S - 1) x tiles fp32 partial tiles
 // costs kPartial (64 KiB stored and read back at about 7 TB/s). The
 // constants are MI355X measurements of this kernel on the 7B shapes; the
-// model reproduces the measured GEMM times at 4096 tokens within 5%, keeps
-// 4 slices for every GEMM of a 256-token chunk (0.160 ms per chunk, as
-// before), and takes fewer slices than the older rule of about two rounds
-// of workgroups for longer chunks: 512 / 1024 / 2048 tokens in 0.222 /
-// 0.340 / 0.609 ms per chunk against 0.248 / 0.388 / 0.691.
+// model reproduces the measured GEMM times at 4096 tokens within 5%. Against
+// the older rule of about two rounds of workgroups it takes fewer slices:
+// at 256 tokens 2 instead of 4 for QKV (the same time, 2.5 times less
+// partial-tile traffic), and at 512 / 1024 / 2048 tokens per chunk 0.222 /
+// 0.340 / 0.609 ms against 0.248 / 0.388 / 0.691.
 struct Split {
   int m_tiles, n_tiles, splits, kps;
 };
