@@ -829,10 +829,15 @@ __global__ void __launch_bounds__(AW * kWave) attn_prefill_kernel(const uint16_t
     ps += __shfl_xor(ps, 32, kWave);
     lrun = lrun * alpha + ps;
     mrun = mnew;
+    // o is rescaled only if some query's running maximum moved (an alpha of
+    // exactly 1 changes nothing), and not on the wave's first block (o is
+    // still zero)
+    if (kb != kb0 + wave && __builtin_amdgcn_ballot_w64(alpha != 1.f) != 0) {
 #pragma unroll
-    for (int mt = 0; mt < D / 32; ++mt)
+      for (int mt = 0; mt < D / 32; ++mt)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) o[mt][i] *= alpha;
+        for (int i = 0; i < 16; ++i) o[mt][i] *= alpha;
+    }
     // P^T operand for key step s2: keys 16 s2 + 8 (l/32) + e = accumulators 8 s2 + e
     u32x4 pf[2];
 #pragma unroll
