@@ -80,3 +80,27 @@ def test_prefill_chunk_window(window):
     ref = ffn_at_h16(w, d.rms_eps, ref)
     for k in ("p_attn", "h", "p_ffn", "y"):   # every row of the chunk
         assert_close(got[k], ref[k], f"window {window} {k}")
+
+
+@pytest.mark.parametrize("window,T", [(33, 77), (200, 161)])
+def test_prefill_window_ragged_gqa(window, T):
+    """A ragged chunk (77 / 161 tokens: a partial last query block) of a GQA
+    layer with head size 128, hidden 1032 and a window that ends inside a key
+    block, at positions 150.. ."""
+    wl = Workload(key=f"swa_ragged{window}", seed_id=962, title="ragged sliding-window GQA layer",
+                  dims=LayerDims(hidden=1032, n_heads=12, n_kv_heads=4, head_dim=128, ffn=900,
+                                 window=window),
+                  fracs=(0.5, 0.5), device=0, weight_sigma=0.03, ctx=150)
+    d = wl.dims
+    li = LayerInputs(wl)
+    gs = GpuShard(wl, li=li, capacity=wl.ctx + T, max_tokens=T)
+    X = np.stack([li.x(t) for t in range(T)])
+    got = gs.prefill(X, wl.ctx)
+    r = oracle_ranges(wl)
+    kc, vc = gs.context()
+    w = oracle_shard_weights(li, r)
+    ref = oracle.prefill(w, r.n_q_heads, r.n_kv_heads, d.head_dim, d.rms_eps, d.rope_base, X, kc,
+                         vc, wl.ctx, window=window)
+    ref = ffn_at_h16(w, d.rms_eps, ref)
+    for k in ("p_attn", "h", "p_ffn", "y"):
+        assert_close(got[k], ref[k], f"window {window} T {T} {k}")
