@@ -83,10 +83,11 @@ __device__ __forceinline__ u32x4 zero_past(u32x4 w, int v) {
 // tokens, N the shard's output features, K the input features. A is
 // k-step-major (see kmajor) with zeros past K; B is row-major. The weights
 // (B) are the large operand and are streamed once; A is small and re-read
-// from L2 by every N tile. The K range is cut into ``splits`` slices so that
-// one launch has about one workgroup per compute unit; the slices of a tile
-// meet through a counter, and the last to arrive adds them in slice order
-// (a fixed summation order) and runs the epilogue.
+// from L2 by every N tile. The K range is cut into ``splits`` slices (the
+// count comes from the host's cost model, choose_split) so that short
+// chunks still fill the compute units; the slices of a tile meet through a
+// counter, and the last to arrive adds them in slice order (a fixed
+// summation order) and runs the epilogue.
 //
 // Tile 128 tokens x 128 features x 64 k per 256-thread workgroup, two
 // workgroups per compute unit (one's barrier and LDS waits are covered by the
@@ -925,11 +926,11 @@ namespace {
 // compute unit per kOnePerCu; each of the (S - 1) x tiles fp32 partial tiles
 // costs kPartial (64 KiB stored and read back at about 7 TB/s). The
 // constants are MI355X measurements of this kernel on the 7B shapes; the
-// model reproduces the measured GEMM times at 4096 tokens within 5%. Against
-// the older rule of about two rounds of workgroups it takes fewer slices:
-// at 256 tokens 2 instead of 4 for QKV (the same time, 2.5 times less
-// partial-tile traffic), and at 512 / 1024 / 2048 tokens per chunk 0.222 /
-// 0.340 / 0.609 ms against 0.248 / 0.388 / 0.691.
+// model reproduces the measured GEMM times at 4096 tokens within 5%. It
+// takes fewer slices than a rule of about two rounds of workgroups: at 256
+// tokens 2 instead of 4 for QKV (the same time, 2.5 times less partial-tile
+// traffic), and at 512 / 1024 / 2048 tokens per chunk 0.222 / 0.340 /
+// 0.609 ms against 0.248 / 0.388 / 0.691 for that rule.
 struct Split {
   int m_tiles, n_tiles, splits, kps;
 };
