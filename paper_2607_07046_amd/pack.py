@@ -119,10 +119,16 @@ def clone_qshard(q: QShardWeightsDev) -> QShardWeightsDev:
 
 def upload_full(src, dims: vt.vt_layer_dims, device="cuda") -> ShardWeightsDev:
     """The whole layer's weights on the device (canonical out x in, each
-    matrix contiguous): the source vt_shard_pack gathers shards from."""
+    matrix contiguous; the rows of Wd padded with zeros to a multiple of 8
+    columns, the row alignment the library requires): the source
+    vt_shard_pack gathers shards from."""
     t = {"g_attn": _dev(src.g_attn(), device), "g_ffn": _dev(src.g_ffn(), device)}
     for name in ("wq", "wk", "wv", "wo", "wg", "wu", "wd"):
         t[name] = _dev(src.full(name), device)
+    wd = t["wd"]
+    if wd.shape[1] % 8:
+        t["wd"] = torch.zeros((wd.shape[0], round_up(wd.shape[1], 8)), dtype=wd.dtype, device=wd.device)
+        t["wd"][:, :wd.shape[1]] = wd
     p = lambda x: x.data_ptr() if x.numel() else None
     st = vt.vt_layer_weights(g_attn=p(t["g_attn"]), wq=p(t["wq"]), ld_q=t["wq"].shape[1],
                              wk=p(t["wk"]), ld_k=t["wk"].shape[1], wv=p(t["wv"]),

@@ -247,3 +247,15 @@ def test_emit_rejects_staged_and_planless_messages():
     with pytest.raises(vt.VoltronError) as e:
         emit_case(wl, plans, staged=True)
     assert e.value.status == vt.VT_ERR_UNSUPPORTED
+
+
+def test_emit_rejects_hidden_not_a_multiple_of_32():
+    """The message's 32-value blocks map whole onto the O and down rows of a
+    workgroup only when the hidden size is a multiple of 32; otherwise the
+    call is refused before anything runs."""
+    wl = tiny_workload(404, 1032, 4, 2, 128, 900, (0.5, 0.5), 0, 16, sigma=0.03)
+    nb = (1032 + 31) // 32
+    plans = plans_for(nb, np.random.default_rng(5), "fp16")
+    with pytest.raises(vt.VoltronError) as e:
+        emit_case(wl, plans)
+    assert e.value.status == vt.VT_ERR_UNSUPPORTED

@@ -41,6 +41,8 @@ CASES = {
     "ragged_3_gqa": lambda: (tiny_workload(421, 512, 8, 4, 64, 1000, (0.33, 0.34, 0.33), 0, 16),
                              (0.33, 0.34, 0.33)),
     "7b_3": lambda: (get("7b"), (0.5, 0.3, 0.2)),
+    "ragged_h1032_gqa3": lambda: (tiny_workload(422, 1032, 12, 4, 128, 900, (0.5, 0.5), 1, 16),
+                                  (0.5, 0.5)),
 }
 
 
