@@ -22,6 +22,7 @@ from synth.gen import LayerInputs
 from tests.common import assert_close, ffn_at_h16, oracle_qshard_weights, oracle_ranges, tiny_workload
 from tests.gpu_common import GpuShard
 from tests.test_gpu_decode import RAGGED_H, RAGGED_IDS
+from tests.test_gpu_random_shapes import IDS as RANDOM_IDS, SHAPES as RANDOM_SHAPES
 
 pytestmark = pytest.mark.gpu
 
@@ -93,7 +94,7 @@ def case(wl, level):
         d = wl.dims
         x = li.x(0)
         ref = oracle.decode(w, r.n_q_heads, r.n_kv_heads, d.head_dim, d.rms_eps, d.rope_base, x,
-                            kc, vc, wl.ctx)
+                            kc, vc, wl.ctx, window=d.window)
         ref = ffn_at_h16(w, d.rms_eps, ref)
         _cache[key] = (li, x, ref)
     return _cache[key]
@@ -138,6 +139,12 @@ def test_decode_q_ragged_hidden(case, level):
     # hidden a multiple of 8 but not of 32: the last 32-column block of every
     # K = hidden row is partial
     run(tiny_workload(*case, sigma=0.03), level)
+
+
+@pytest.mark.parametrize("level", LEVELS)
+@pytest.mark.parametrize("wl", RANDOM_SHAPES[:4], ids=RANDOM_IDS[:4])
+def test_decode_q_random_shapes(wl, level):
+    run(wl, level)
 
 
 @pytest.mark.parametrize("level", LEVELS)
