@@ -23,6 +23,7 @@ from synth.gen import LayerInputs
 from tests.common import assert_close, ffn_at_h16, oracle_ranges, oracle_shard_weights, \
     tiny_workload
 from tests.gpu_common import lib_dims
+from tests.test_gpu_random_shapes import IDS as RANDOM_IDS, SHAPES as RANDOM_SHAPES
 
 pytestmark = pytest.mark.gpu
 KEYS = ("p_attn", "h", "p_ffn", "y")
@@ -149,6 +150,14 @@ def test_ragged_hidden_stack_equals_layer_chain():
     # hidden a multiple of 8 but not of 16 (the last weight piece of every
     # K = hidden row and the next layer's x staging are ragged)
     wl = tiny_workload(504, 1032, 4, 2, 128, 900, (0.5, 0.5), 1, 20, sigma=0.03)
+    st = Stack(wl, 3, wl.ctx + 3)
+    outs = check_equal(st, 3)
+    check_first_layer(st, outs, 3)
+
+
+@pytest.mark.parametrize("wl", [w for w in RANDOM_SHAPES if w.dims.window == 0][:2],
+                         ids=[i for w, i in zip(RANDOM_SHAPES, RANDOM_IDS) if w.dims.window == 0][:2])
+def test_random_shape_stack_equals_layer_chain(wl):
     st = Stack(wl, 3, wl.ctx + 3)
     outs = check_equal(st, 3)
     check_first_layer(st, outs, 3)
