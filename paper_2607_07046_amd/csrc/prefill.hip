@@ -118,6 +118,7 @@ constexpr int GEMM_LDS_BYTES = (GBM * TLD + GBM) * 4 > 2 * STAGE * 2 ? (GBM * TL
 static_assert(2 * GEMM_LDS_BYTES <= 160 * 1024, "two workgroups per compute unit");
 constexpr int GEMM_SLOTS = 512;            // two workgroups per compute unit
 constexpr int MAX_SPLITS = 4;
+constexpr int RASTER_M = 8;                // M tiles per block of an XCD's tile walk
 constexpr unsigned kWaitLimit = 1u << 22;  // polls of the split-K wait: far beyond any slice's stores
 
 
@@ -161,13 +162,22 @@ struct GemmArgs {
 
 __global__ void __launch_bounds__(GT, 2) gemm_kernel(GemmArgs g) {
   extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
-  // Workgroups with equal index mod 8 run on one XCD: the M tiles of one
-  // (N tile, split) pair get indices that differ by multiples of 8, so their
-  // B slice is fetched once into that XCD's L2.
+  // Workgroups with equal index mod 8 run on one XCD. An XCD takes every
+  // eighth (N tile, split) unit and walks its tiles in blocks of up to
+  // RASTER_M M tiles x all its units, M tile fastest: the M tiles of one
+  // unit run together (its B slice comes into that XCD's L2 once), and with
+  // many M tiles the workgroups resident at once still share each
+  // activation k-slab across all the XCD's units instead of re-reading the
+  // whole of A for every few units (4096-token chunk: 1.31 -> 1.21 ms).
   const int id = blockIdx.x;
-  const int slot = id / 8;
-  const int unit = (slot / g.m_tiles) * 8 + id % 8;
-  const int m_tile = slot % g.m_tiles;
+  const int groups = (g.n_tiles * g.splits + 7) / 8;  // units per XCD (at most)
+  const int j = id / 8;
+  const int bm = min(g.m_tiles, RASTER_M);
+  const int blk = j / (bm * groups);
+  const int rows = min(bm, g.m_tiles - blk * bm);  // M tiles in this block
+  const int r = j - blk * bm * groups;
+  const int unit = (r / rows) * 8 + id % 8;
+  const int m_tile = blk * bm + r % rows;
   if (unit >= g.n_tiles * g.splits) return;
   const int n_tile = unit % g.n_tiles, split = unit / g.n_tiles;
   const int m0 = m_tile * GBM, n0 = n_tile * GBN;
@@ -925,8 +935,9 @@ namespace {
 // one k-tile per kTwoPerCu microseconds, a last round of at most one per
 // compute unit per kOnePerCu; each of the (S - 1) x tiles fp32 partial tiles
 // costs kPartial (64 KiB stored and read back at about 7 TB/s). The
-// constants are MI355X measurements of this kernel on the 7B shapes; the
-// model reproduces the measured GEMM times at 4096 tokens within 5%. It
+// constants are MI355X measurements of this kernel on the 7B shapes (the
+// per-k-tile rates from the 4096-token chunk's GEMMs, which the model then
+// reproduced within 5%, the partial-tile cost from the chip's copy rate). It
 // takes fewer slices than a rule of about two rounds of workgroups: at 256
 // tokens 2 instead of 4 for QKV (the same time, 2.5 times less partial-tile
 // traffic), and at 512 / 1024 / 2048 tokens per chunk 0.222 / 0.340 /
