@@ -28,24 +28,25 @@ pytestmark = pytest.mark.gpu
 KEYS = ("p_attn", "h", "p_ffn", "y")
 
 
-def _draw(n=12, seed=20261204):
+def _draw(n=12, seed=20261204, small=False):
     rng = np.random.default_rng(seed)
     out = []
     while len(out) < n:
-        nkv = int(rng.integers(1, 9))
-        G = int(rng.integers(1, 9))
+        nkv = int(rng.integers(1, 9)) if not small else int(rng.integers(1, 3))
+        G = int(rng.integers(1, 9)) if not small else int(rng.integers(1, 4))
         d = int(rng.choice([64, 128]))
-        H = 8 * int(rng.integers(16, 401))
-        F = int(rng.integers(64, 4001))
+        H = 8 * int(rng.integers(16, 401)) if not small else 8 * int(rng.integers(2, 65))
+        F = int(rng.integers(64, 4001)) if not small else int(rng.integers(1, 200))
         ndev = int(rng.integers(1, 5))
         fr = rng.dirichlet(np.ones(ndev))
         fr = tuple(float(round(f, 3)) for f in fr)
         fr = fr[:-1] + (round(1.0 - sum(fr[:-1]), 3),)
         dev = int(rng.integers(0, ndev))
-        ctx = int(rng.integers(0, 701))
-        T = int(rng.integers(1, 301))
+        ctx = int(rng.integers(0, 701)) if not small else int(rng.integers(0, 40))
+        T = int(rng.integers(1, 301)) if not small else int(rng.integers(1, 41))
         window = int(rng.choice([0, 0, 0, int(rng.integers(1, 400))]))
-        wl = Workload(key=f"rand{len(out)}", seed_id=700 + len(out), title="random test layer",
+        wl = Workload(key=f"rand{'s' if small else ''}{len(out)}", seed_id=(760 if small else 700) + len(out),
+                      title="random test layer",
                       dims=LayerDims(hidden=H, n_heads=nkv * G, n_kv_heads=nkv, head_dim=d, ffn=F,
                                      window=window),
                       fracs=fr, device=dev, weight_sigma=float(1.0 / np.sqrt(H)), ctx=ctx, chunk=T)
@@ -59,7 +60,9 @@ def _draw(n=12, seed=20261204):
     return out
 
 
-SHAPES = _draw()
+# the main draw, then small layers (hidden 16-512, 1-2 KV heads, FFN shares
+# down to a single column, contexts and chunks under 40 positions)
+SHAPES = _draw() + _draw(n=8, seed=20261206, small=True)
 IDS = [f"{w.key}-H{w.dims.hidden}-kv{w.dims.n_kv_heads}x{w.dims.n_heads // w.dims.n_kv_heads}-"
        f"d{w.dims.head_dim}-F{w.dims.ffn}-n{len(w.fracs)}-c{w.ctx}-T{w.chunk}-w{w.dims.window}"
        for w in SHAPES]
