@@ -74,23 +74,32 @@ def test_random_shape_decode_and_prefill(wl):
     li = LayerInputs(wl)
     r = oracle_ranges(wl)
     w = oracle_shard_weights(li, r)
-    # decode at position ctx
-    gs = GpuShard(wl, li=li)
+    # decode at position ctx, with the other devices' partials; the staged
+    # and the cooperative launches give the same bits as the fused one
     x = li.x(0)
-    got = gs.decode(x, wl.ctx, vt.VT_ATTN | vt.VT_FFN)
+    pa, pf = li.peer("attn"), li.peer("ffn")
+    runs = []
+    for flags in (0, vt.VT_STAGED, vt.VT_COOPERATIVE):
+        gs = GpuShard(wl, li=li)
+        runs.append(gs.decode(x, wl.ctx, vt.VT_ATTN | vt.VT_FFN | flags, peer_attn=pa, peer_ffn=pf))
+        assert not gs.sync_words().any()
+    got = runs[0]
+    for other in runs[1:]:
+        for k in KEYS:
+            assert np.array_equal(other[k], got[k]), k
     kc, vc = gs.context()
-    ref = oracle_decode(wl, li, r, x, kc, vc, wl.ctx, w=w)
+    ref = oracle_decode(wl, li, r, x, kc, vc, wl.ctx, peer_attn=pa, peer_ffn=pf, w=w)
     for k in KEYS:
         assert_close(got[k], ref[k], f"decode {k}")
-    assert not gs.sync_words().any()
     # a prefill chunk of T tokens at positions ctx.. on a fresh cache
     T = wl.chunk
     gp = GpuShard(wl, li=li, capacity=wl.ctx + T, max_tokens=T)
     X = li.x_chunk(T)
-    got = gp.prefill(X, wl.ctx)
+    qa, qf = li.peer("attn", rows=T), li.peer("ffn", rows=T)
+    got = gp.prefill(X, wl.ctx, peer_attn=qa, peer_ffn=qf)
     refp = oracle.prefill(w, r.n_q_heads, r.n_kv_heads, d.head_dim, d.rms_eps, d.rope_base, X, kc,
-                          vc, wl.ctx, window=d.window)
-    refp = ffn_at_h16(w, d.rms_eps, refp)
+                          vc, wl.ctx, qa, qf, window=d.window)
+    refp = ffn_at_h16(w, d.rms_eps, refp, qf)
     for k in KEYS:
         assert_close(got[k], refp[k], f"prefill {k}")
     kc1, vc1 = gp.cache()
