@@ -53,3 +53,21 @@ def test_noalloc_matches_workspace_decode_on_consecutive_calls():
             assert np.array_equal(ga[k], gb[k]), (key, k)
         assert np.array_equal(ca[0], cb[0]) and np.array_equal(ca[1], cb[1]), key
         assert la == lb == get(key).ctx + 1, key
+
+
+def test_noalloc_on_random_shapes():
+    """Seeded random layer shapes (hidden sizes that are multiples of 8 only,
+    GQA groups up to 8, sliding windows) in a row through the scratch array:
+    each equals the decode with a caller workspace bit for bit."""
+    from tests.test_gpu_random_shapes import SHAPES
+    for wl in SHAPES[:6] + SHAPES[12:15]:
+        li = LayerInputs(wl)
+        x = li.x(5)
+        a = GpuShard(wl, li=li)
+        b = GpuShard(wl, li=li)
+        ga = a.decode(x, wl.ctx, BOTH)
+        gb = decode_noalloc(b, x)
+        for k in ("p_attn", "h", "p_ffn", "y"):
+            assert np.array_equal(ga[k], gb[k]), (wl.key, k)
+        ca, cb = a.cache(), b.cache()
+        assert np.array_equal(ca[0], cb[0]) and np.array_equal(ca[1], cb[1]), wl.key
