@@ -536,8 +536,9 @@ def main():
 
 
 def repack_section(spec, dims, info, wl, reps, enqueue, copies):
-    """Elastic re-partition: vt_shard_pack of the headline shard out of the
-    whole layer's device weights (its bytes read and written), alone and
+    """Elastic re-partition: vt_shard_pack of the decode_7b section's shard
+    (7B-shaped layer, 30% shard) out of the whole layer's device weights (its
+    bytes read and written), alone and
     while decode steps run on the default stream; the decode step time with
     and without a pack running beside it on a second stream (both at the
     default priority)."""
@@ -696,8 +697,9 @@ def quant_section(spec, dims, info, wl, steps, warmup, fp16_weights, eager=False
                      "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4), "weight_copies": copies,
                      "steps": n}
         del layers, q0
-    res["note"] = ("same shard and position as the headline; bytes = codes + fp16 block scales "
-                   "+ K/V + vectors; the format is the library's own 32-column block format")
+    res["note"] = ("same shard and position as the decode_7b section (7B-shaped layer, 30% shard, "
+                   "pos 1024); bytes = codes + fp16 block scales + K/V + vectors; the format is the "
+                   "library's own 32-column block format")
     return res
 
 
