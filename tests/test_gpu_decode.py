@@ -245,6 +245,23 @@ def test_gqa_groups_not_powers_of_two(key, mode):
     check_kv(gs, ref, wl.ctx, k0, v0)
 
 
+@pytest.mark.parametrize("mode", MODES)
+@pytest.mark.parametrize("ctx", [16000, 32767])
+def test_long_contexts(ctx, mode):
+    """Decode at 16000 and 32767 cached positions on a GQA shard (8 query
+    heads over 2 KV heads, head size 128): many attention chunks, the merge
+    of their partial records in several batches."""
+    wl = tiny_workload(620 if ctx == 16000 else 621, 1024, 16, 4, 128, 2000, (0.5, 0.5), 0, ctx,
+                       sigma=0.03)
+    li, r, x, ref = oracle_case(wl)
+    gs = GpuShard(wl, li=li)
+    k0, v0 = gs.cache()
+    got = gs.decode(x, wl.ctx, BOTH | MODES[mode])
+    check_outputs(got, ref)
+    check_kv(gs, ref, wl.ctx, k0, v0)
+    assert not np.any(gs.sync_words()), "synchronisation words not cleared"
+
+
 def test_empty_shard_outputs_zero_partials():
     """A device that gets no heads and no columns (e.g. one whose share was
     pruned away) contributes zero partials; h and y pass x and peers through."""
