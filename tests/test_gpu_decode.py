@@ -31,7 +31,7 @@ _cache = {}
 
 def oracle_case(wl, device=None, li=None):
     """Oracle inputs/outputs of the workload's shard at its decode position."""
-    key = (wl.key, wl.seed_id, device)
+    key = (repr(wl), device)  # the whole workload: shapes, partition, context
     if key not in _cache:
         li = li or LayerInputs(wl)
         r = oracle_ranges(wl, device)

@@ -85,7 +85,7 @@ _cache = {}
 
 
 def case(wl, level):
-    key = (wl.key, wl.seed_id, level)
+    key = (repr(wl), level)  # the whole workload: shapes, partition, context
     if key not in _cache:
         li = LayerInputs(wl)
         r = oracle_ranges(wl)
