@@ -140,6 +140,7 @@ CASES = [
     (304, 768, 12, 12, 64, 2000, (0.3, 0.7), 1, 100, 129),  # M > one 128-row tile, 5 query blocks
     (310, 1536, 12, 4, 128, 1000, (0.5, 0.5), 1, 90, 77),   # GQA group 3
     (311, 1792, 28, 4, 64, 1200, (0.5, 0.5), 0, 45, 140),   # GQA group 7
+    (312, 1024, 16, 4, 128, 1000, (0.5, 0.5), 1, 30000, 64),  # a 64-token chunk after 30000 positions
 ]
 
 
