@@ -205,6 +205,92 @@ def test_stack_decode_validation_errors(lib):
     assert kv.len == 128
 
 
+def _full_kv(A=1 << 20):
+    return vt.vt_kv_view(k=A, v=A, capacity=128, n_kv_heads=4, head_dim=64, len=128)
+
+
+def test_prefill_validation_errors(lib):
+    # every case fails on the host, before anything is enqueued
+    spec = _tiny_spec()
+    ws_need = vt.vt_workspace_size(spec, 16, 200)
+    A = 1 << 20
+    kv = vt.vt_kv_view(k=A, v=A, capacity=200, n_kv_heads=4, head_dim=64, len=128)
+
+    def call(w=None, kv_=kv, io=None, n_tok=16, pos0=128, phases=vt.VT_ATTN | vt.VT_FFN, ws=A,
+             wsb=ws_need):
+        with pytest.raises(vt.VoltronError) as e:
+            vt.vt_layer_prefill_chunk(spec, w or _fake_weights(), kv_, io or _fake_io(), n_tok, pos0,
+                                      phases, ws, wsb)
+        return e.value.status
+
+    assert call(n_tok=0) == vt.VT_ERR_ARG
+    assert call(n_tok=65537) == vt.VT_ERR_ARG
+    assert call(phases=0) == vt.VT_ERR_ARG
+    assert call(phases=vt.VT_ATTN | vt.VT_STAGED) == vt.VT_ERR_ARG  # one launch per kernel already
+    assert call(pos0=127) == vt.VT_ERR_POS
+    assert call(n_tok=73) == vt.VT_ERR_KV_FULL  # 128 + 73 > 200
+    assert call(wsb=256) == vt.VT_ERR_WORKSPACE
+    assert call(ws=None) == vt.VT_ERR_WORKSPACE
+    assert call(n_tok=17) == vt.VT_ERR_WORKSPACE  # sized for 16 tokens
+    assert call(ws=A + 8, wsb=ws_need + 64) == vt.VT_ERR_ALIGN
+    w = _fake_weights()
+    w.wq = A + 8
+    assert call(w=w) == vt.VT_ERR_ALIGN
+    w = _fake_weights()
+    w.ld_d = 690
+    assert call(w=w) == vt.VT_ERR_ALIGN
+    w = _fake_weights()
+    w.wd = None
+    assert call(w=w) == vt.VT_ERR_ARG
+    assert call(w=w, phases=vt.VT_ATTN, kv_=_full_kv()) == vt.VT_ERR_KV_FULL  # the FFN weights unused
+    io = _fake_io()
+    io.x = None
+    assert call(io=io) == vt.VT_ERR_ARG
+    io = _fake_io()
+    io.attn_partial = A + 2
+    assert call(io=io) == vt.VT_ERR_ALIGN
+    io = _fake_io()
+    io.h = None
+    assert call(io=io) == vt.VT_ERR_ARG
+    io = _fake_io()
+    io.ffn_partial = None
+    assert call(io=io) == vt.VT_ERR_ARG
+    io = _fake_io()
+    io.y = A + 4
+    assert call(io=io) == vt.VT_ERR_ALIGN
+    bad_kv = vt.vt_kv_view(k=A, v=A, capacity=200, n_kv_heads=3, head_dim=64, len=128)
+    assert call(kv_=bad_kv) == vt.VT_ERR_ARG
+    assert kv.len == 128
+
+
+def test_emit_validation_errors(lib):
+    spec = _tiny_spec()
+    ws_need = vt.vt_workspace_size(spec, 1, 129)
+    A = 1 << 20
+    kv = vt.vt_kv_view(k=A, v=A, capacity=200, n_kv_heads=4, head_dim=64, len=128)
+
+    def call(em, spec_=spec, phases=vt.VT_ATTN | vt.VT_FFN):
+        with pytest.raises(vt.VoltronError) as e:
+            vt.vt_layer_decode_emit(spec_, _fake_weights(), kv, _fake_io(), 128, phases, em, A,
+                                    ws_need)
+        return e.value.status
+
+    plan = dict(prec_attn=A, off_attn=A, msg_attn=A, msg_attn_bytes=256, prec_ffn=A, off_ffn=A,
+                msg_ffn=A, msg_ffn_bytes=256)
+    assert call(vt.vt_emit(**plan), phases=vt.VT_ATTN | vt.VT_FFN | vt.VT_STAGED) == \
+        vt.VT_ERR_UNSUPPORTED
+    assert call(vt.vt_emit(**{**plan, "prec_attn": None})) == vt.VT_ERR_ARG
+    assert call(vt.vt_emit(**{**plan, "off_ffn": None})) == vt.VT_ERR_ARG
+    assert call(vt.vt_emit(**{**plan, "off_attn": A + 2})) == vt.VT_ERR_ALIGN
+    assert call(vt.vt_emit(**plan), phases=vt.VT_ATTN) == vt.VT_ERR_ARG  # FFN message, no FFN
+    assert call(vt.vt_emit(**{**plan, "msg_attn_bytes": 1 << 31})) == vt.VT_ERR_UNSUPPORTED
+    dims = vt.vt_layer_dims(hidden=528, n_heads=8, n_kv_heads=8, head_dim=64, ffn=1376,
+                            rms_eps=1e-5, rope_base=1e4)
+    odd = vt.vt_shard_spec_create(dims, (0.5, 0.5), (0.5, 0.5), 0)
+    assert call(vt.vt_emit(**plan), spec_=odd) == vt.VT_ERR_UNSUPPORTED  # 528 % 32 != 0
+    assert kv.len == 128
+
+
 def test_noalloc_decode_rejects_oversized_workspace(lib):
     """The allocation-free decode holds VT_NOALLOC_SCRATCH_BYTES of scratch:
     a context whose attention records need more is refused before anything
