@@ -90,11 +90,15 @@ class GpuShard:
             vt.vt_layer_decode(self.spec, self.w.struct, self.kv, io, pos, phases, ptr(self.ws),
                                self.ws_bytes, None)
         torch.cuda.synchronize()
+        if on_device:
+            return out
         return {k: v.float().cpu().numpy().astype(np.float64) for k, v in out.items()}
 
     def prefill(self, X, pos0=None, phases=vt.VT_ATTN | vt.VT_FFN, peer_attn=None,
-                peer_ffn=None, h_in=None):
-        """vt_layer_prefill_chunk of the [T][H] fp16 rows X at positions pos0.. ."""
+                peer_ffn=None, h_in=None, on_device=False):
+        """vt_layer_prefill_chunk of the [T][H] fp16 rows X at positions pos0.. .
+        The outputs as float64 host arrays, or (on_device) as the fp16 device
+        tensors the call wrote."""
         H = self.dims.hidden
         T = X.shape[0] if X is not None else h_in.shape[0]
         pos0 = self.kv.len if pos0 is None else pos0
@@ -111,6 +115,8 @@ class GpuShard:
         vt.vt_layer_prefill_chunk(self.spec, self.w.struct, self.kv, io, T, pos0, phases,
                                   ptr(self.ws), self.ws_bytes, None)
         torch.cuda.synchronize()
+        if on_device:
+            return out
         return {k: v.float().cpu().numpy().astype(np.float64) for k, v in out.items()}
 
     def sync_words(self):

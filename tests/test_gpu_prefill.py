@@ -18,8 +18,8 @@ import oracle
 from paper_2607_07046_amd import voltron as vt
 from synth import get
 from synth.gen import LayerInputs
-from tests.common import (assert_close, ffn_at_h16, max_rel_err, norm_rel_err, oracle_ranges,
-                          oracle_shard_weights, tiny_workload)
+from tests.common import (FLOOR, NORM_TOL, REL_TOL, assert_close, ffn_at_h16, max_rel_err,
+                          norm_rel_err, oracle_ranges, oracle_shard_weights, tiny_workload)
 from tests.gpu_common import GpuShard
 
 pytestmark = pytest.mark.gpu
@@ -130,6 +130,77 @@ def test_prefill_long_chunks(T):
             ref[k].append(o[k])
     for k in ref:
         assert_close(got[k][rows], np.stack(ref[k]), f"{k} on {len(rows)} sampled rows")
+
+
+def _close_dev(got, ref, what):
+    """The parity bar (element-wise with the row-RMS floor, and normwise) of
+    two fp16 [rows, H] device tensors, evaluated on the device."""
+    g, r = got.double(), ref.double()
+    assert bool(torch.isfinite(g).all()), what
+    floor = FLOOR * torch.sqrt((r * r).mean(dim=1, keepdim=True))
+    e = float(((g - r).abs() / torch.maximum(r.abs(), floor)).max())
+    n = float(torch.linalg.norm(g - r) / torch.linalg.norm(r))
+    print(f"{what}: element-wise {e:.3g}, normwise {n:.3g}")
+    assert e <= REL_TOL and n <= NORM_TOL, f"{what}: element-wise {e:.3g}, normwise {n:.3g}"
+
+
+def test_prefill_max_chunk():
+    """The largest chunk the entry point takes: 65536 tokens at positions
+    768.. of the 7B 50% shard in one call (GEMM grids of 512 row tiles, 2048
+    query blocks per head, keys up to 66303). The first 1024 tokens' keys,
+    values and sampled output rows against the oracle (those rows attend to
+    the context and the first 1024 tokens only); every output row and every
+    appended key and value against the same tokens prefilled as sixteen
+    4096-token chunks, at the same bar; the context's cache bytes unchanged."""
+    T, C, R = 65536, 4096, 1024
+    wl = get("7b_prefill")
+    li = LayerInputs(wl)
+    d = wl.dims
+    X = li.x_chunk(T)
+    one = GpuShard(wl, li=li, capacity=wl.ctx + T, max_tokens=T)
+    k0, v0 = one.cache()
+    big = one.prefill(X, wl.ctx, BOTH, on_device=True)
+    assert not one.sync_words().any()
+    assert one.kv.len == wl.ctx + T
+    split = GpuShard(wl, li=li, capacity=wl.ctx + T, max_tokens=C)
+    parts = [split.prefill(X[i:i + C], wl.ctx + i, BOTH, on_device=True) for i in range(0, T, C)]
+    assert not split.sync_words().any()
+    for k in ("p_attn", "h", "p_ffn", "y"):
+        _close_dev(big[k], torch.cat([pt[k] for pt in parts]), f"{k}, one chunk vs 16")
+    del parts
+    new = slice(wl.ctx, wl.ctx + T)
+    for a, b, name in ((one.kc, split.kc, "keys"), (one.vc, split.vc, "values")):
+        _close_dev(a[:, new].reshape(-1, a.shape[-1] * 16), b[:, new].reshape(-1, a.shape[-1] * 16),
+                   f"appended {name}, one chunk vs 16")
+    kc1, vc1 = one.cache()
+    assert np.array_equal(kc1[:, :wl.ctx], k0[:, :wl.ctx])
+    assert np.array_equal(vc1[:, :wl.ctx], v0[:, :wl.ctx])
+
+    # the oracle on the first R tokens
+    r = oracle_ranges(wl)
+    w = oracle_shard_weights(li, r)
+    w = oracle.ShardWeights(**{f.name: np.asarray(getattr(w, f.name), np.float64)
+                               for f in dataclasses.fields(w)})
+    kc, vc = li.kv_context_heads(r.kv_head_begin, r.kv_head_begin + r.n_kv_heads)
+    _, _, K, V = oracle.attn_sublayer(w, r.n_q_heads, r.n_kv_heads, d.head_dim, d.rms_eps,
+                                      d.rope_base, X[:R], kc, vc, wl.ctx, window=1)
+    first = slice(wl.ctx, wl.ctx + R)
+    kn = kc1[:, first].view(np.float16).astype(np.float64)
+    vn = vc1[:, first].view(np.float16).astype(np.float64)
+    assert_close(np.transpose(kn, (1, 0, 2)).reshape(R, -1), K.reshape(R, -1), "appended keys")
+    assert_close(np.transpose(vn, (1, 0, 2)).reshape(R, -1), V.reshape(R, -1), "appended values")
+    rows = _sample_rows(R, 7100, n_random=8)
+    got = {k: big[k][rows].float().cpu().numpy().astype(np.float64) for k in big}
+    ref = {k: [] for k in ("p_attn", "h", "p_ffn", "y")}
+    for t in rows:
+        kt, vt_ = oracle.append_kv(kc, vc, K[:t], V[:t], wl.ctx)
+        o = oracle.decode(w, r.n_q_heads, r.n_kv_heads, d.head_dim, d.rms_eps, d.rope_base, X[t],
+                          kt, vt_, wl.ctx + t, None, None)
+        o = ffn_at_h16(w, d.rms_eps, o)
+        for k in ref:
+            ref[k].append(o[k])
+    for k in ref:
+        assert_close(got[k], np.stack(ref[k]), f"{k} on {len(rows)} sampled rows")
 
 
 CASES = [
