@@ -90,8 +90,6 @@ class GpuShard:
             vt.vt_layer_decode(self.spec, self.w.struct, self.kv, io, pos, phases, ptr(self.ws),
                                self.ws_bytes, None)
         torch.cuda.synchronize()
-        if on_device:
-            return out
         return {k: v.float().cpu().numpy().astype(np.float64) for k, v in out.items()}
 
     def prefill(self, X, pos0=None, phases=vt.VT_ATTN | vt.VT_FFN, peer_attn=None,

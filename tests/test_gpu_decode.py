@@ -262,6 +262,23 @@ def test_long_contexts(ctx, mode):
     assert not np.any(gs.sync_words()), "synchronisation words not cleared"
 
 
+@pytest.mark.parametrize("mode", MODES)
+def test_million_position_context(mode):
+    """Decode after 1,000,000 cached positions (8 query heads over one KV
+    head of 128; 256 MB each of cached keys and values): about 3900
+    attention chunks per query head, whose partial records the merge reads
+    in many batches."""
+    wl = tiny_workload(622, 1024, 16, 2, 128, 2000, (0.5, 0.5), 0, 1_000_000, sigma=0.03)
+    li, r, x, ref = oracle_case(wl)
+    assert r.n_q_heads == 8 and r.n_kv_heads == 1
+    gs = GpuShard(wl, li=li)
+    k0, v0 = gs.cache()
+    got = gs.decode(x, wl.ctx, BOTH | MODES[mode])
+    check_outputs(got, ref)
+    check_kv(gs, ref, wl.ctx, k0, v0)
+    assert not np.any(gs.sync_words()), "synchronisation words not cleared"
+
+
 def test_empty_shard_outputs_zero_partials():
     """A device that gets no heads and no columns (e.g. one whose share was
     pruned away) contributes zero partials; h and y pass x and peers through."""
