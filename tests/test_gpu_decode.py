@@ -279,6 +279,22 @@ def test_million_position_context(mode):
     assert not np.any(gs.sync_words()), "synchronisation words not cleared"
 
 
+@pytest.mark.parametrize("mode", MODES)
+def test_long_context_head_dim_64(mode):
+    """Decode after 100,000 cached positions with head size 64 (8 threads per
+    position, 64 positions per pass, chunks of up to 512 positions), device
+    1 of two: 8 query heads over 2 KV heads."""
+    wl = tiny_workload(623, 1024, 16, 4, 64, 2000, (0.5, 0.5), 1, 100_000, sigma=0.03)
+    li, r, x, ref = oracle_case(wl)
+    assert r.n_q_heads == 8 and r.n_kv_heads == 2
+    gs = GpuShard(wl, li=li)
+    k0, v0 = gs.cache()
+    got = gs.decode(x, wl.ctx, BOTH | MODES[mode])
+    check_outputs(got, ref)
+    check_kv(gs, ref, wl.ctx, k0, v0)
+    assert not np.any(gs.sync_words()), "synchronisation words not cleared"
+
+
 def test_empty_shard_outputs_zero_partials():
     """A device that gets no heads and no columns (e.g. one whose share was
     pruned away) contributes zero partials; h and y pass x and peers through."""
