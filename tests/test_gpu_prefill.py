@@ -212,6 +212,7 @@ CASES = [
     (310, 1536, 12, 4, 128, 1000, (0.5, 0.5), 1, 90, 77),   # GQA group 3
     (311, 1792, 28, 4, 64, 1200, (0.5, 0.5), 0, 45, 140),   # GQA group 7
     (312, 1024, 16, 4, 128, 1000, (0.5, 0.5), 1, 30000, 64),  # a 64-token chunk after 30000 positions
+    (313, 1024, 16, 4, 64, 1000, (0.5, 0.5), 0, 20000, 200),  # head size 64 after 20000 positions
 ]
 
 
