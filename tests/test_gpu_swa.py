@@ -53,6 +53,13 @@ def test_tiny_windows(window, mode):
     check(tiny_swa(window), BOTH | mode)
 
 
+@pytest.mark.parametrize("mode", [0, vt.VT_STAGED])
+def test_window_after_a_million_positions(mode):
+    """A window of 4096 at position 1,000,000: the attended range starts
+    far into the cache (the first 995,905 positions are never read)."""
+    check(tiny_swa(4096, ctx=1_000_000, seed=962), BOTH | mode)
+
+
 def test_window_covering_context_is_full_attention():
     a = check(tiny_swa(301))                       # positions 0..300: all of them
     b = check(dataclasses.replace(tiny_swa(301), dims=dataclasses.replace(tiny_swa(301).dims,
